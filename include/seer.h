@@ -1,0 +1,247 @@
+/*
+ * seer.h -- C ABI of the Seer hot path on MI355X (gfx950).
+ *
+ * Seer ("Seeing the End at Step Zero") shortens the fixed generation window
+ * of a diffusion multimodal LLM: at denoising step 0 the MLP of an early layer
+ * exposes, per window position, a near-zero activation count; an SNR
+ * jump/plateau test on that count finds where the semantic text ends; the
+ * suffix is cut once and every later layer and step runs on the shorter,
+ * compacted batch (Sec. 3.2-3.5 of the paper).
+ *
+ * Entry points (all asynchronous on the given HIP stream):
+ *   seer_prepack_weights       one-time weight layout for the layer kernels
+ *   seer_layer_forward_varlen  one bidirectional transformer layer over
+ *                              packed variable-length sequences, with the
+ *                              optional fused near-zero activation count
+ *   seer_step0_detect          the SNR boundary criterion per sequence
+ *   seer_batch_repack          padding-waste-aware routing plus compaction
+ *
+ * Conventions shared by every call:
+ *   - Buffers are owned by the caller.  Pointers are device pointers unless a
+ *     parameter says "host".  The library never allocates or frees caller
+ *     memory; layer scratch comes from a caller workspace sized by
+ *     seer_layer_workspace_bytes().
+ *   - Row-major everywhere.  Weights use the [out, in] layout (input features
+ *     contiguous).  Element type is given by seer_dims.dtype: bf16 (raw
+ *     16-bit brain-float bits) or fp32.  Counts, offsets and lengths are int32.
+ *   - Packed sequences: sequence b occupies rows [cu_seqlens[b], cu_seqlens[b+1])
+ *     of a row buffer; cu_seqlens[0] == 0 and the array is non-decreasing.
+ *     cu_seqlens lives in device memory and is read by the kernels, so the
+ *     host never needs the real row count: it passes an upper bound that
+ *     sizes the launch grids.
+ *   - Return value: 0 on success, a negative SEER_E* code otherwise.  On error
+ *     nothing is launched and seer_last_error() (per host thread) describes
+ *     the problem.  Errors detected on the device (a buffer too small for the
+ *     routed layout) are reported through seer_route_ctrl.status.
+ *   - Outputs are valid once the stream reaches the point of the call.
+ *     Calls on distinct streams with distinct workspaces may run concurrently.
+ */
+#ifndef SEER_H_
+#define SEER_H_
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---- status codes ------------------------------------------------------ */
+#define SEER_OK            0
+#define SEER_EINVAL       -1   /* bad argument (null pointer, bad size, ...) */
+#define SEER_EUNSUPPORTED -2   /* shape or dtype this build has no kernel for */
+#define SEER_EWORKSPACE   -3   /* workspace or destination buffer too small */
+#define SEER_EHIP         -4   /* a HIP runtime call failed */
+
+/* ---- element types ----------------------------------------------------- */
+#define SEER_DTYPE_BF16 1
+#define SEER_DTYPE_F32  2
+
+/* Layer geometry.  d_model = n_heads * head_dim.
+ * bf16 kernels need d_model % 256 == 0, d_ff % 128 == 0, head_dim == 128.
+ * fp32 kernels accept any d_model, d_ff and head_dim <= 128 (head_dim % 4 == 0). */
+typedef struct seer_dims {
+  int32_t d_model;
+  int32_t n_heads;
+  int32_t head_dim;
+  int32_t d_ff;        /* SwiGLU intermediate size I */
+  int32_t dtype;       /* SEER_DTYPE_* */
+  float rms_eps;       /* RMSNorm epsilon (1e-5 for the LLaDA-shaped layer) */
+} seer_dims;
+
+/* Source weights of one layer (device pointers, dtype = dims.dtype, [out, in]):
+ * wq, wk, wv, wo [d, d]; wg, wu [I, d]; wd [d, I].  g1, g2: fp32 RMSNorm gains
+ * [d] before attention and before the MLP, or NULL for unit gains. */
+typedef struct seer_layer_weights {
+  const void* wq;
+  const void* wk;
+  const void* wv;
+  const void* wo;
+  const void* wg;
+  const void* wu;
+  const void* wd;
+  const float* g1;
+  const float* g2;
+} seer_layer_weights;
+
+/* Size in bytes of the prepacked weights of one layer. */
+size_t seer_prepacked_bytes(const seer_dims* dims);
+
+/* Repack one layer's weights into the kernels' layout in `dst` (device,
+ * seer_prepacked_bytes() bytes, 256-byte aligned): q/k/v stacked, gate and up
+ * rows interleaved in blocks of 32 so that one tile holds matching gate and
+ * up columns, and the RMSNorm gains folded into the input columns of the
+ * projections they feed (exact for unit gains).  The source is not modified. */
+int seer_prepack_weights(const seer_dims* dims, const seer_layer_weights* src,
+                         void* dst, size_t dst_bytes, hipStream_t stream);
+
+/* Workspace bytes needed by seer_layer_forward_varlen for up to max_rows
+ * packed rows (qkv, attention output, post-attention residual, SwiGLU
+ * activations and two per-row RMS statistics). */
+size_t seer_layer_workspace_bytes(const seer_dims* dims, int32_t max_rows);
+
+/* Byte offsets of the intermediates that the last seer_layer_forward_varlen
+ * call on a workspace left there, for a call made with total_rows_ub ==
+ * max_rows (the layout depends on that bound).  Element type dims.dtype
+ * unless noted:
+ *   offsets[0] qkv  [max_rows, 3*d_model]   q | k | v after the folded RMSNorm
+ *   offsets[1] o    [max_rows, d_model]     attention output (pre projection)
+ *   offsets[2] h1   [max_rows, d_model]     x + o Wo^T
+ *   offsets[3] act  [max_rows, d_ff]        silu(gate) * up
+ *   offsets[4] fp32 [max_rows]              1/rms of x
+ *   offsets[5] fp32 [max_rows]              1/rms of h1
+ * Rows [0, cu_seqlens[batch]) of the last call are valid.  Meant for
+ * inspection and teacher-forced checks.  Errors: EINVAL, EUNSUPPORTED. */
+int seer_layer_workspace_offsets(const seer_dims* dims, int32_t max_rows, size_t offsets[6]);
+
+/* One bidirectional transformer layer over packed sequences: the work every
+ * denoising step repeats for every position of the window (Sec. 3.1):
+ *     a   = RMSNorm(x) * g1;   q,k,v = a Wq^T, a Wk^T, a Wv^T
+ *     o   = per head softmax(q k^T / sqrt(head_dim)) v, over all keys of the
+ *           same sequence (no causal mask, Sec. 3.6 attention equations)
+ *     h1  = x + o Wo^T
+ *     b   = RMSNorm(h1) * g2;  act = silu(b Wg^T) * (b Wu^T)
+ *     y   = h1 + act Wd^T
+ * x_in, x_out: [total_rows_ub, d_model] rows (may not alias).  Only rows
+ * [0, cu_seqlens[batch]) are read and written.
+ * seqused: optional [batch]; when given, rows at index >= seqused[b] inside
+ * sequence b are padding: they are masked as keys (the attention-mask rewrite
+ * of the static-bucket path, Sec. 3.5) and receive no attention output.
+ * act_count: optional [total_rows_ub] int32; when non-NULL the call zeroes it
+ * and stores, per row, the number of SwiGLU activations with
+ * |act| < act_eps (strict), counted on the fp32 values before rounding --
+ * the per-position MLP sparsity statistic of Sec. 3.2-3.3.
+ * workspace: >= seer_layer_workspace_bytes(dims, total_rows_ub) bytes,
+ * 256-byte aligned.  Errors: EINVAL (null pointers, batch < 1,
+ * total_rows_ub < 1), EUNSUPPORTED (dims), EWORKSPACE. */
+int seer_layer_forward_varlen(const seer_dims* dims, const void* w_packed,
+                              const void* x_in, void* x_out, int32_t total_rows_ub,
+                              const int32_t* cu_seqlens, const int32_t* seqused,
+                              int32_t batch, float act_eps, int32_t* act_count,
+                              void* workspace, size_t workspace_bytes,
+                              hipStream_t stream);
+
+/* SNR criterion parameters as exact rationals: tau_jump = tau_num/tau_den,
+ * gamma = gamma_num/gamma_den; lookahead = size of the window W_i.
+ * The paper's defaults are {3, 100, 3, 5, 3}. */
+typedef struct seer_snr_params {
+  int32_t tau_num;
+  int32_t tau_den;
+  int32_t gamma_num;
+  int32_t gamma_den;
+  int32_t lookahead;
+} seer_snr_params;
+
+/* SNR-aware boundary detection (Sec. 3.3).  For sequence b the window counts
+ * are c_i = act_count[cu_seqlens[b] + win_off[b] + i], i in [0, win_len[b]),
+ * and s_i = c_i / d_ff.  The boundary is the first i in [1, win_len-lookahead]
+ * with  min(W_i) - s_{i-1} >= tau  and  max(W_i) - min(W_i) <= gamma * jump,
+ * evaluated exactly in 64-bit integers (tau_den*jump >= tau_num*d_ff and
+ * gamma_den*noise <= gamma_num*jump on the counts).  Outputs per sequence:
+ * boundary[b] = i* (win_len[b] when no position qualifies) and
+ * keep_len[b] = min(i* + 1, win_len[b]) (one extra token is kept).
+ * Errors: EINVAL (null pointers, batch < 1, d_ff < 1, denominators < 1,
+ * lookahead < 1, negative numerators). */
+int seer_step0_detect(const int32_t* act_count, const int32_t* cu_seqlens,
+                      const int32_t* win_off, const int32_t* win_len, int32_t batch,
+                      int32_t d_ff, const seer_snr_params* params,
+                      int32_t* boundary, int32_t* keep_len, hipStream_t stream);
+
+/* Routing policies (Sec. 3.4 and the system study of Sec. 4):
+ * HYBRID = three-tier Static / Varlen / Eager routing by padding waste ratio;
+ * NAIVE_PAD = every sequence padded to the bucket of the batch-max length;
+ * VARLEN_ONLY = every sequence packed without padding. */
+#define SEER_ROUTE_HYBRID      0
+#define SEER_ROUTE_NAIVE_PAD   1
+#define SEER_ROUTE_VARLEN_ONLY 2
+
+/* Paths written to route[b*3+0]. */
+#define SEER_PATH_STATIC 0
+#define SEER_PATH_VARLEN 1
+#define SEER_PATH_EAGER  2
+
+typedef struct seer_repack_desc {
+  int32_t policy;            /* SEER_ROUTE_* */
+  int32_t tau_pad_num;       /* static path iff rho <= tau_pad_num/tau_pad_den */
+  int32_t tau_pad_den;       /*   (paper default 1/5) */
+  int32_t granule;           /* packed capacity rounded up to a multiple (>= 1) */
+  int32_t row_bytes;         /* bytes per row, a positive multiple of 16 */
+  int32_t dst_capacity_rows; /* rows available in every dst buffer */
+  int32_t max_batch_hint;    /* unused, 0 */
+  int32_t reserved;
+} seer_repack_desc;
+
+/* Control word written by seer_batch_repack: the routed shape of the batch,
+ * so a host can pick the launch configuration of the next steps without
+ * waiting for the data tensors (Sec. 3.5).  `ready` is written last. */
+typedef struct seer_route_ctrl {
+  int32_t total_rows;        /* cu_dst[batch] */
+  int32_t capacity_rows;     /* total_rows rounded up to the granule */
+  int32_t n_static;
+  int32_t n_varlen;
+  int32_t n_eager;
+  int32_t n_groups;
+  int32_t max_alloc;         /* largest per-sequence window allocation */
+  int32_t status;            /* 0 ok, SEER_EWORKSPACE if dst was too small */
+  int32_t ready;             /* 1 once the fields above are final */
+  int32_t reserved[7];
+} seer_route_ctrl;
+
+/* Routing + in-GPU compaction (Sec. 3.4-3.5), one launch, no host sync.
+ * Route: bucket(L) = smallest of {8,16,32,...} u {N_max} that is >= L
+ * (N_max = max_b win_len[b]); sequences fall in coarse classes
+ * k = ceil(log4 max(L,8)), one group per class; a group G with bucket B_G has
+ * padding waste rho = 1 - sum L / (|G| B_G); path = eager if |G| == 1 or
+ * max L <= 4, else static if rho <= tau_pad, else varlen.  route[b*3+0] =
+ * path, route[b*3+1] = group id (ascending class order), route[b*3+2] =
+ * rows allocated to the window (B_G on the static path, keep_len otherwise).
+ * Compaction, for each of the n_buffers (src[i] -> dst[i]) pairs (host
+ * arrays of device pointers, rows of desc->row_bytes bytes, src laid out by
+ * cu_src): sequence b's first win_off[b] + keep_len[b] rows are copied to
+ * rows [cu_dst[b], ...) and the rest of its allocation is zero-filled;
+ * cu_dst[b+1] = cu_dst[b] + win_off[b] + alloc_b; seqused[b] =
+ * win_off[b] + keep_len[b]; rows [cu_dst[batch], capacity) are zero-filled.
+ * Order of sequences is preserved.  ctrl_dev (device) and ctrl_host
+ * (host-pinned, hipHostMalloc'ed) are optional.  If the routed capacity
+ * exceeds desc->dst_capacity_rows, nothing is copied, cu_dst is all zero and
+ * ctrl.status = SEER_EWORKSPACE.  Errors: EINVAL (null pointers, batch < 1,
+ * n_buffers < 1, bad desc fields). */
+int seer_batch_repack(const seer_repack_desc* desc, const void* const* src,
+                      void* const* dst, int32_t n_buffers, const int32_t* cu_src,
+                      const int32_t* win_off, const int32_t* win_len,
+                      const int32_t* keep_len, int32_t batch, int32_t* cu_dst,
+                      int32_t* seqused, int32_t* route, seer_route_ctrl* ctrl_dev,
+                      seer_route_ctrl* ctrl_host, hipStream_t stream);
+
+/* Description of the last error on the calling host thread ("" if none). */
+const char* seer_last_error(void);
+
+/* ABI version of this library (major * 100 + minor). */
+int32_t seer_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SEER_H_ */

@@ -1,0 +1,255 @@
+// Variable-length bidirectional attention on gfx950 matrix cores (bf16, head_dim 128).
+//
+// Every query of a sequence attends to every key of the same sequence -- no
+// causal mask (the denoising step sees the whole window, Sec. 3.1; logits
+// q.k / sqrt(head_dim) and a softmax over the sequence, Sec. 3.6).  Keys at
+// positions >= seqused[b] are masked and those query rows get a zero output
+// (the static-bucket padding of Sec. 3.5).
+//
+// Design: one workgroup = (sequence, 128-query tile, head); four waves of 32
+// queries.  K and V tiles of 64 keys are staged in LDS and shared by the four
+// waves.  Scores are computed transposed, S^T = K Q^T (32x32x16 bf16 MFMA), so
+// that each lane owns one query column: the online-softmax statistics are
+// per-lane values and the probabilities already sit in the B-operand layout
+// of the next product O^T = V^T P^T -- no shuffle of P through LDS.  V is
+// transposed while it is written to LDS, with keys permuted inside each group
+// of 16 so that every lane's eight keys are one 16-byte read.
+#include <math.h>
+
+#include "common.h"
+#include "kernels.h"
+
+namespace seer {
+
+namespace {
+
+constexpr int QT = 128;   // queries per workgroup
+constexpr int KT = 64;    // keys per LDS tile
+constexpr int DH = 128;   // head dim
+constexpr int NT = 256;
+constexpr int K_ROW = DH * 2;   // 256 bytes per key row of K
+constexpr int V_ROW = KT * 2;   // 128 bytes per dim row of V^T
+
+__device__ __forceinline__ int swz8(int r) { return (r & 7) ^ ((r >> 3) & 1); }
+
+// Position of key k (0..63) inside a V^T row: within each 16-key group the
+// quads are stored in the order {0, 2, 1, 3}.
+__device__ __forceinline__ int vpos(int k) {
+  const int q = (k >> 2) & 3;
+  const int pq = ((q & 1) << 1) | (q >> 1);
+  return (k & ~15) | (pq << 2) | (k & 3);
+}
+
+}  // namespace
+
+__global__ __launch_bounds__(NT, 2) void attn_bf16_kernel(AttnParams p) {
+  __shared__ __attribute__((aligned(16))) uint8_t k_lds[KT * K_ROW];
+  __shared__ __attribute__((aligned(16))) uint8_t v_lds[DH * V_ROW];
+
+  // ---- which (sequence, query tile) this block owns -------------------------
+  int b = -1, t = 0;
+  {
+    int acc = 0;
+    const int j = blockIdx.x;
+    for (int s = 0; s < p.B; ++s) {
+      int len = p.cu[s + 1] - p.cu[s];
+      len = len < 0 ? 0 : len;
+      const int nt = (len + QT - 1) / QT;
+      if (j < acc + nt) { b = s; t = j - acc; break; }
+      acc += nt;
+    }
+  }
+  if (b < 0) return;
+  const int h = blockIdx.y;
+  const int s0 = p.cu[b];
+  if (s0 < 0 || s0 >= p.rows_ub) return;
+  int len = p.cu[b + 1] - s0;
+  len = len > p.rows_ub - s0 ? p.rows_ub - s0 : len;   // never touch rows past the bound
+  if (t * QT >= len) return;
+  int used = p.used ? p.used[b] : len;
+  used = used < 0 ? 0 : (used > len ? len : used);
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int fr = lane & 31;
+  const int fhalf = lane >> 5;
+  const size_t ld = (size_t)3 * p.d;
+  const uint16_t* qkv = static_cast<const uint16_t*>(p.qkv);
+  uint16_t* out = static_cast<uint16_t*>(p.out);
+
+  const int q_row = t * QT + wave * 32 + fr;            // query row inside the sequence
+  const int q_src = q_row < len ? q_row : len - 1;
+
+  // Q as the B operand of S^T = K Q^T: lane holds query fr, dims 16*ks + 8*fhalf .. +8.
+  bf16x8_t qf[8];
+  {
+    const uint16_t* qp = qkv + (size_t)(s0 + q_src) * ld + h * DH + fhalf * 8;
+#pragma unroll
+    for (int ks = 0; ks < 8; ++ks) qf[ks] = as_bf16x8(*reinterpret_cast<const uint4*>(qp + ks * 16));
+  }
+
+  f32x16_t o[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) o[i][r] = 0.0f;
+  float m_run = -INFINITY;
+  float l_run = 0.0f;
+  const float c = p.scale * 1.4426950408889634f;
+
+  // ---- K/V tile staging -------------------------------------------------------
+  // K: thread loads 16-byte chunks id = tid + 256*i: key id/16, dim chunk id%16.
+  // V: thread loads keys 4*(tid/16) .. +3 at dim chunk tid%16, transposes 4x8.
+  uint4 kreg[4], vreg[4];
+  const int vkq = tid >> 4;
+  const int vdc = tid & 15;
+  auto load_tile = [&](int kbase) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int id = tid + NT * i;
+      int key = kbase + (id >> 4);
+      key = key < used ? key : used - 1;
+      kreg[i] = *reinterpret_cast<const uint4*>(qkv + (size_t)(s0 + key) * ld + p.d + h * DH + (id & 15) * 8);
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      int key = kbase + vkq * 4 + i;
+      key = key < used ? key : used - 1;
+      vreg[i] = *reinterpret_cast<const uint4*>(qkv + (size_t)(s0 + key) * ld + 2 * p.d + h * DH + vdc * 8);
+    }
+  };
+  auto store_tile = [&]() {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int id = tid + NT * i;
+      const int key = id >> 4;
+      const int ch = (id & 15) ^ (key & 15);
+      *reinterpret_cast<uint4*>(k_lds + key * K_ROW + ch * 16) = kreg[i];
+    }
+    const uint32_t* w = reinterpret_cast<const uint32_t*>(vreg);  // w[4*i + e/2] = key i, dims e, e+1
+    const int pos = vpos(vkq * 4);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int sh = (e & 1) * 16;
+      const uint32_t k0 = (w[0 * 4 + e / 2] >> sh) & 0xffffu;
+      const uint32_t k1 = (w[1 * 4 + e / 2] >> sh) & 0xffffu;
+      const uint32_t k2 = (w[2 * 4 + e / 2] >> sh) & 0xffffu;
+      const uint32_t k3 = (w[3 * 4 + e / 2] >> sh) & 0xffffu;
+      const int dim = vdc * 8 + e;
+      const int ch = (pos >> 3) ^ swz8(dim);
+      uint2 v;
+      v.x = k0 | (k1 << 16);
+      v.y = k2 | (k3 << 16);
+      *reinterpret_cast<uint2*>(v_lds + dim * V_ROW + ch * 16 + (pos & 7) * 2) = v;
+    }
+  };
+
+  const int n_kv = (used + KT - 1) / KT;
+  if (n_kv > 0) {
+    load_tile(0);
+    store_tile();
+  }
+  __syncthreads();
+  for (int kt = 0; kt < n_kv; ++kt) {
+    const int kbase = kt * KT;
+    if (kt + 1 < n_kv) load_tile(kbase + KT);
+
+    // S^T for 64 keys: two 32-key MFMA row tiles.
+    f32x16_t s[2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) s[i][r] = 0.0f;
+      const int key = i * 32 + fr;
+#pragma unroll
+      for (int ks = 0; ks < 8; ++ks) {
+        const int ch = (2 * ks + fhalf) ^ (key & 15);
+        const bf16x8_t kf = as_bf16x8(*reinterpret_cast<const uint4*>(k_lds + key * K_ROW + ch * 16));
+        s[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ks], s[i], 0, 0, 0);
+      }
+    }
+    // mask, running max
+    float mt = -INFINITY;
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int key = kbase + i * 32 + (r >> 2) * 8 + fhalf * 4 + (r & 3);
+        if (key >= used) s[i][r] = -INFINITY;
+        mt = fmaxf(mt, s[i][r]);
+      }
+    mt = fmaxf(mt, __shfl_xor(mt, 32, kWave));
+    const float m_new = fmaxf(m_run, mt);
+    const float alpha = exp2f((m_run - m_new) * c);
+    m_run = m_new;
+    const float mc = m_new * c;
+    float lsum = 0.0f;
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const float e = exp2f(s[i][r] * c - mc);
+        s[i][r] = e;
+        lsum += e;
+      }
+    l_run = l_run * alpha + lsum;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) o[i][r] *= alpha;
+
+    // O^T += V^T P^T over four 16-key slices.
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+#pragma unroll
+      for (int hf = 0; hf < 2; ++hf) {
+        uint4 pk;
+        pk.x = pack_bf2(s[i][hf * 8 + 0], s[i][hf * 8 + 1]);
+        pk.y = pack_bf2(s[i][hf * 8 + 2], s[i][hf * 8 + 3]);
+        pk.z = pack_bf2(s[i][hf * 8 + 4], s[i][hf * 8 + 5]);
+        pk.w = pack_bf2(s[i][hf * 8 + 6], s[i][hf * 8 + 7]);
+        const bf16x8_t pf = as_bf16x8(pk);
+        const int chunk = i * 4 + hf * 2 + fhalf;
+#pragma unroll
+        for (int dt = 0; dt < 4; ++dt) {
+          const int dim = dt * 32 + fr;
+          const int ch = chunk ^ swz8(dim);
+          const bf16x8_t vf = as_bf16x8(*reinterpret_cast<const uint4*>(v_lds + dim * V_ROW + ch * 16));
+          o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf, o[dt], 0, 0, 0);
+        }
+      }
+    }
+    __syncthreads();
+    if (kt + 1 < n_kv) {
+      store_tile();
+      __syncthreads();
+    }
+  }
+
+  // ---- normalise and store ----------------------------------------------------
+  const float l_tot = l_run + __shfl_xor(l_run, 32, kWave);
+  if (q_row < len) {
+    const bool real = q_row < used;
+    const float inv = (real && l_tot > 0.0f) ? 1.0f / l_tot : 0.0f;
+    uint16_t* op = out + (size_t)(s0 + q_row) * p.d + h * DH + fhalf * 4;
+#pragma unroll
+    for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        uint2 v;
+        v.x = pack_bf2(o[dt][g * 4 + 0] * inv, o[dt][g * 4 + 1] * inv);
+        v.y = pack_bf2(o[dt][g * 4 + 2] * inv, o[dt][g * 4 + 3] * inv);
+        *reinterpret_cast<uint2*>(op + dt * 32 + g * 8) = v;
+      }
+  }
+}
+
+int launch_attn_bf16(const AttnParams& p, hipStream_t s) {
+  if (p.head_dim != DH) return -1;
+  dim3 grid((p.rows_ub + QT - 1) / QT + p.B, p.n_heads), block(NT);
+  hipLaunchKernelGGL(attn_bf16_kernel, grid, block, 0, s, p);
+  return hipGetLastError() == hipSuccess ? 0 : -1;
+}
+
+}  // namespace seer

@@ -1,0 +1,113 @@
+// Internal launchers of the Seer layer library (not part of the public ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace seer {
+
+enum Epilogue { EPI_SCALE = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_SWIGLU_COUNT = 3 };
+
+// C[M,N] = A[M,K] * B[N,K]^T with a fused epilogue.  M is read on the device
+// from m_ptr (clamped to m_ub, the bound the grid is sized from).
+struct GemmParams {
+  const void* A;
+  const void* B;
+  void* C;
+  const void* R;      // residual rows (RESID), same element type as C
+  const float* rs;    // per-row scale (SCALE, SWIGLU*)
+  int* cnt;           // per-row near-zero count (SWIGLU_COUNT)
+  float eps;
+  const int* m_ptr;
+  int m_ub;
+  int N;
+  int K;
+  int lda, ldb, ldc, ldr;
+  // fp32 SwiGLU only: the up-projection weight as a second [N, K] operand
+  const void* B2;
+};
+
+// bf16 operands; requires N % 256 == 0, K % 64 == 0, 16-byte aligned rows.
+// For SWIGLU*, N is the packed 2*I and C has I columns.
+int launch_gemm_bf16(int epi, const GemmParams& p, hipStream_t s);
+
+// fp32 operands, any N and K.  For SWIGLU*, B = Wg, B2 = Wu, both [N=I, K].
+int launch_gemm_f32(int epi, const GemmParams& p, hipStream_t s);
+
+// inv_rms[r] = 1 / sqrt(mean_j x[r,j]^2 + eps) for r < M.
+int launch_rms_inv(bool bf16, const void* x, int ld, int d, const int* m_ptr, int m_ub,
+                   float eps, float* out, hipStream_t s);
+
+struct AttnParams {
+  const void* qkv;       // [T, 3d]: q | k | v, head h at columns h*dh of each
+  void* out;             // [T, d]
+  const int* cu;         // [B+1]
+  const int* used;       // [B] or null
+  int B;
+  int d;
+  int n_heads;
+  int head_dim;
+  int rows_ub;           // bound on cu[B] (sizes the grid)
+  float scale;           // 1/sqrt(head_dim)
+};
+
+int launch_attn_bf16(const AttnParams& p, hipStream_t s);
+int launch_attn_f32(const AttnParams& p, hipStream_t s);
+
+// Zero an int32 array of n entries.
+int launch_zero_i32(int* p, int n, hipStream_t s);
+
+struct DetectParams {
+  const int* cnt;
+  const int* cu;
+  const int* win_off;
+  const int* win_len;
+  int B;
+  int d_ff;
+  int tau_num, tau_den, gamma_num, gamma_den, lookahead;
+  int* boundary;
+  int* keep_len;
+};
+int launch_detect(const DetectParams& p, hipStream_t s);
+
+constexpr int kRepackMaxBatch = 1024;
+constexpr int kRepackMaxBuffers = 4;
+
+struct RepackParams {
+  const uint8_t* src[kRepackMaxBuffers];
+  uint8_t* dst[kRepackMaxBuffers];
+  int n_buffers;
+  const int* cu_src;
+  const int* win_off;
+  const int* win_len;
+  const int* keep_len;
+  int B;
+  int policy;
+  int tau_num, tau_den;
+  int granule;
+  int row_bytes;
+  int dst_capacity_rows;
+  int* cu_dst;
+  int* seqused;
+  int* route;
+  int* ctrl_dev;    // seer_route_ctrl as int[16]
+  int* ctrl_host;
+};
+int launch_repack(const RepackParams& p, hipStream_t s);
+
+struct PrepackParams {
+  const void* wq; const void* wk; const void* wv; const void* wo;
+  const void* wg; const void* wu; const void* wd;
+  const float* g1; const float* g2;
+  void* dst;
+  int d, d_ff;
+  bool bf16;
+};
+// Offsets (in elements) of the packed blocks.
+struct PackedLayout {
+  size_t qkv, o, gu, dn, total_bytes;
+};
+PackedLayout packed_layout(int d, int d_ff, bool bf16);
+int launch_prepack(const PrepackParams& p, hipStream_t s);
+
+}  // namespace seer

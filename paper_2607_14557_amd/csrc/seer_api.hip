@@ -1,0 +1,288 @@
+// C ABI of the Seer hot path: argument checks, workspace layout and the launch
+// sequence of each entry point.  Kernels live in gemm_bf16.hip, attn_bf16.hip,
+// f32_kernels.hip and rows.hip.
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+
+#include <string>
+
+#include "../../include/seer.h"
+#include "kernels.h"
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return code;
+}
+
+int ok() {
+  g_err.clear();
+  return SEER_OK;
+}
+
+int hip_fail(const char* what) {
+  const hipError_t e = hipGetLastError();
+  return fail(SEER_EHIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+size_t up256(size_t n) { return (n + 255) / 256 * 256; }
+
+int check_dims(const seer_dims* d) {
+  if (!d) return fail(SEER_EINVAL, "dims is NULL");
+  if (d->d_model <= 0 || d->n_heads <= 0 || d->head_dim <= 0 || d->d_ff <= 0)
+    return fail(SEER_EINVAL, "dims must be positive (d_model=%d n_heads=%d head_dim=%d d_ff=%d)",
+                d->d_model, d->n_heads, d->head_dim, d->d_ff);
+  if (d->n_heads * d->head_dim != d->d_model)
+    return fail(SEER_EINVAL, "n_heads * head_dim (%d) != d_model (%d)", d->n_heads * d->head_dim,
+                d->d_model);
+  if (!(d->rms_eps >= 0.0f) || !isfinite(d->rms_eps)) return fail(SEER_EINVAL, "rms_eps must be finite and >= 0");
+  if (d->dtype == SEER_DTYPE_BF16) {
+    if (d->d_model % 256 != 0 || d->d_ff % 128 != 0 || d->head_dim != 128)
+      return fail(SEER_EUNSUPPORTED,
+                  "bf16 kernels need d_model %% 256 == 0, d_ff %% 128 == 0, head_dim == 128 "
+                  "(got %d, %d, %d)", d->d_model, d->d_ff, d->head_dim);
+  } else if (d->dtype == SEER_DTYPE_F32) {
+    if (d->head_dim > 128) return fail(SEER_EUNSUPPORTED, "fp32 attention needs head_dim <= 128");
+  } else {
+    return fail(SEER_EUNSUPPORTED, "unknown dtype %d", d->dtype);
+  }
+  return SEER_OK;
+}
+
+struct WsLayout {
+  size_t qkv, o, h1, act, inv1, inv2, total;
+};
+
+WsLayout ws_layout(const seer_dims* d, int rows) {
+  const size_t es = d->dtype == SEER_DTYPE_BF16 ? 2 : 4;
+  const size_t R = (size_t)(rows > 0 ? rows : 0);
+  WsLayout L;
+  size_t off = 0;
+  L.qkv = off; off = up256(off + R * 3 * d->d_model * es);
+  L.o = off;   off = up256(off + R * d->d_model * es);
+  L.h1 = off;  off = up256(off + R * d->d_model * es);
+  L.act = off; off = up256(off + R * d->d_ff * es);
+  L.inv1 = off; off = up256(off + R * 4);
+  L.inv2 = off; off = up256(off + R * 4);
+  L.total = off;
+  return L;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* seer_last_error(void) { return g_err.c_str(); }
+
+int32_t seer_abi_version(void) { return 100; }
+
+size_t seer_prepacked_bytes(const seer_dims* dims) {
+  if (check_dims(dims) != SEER_OK) return 0;
+  return seer::packed_layout(dims->d_model, dims->d_ff, dims->dtype == SEER_DTYPE_BF16).total_bytes;
+}
+
+int seer_prepack_weights(const seer_dims* dims, const seer_layer_weights* src, void* dst,
+                         size_t dst_bytes, hipStream_t stream) {
+  int rc = check_dims(dims);
+  if (rc) return rc;
+  if (!src || !dst) return fail(SEER_EINVAL, "src/dst is NULL");
+  if (!src->wq || !src->wk || !src->wv || !src->wo || !src->wg || !src->wu || !src->wd)
+    return fail(SEER_EINVAL, "a weight pointer is NULL");
+  if (!aligned(dst, 256)) return fail(SEER_EINVAL, "dst must be 256-byte aligned");
+  const bool bf16 = dims->dtype == SEER_DTYPE_BF16;
+  const size_t need = seer::packed_layout(dims->d_model, dims->d_ff, bf16).total_bytes;
+  if (dst_bytes < need) return fail(SEER_EWORKSPACE, "dst holds %zu bytes, need %zu", dst_bytes, need);
+  seer::PrepackParams p{};
+  p.wq = src->wq; p.wk = src->wk; p.wv = src->wv; p.wo = src->wo;
+  p.wg = src->wg; p.wu = src->wu; p.wd = src->wd;
+  p.g1 = src->g1; p.g2 = src->g2;
+  p.dst = dst;
+  p.d = dims->d_model;
+  p.d_ff = dims->d_ff;
+  p.bf16 = bf16;
+  if (seer::launch_prepack(p, stream)) return hip_fail("prepack launch");
+  return ok();
+}
+
+size_t seer_layer_workspace_bytes(const seer_dims* dims, int32_t max_rows) {
+  if (check_dims(dims) != SEER_OK || max_rows < 0) return 0;
+  return ws_layout(dims, max_rows).total;
+}
+
+int seer_layer_workspace_offsets(const seer_dims* dims, int32_t max_rows, size_t offsets[6]) {
+  int rc = check_dims(dims);
+  if (rc) return rc;
+  if (!offsets || max_rows < 0) return fail(SEER_EINVAL, "offsets is NULL or max_rows < 0");
+  const WsLayout L = ws_layout(dims, max_rows);
+  offsets[0] = L.qkv; offsets[1] = L.o; offsets[2] = L.h1;
+  offsets[3] = L.act; offsets[4] = L.inv1; offsets[5] = L.inv2;
+  return ok();
+}
+
+int seer_layer_forward_varlen(const seer_dims* dims, const void* w_packed, const void* x_in,
+                              void* x_out, int32_t total_rows_ub, const int32_t* cu_seqlens,
+                              const int32_t* seqused, int32_t batch, float act_eps,
+                              int32_t* act_count, void* workspace, size_t workspace_bytes,
+                              hipStream_t stream) {
+  int rc = check_dims(dims);
+  if (rc) return rc;
+  if (!w_packed || !x_in || !x_out || !cu_seqlens || !workspace)
+    return fail(SEER_EINVAL, "a required pointer is NULL");
+  if (batch < 1) return fail(SEER_EINVAL, "batch must be >= 1 (got %d)", batch);
+  if (total_rows_ub < 1) return fail(SEER_EINVAL, "total_rows_ub must be >= 1 (got %d)", total_rows_ub);
+  if (x_in == x_out) return fail(SEER_EINVAL, "x_in and x_out may not alias");
+  if (act_count && !(act_eps >= 0.0f)) return fail(SEER_EINVAL, "act_eps must be >= 0");
+  const bool bf16 = dims->dtype == SEER_DTYPE_BF16;
+  if (bf16 && (!aligned(w_packed, 256) || !aligned(x_in, 16) || !aligned(x_out, 16)))
+    return fail(SEER_EINVAL, "bf16 weights need 256-byte and rows 16-byte alignment");
+  if (!aligned(workspace, 256)) return fail(SEER_EINVAL, "workspace must be 256-byte aligned");
+  const WsLayout L = ws_layout(dims, total_rows_ub);
+  if (workspace_bytes < L.total)
+    return fail(SEER_EWORKSPACE, "workspace holds %zu bytes, need %zu", workspace_bytes, L.total);
+
+  const int d = dims->d_model, I = dims->d_ff, R = total_rows_ub;
+  uint8_t* ws = static_cast<uint8_t*>(workspace);
+  void* qkv = ws + L.qkv;
+  void* o = ws + L.o;
+  void* h1 = ws + L.h1;
+  void* act = ws + L.act;
+  float* inv1 = reinterpret_cast<float*>(ws + L.inv1);
+  float* inv2 = reinterpret_cast<float*>(ws + L.inv2);
+  const int* m_ptr = cu_seqlens + batch;
+  const seer::PackedLayout P = seer::packed_layout(d, I, bf16);
+  const size_t es = bf16 ? 2 : 4;
+  const uint8_t* wb = static_cast<const uint8_t*>(w_packed);
+  auto gemm = bf16 ? seer::launch_gemm_bf16 : seer::launch_gemm_f32;
+
+  // 1. RMSNorm statistics of the layer input
+  if (seer::launch_rms_inv(bf16, x_in, d, d, m_ptr, R, dims->rms_eps, inv1, stream))
+    return hip_fail("rms launch");
+  // 2. QKV projection, RMSNorm folded in as a row scale
+  {
+    seer::GemmParams g{};
+    g.A = x_in; g.B = wb + P.qkv * es; g.C = qkv; g.rs = inv1;
+    g.m_ptr = m_ptr; g.m_ub = R; g.N = 3 * d; g.K = d;
+    g.lda = d; g.ldb = d; g.ldc = 3 * d;
+    if (gemm(seer::EPI_SCALE, g, stream)) return hip_fail("qkv gemm launch");
+  }
+  // 3. bidirectional varlen attention
+  {
+    seer::AttnParams a{};
+    a.qkv = qkv; a.out = o; a.cu = cu_seqlens; a.used = seqused; a.B = batch;
+    a.d = d; a.n_heads = dims->n_heads; a.head_dim = dims->head_dim; a.rows_ub = R;
+    a.scale = 1.0f / sqrtf((float)dims->head_dim);
+    if ((bf16 ? seer::launch_attn_bf16(a, stream) : seer::launch_attn_f32(a, stream)))
+      return hip_fail("attention launch");
+  }
+  // 4. output projection + residual
+  {
+    seer::GemmParams g{};
+    g.A = o; g.B = wb + P.o * es; g.C = h1; g.R = x_in;
+    g.m_ptr = m_ptr; g.m_ub = R; g.N = d; g.K = d;
+    g.lda = d; g.ldb = d; g.ldc = d; g.ldr = d;
+    if (gemm(seer::EPI_RESID, g, stream)) return hip_fail("o gemm launch");
+  }
+  // 5. RMSNorm statistics before the MLP
+  if (seer::launch_rms_inv(bf16, h1, d, d, m_ptr, R, dims->rms_eps, inv2, stream))
+    return hip_fail("rms launch");
+  // 6. gate/up projection + SwiGLU (+ near-zero count)
+  {
+    if (act_count && seer::launch_zero_i32(act_count, R, stream)) return hip_fail("zero launch");
+    seer::GemmParams g{};
+    g.A = h1; g.C = act; g.rs = inv2; g.cnt = act_count; g.eps = act_eps;
+    g.m_ptr = m_ptr; g.m_ub = R; g.K = d; g.lda = d; g.ldb = d; g.ldc = I;
+    if (bf16) {
+      g.B = wb + P.gu * es;
+      g.N = 2 * I;
+    } else {
+      g.B = wb + P.gu * es;
+      g.B2 = wb + (P.gu + (size_t)I * d) * es;
+      g.N = I;
+    }
+    if (gemm(act_count ? seer::EPI_SWIGLU_COUNT : seer::EPI_SWIGLU, g, stream))
+      return hip_fail("gate/up gemm launch");
+  }
+  // 7. down projection + residual
+  {
+    seer::GemmParams g{};
+    g.A = act; g.B = wb + P.dn * es; g.C = x_out; g.R = h1;
+    g.m_ptr = m_ptr; g.m_ub = R; g.N = d; g.K = I;
+    g.lda = I; g.ldb = I; g.ldc = d; g.ldr = d;
+    if (gemm(seer::EPI_RESID, g, stream)) return hip_fail("down gemm launch");
+  }
+  return ok();
+}
+
+int seer_step0_detect(const int32_t* act_count, const int32_t* cu_seqlens, const int32_t* win_off,
+                      const int32_t* win_len, int32_t batch, int32_t d_ff,
+                      const seer_snr_params* params, int32_t* boundary, int32_t* keep_len,
+                      hipStream_t stream) {
+  if (!act_count || !cu_seqlens || !win_off || !win_len || !params || !boundary || !keep_len)
+    return fail(SEER_EINVAL, "a required pointer is NULL");
+  if (batch < 1) return fail(SEER_EINVAL, "batch must be >= 1 (got %d)", batch);
+  if (d_ff < 1) return fail(SEER_EINVAL, "d_ff must be >= 1");
+  if (params->tau_den < 1 || params->gamma_den < 1 || params->tau_num < 0 || params->gamma_num < 0)
+    return fail(SEER_EINVAL, "tau/gamma must be non-negative rationals with positive denominators");
+  if (params->lookahead < 1) return fail(SEER_EINVAL, "lookahead must be >= 1");
+  seer::DetectParams p{};
+  p.cnt = act_count; p.cu = cu_seqlens; p.win_off = win_off; p.win_len = win_len;
+  p.B = batch; p.d_ff = d_ff;
+  p.tau_num = params->tau_num; p.tau_den = params->tau_den;
+  p.gamma_num = params->gamma_num; p.gamma_den = params->gamma_den;
+  p.lookahead = params->lookahead;
+  p.boundary = boundary; p.keep_len = keep_len;
+  if (seer::launch_detect(p, stream)) return hip_fail("detect launch");
+  return ok();
+}
+
+int seer_batch_repack(const seer_repack_desc* desc, const void* const* src, void* const* dst,
+                      int32_t n_buffers, const int32_t* cu_src, const int32_t* win_off,
+                      const int32_t* win_len, const int32_t* keep_len, int32_t batch,
+                      int32_t* cu_dst, int32_t* seqused, int32_t* route, seer_route_ctrl* ctrl_dev,
+                      seer_route_ctrl* ctrl_host, hipStream_t stream) {
+  if (!desc || !src || !dst || !cu_src || !win_off || !win_len || !keep_len || !cu_dst || !seqused ||
+      !route)
+    return fail(SEER_EINVAL, "a required pointer is NULL");
+  if (batch < 1 || batch > seer::kRepackMaxBatch)
+    return fail(batch < 1 ? SEER_EINVAL : SEER_EUNSUPPORTED, "batch must be in [1, %d] (got %d)",
+                seer::kRepackMaxBatch, batch);
+  if (n_buffers < 1 || n_buffers > seer::kRepackMaxBuffers)
+    return fail(SEER_EINVAL, "n_buffers must be in [1, %d]", seer::kRepackMaxBuffers);
+  if (desc->policy < 0 || desc->policy > 2) return fail(SEER_EINVAL, "unknown policy %d", desc->policy);
+  if (desc->tau_pad_den < 1 || desc->tau_pad_num < 0) return fail(SEER_EINVAL, "bad tau_pad");
+  if (desc->granule < 1) return fail(SEER_EINVAL, "granule must be >= 1");
+  if (desc->row_bytes < 16 || desc->row_bytes % 16) return fail(SEER_EINVAL, "row_bytes must be a positive multiple of 16");
+  if (desc->dst_capacity_rows < 0) return fail(SEER_EINVAL, "dst_capacity_rows must be >= 0");
+  seer::RepackParams p{};
+  for (int i = 0; i < n_buffers; ++i) {
+    if (!src[i] || !dst[i]) return fail(SEER_EINVAL, "buffer %d is NULL", i);
+    if (!aligned(src[i], 16) || !aligned(dst[i], 16)) return fail(SEER_EINVAL, "buffers must be 16-byte aligned");
+    if (src[i] == dst[i]) return fail(SEER_EINVAL, "src and dst may not alias");
+    p.src[i] = static_cast<const uint8_t*>(src[i]);
+    p.dst[i] = static_cast<uint8_t*>(dst[i]);
+  }
+  p.n_buffers = n_buffers;
+  p.cu_src = cu_src; p.win_off = win_off; p.win_len = win_len; p.keep_len = keep_len;
+  p.B = batch; p.policy = desc->policy;
+  p.tau_num = desc->tau_pad_num; p.tau_den = desc->tau_pad_den;
+  p.granule = desc->granule; p.row_bytes = desc->row_bytes;
+  p.dst_capacity_rows = desc->dst_capacity_rows;
+  p.cu_dst = cu_dst; p.seqused = seqused; p.route = route;
+  p.ctrl_dev = reinterpret_cast<int*>(ctrl_dev);
+  p.ctrl_host = reinterpret_cast<int*>(ctrl_host);
+  if (seer::launch_repack(p, stream)) return hip_fail("repack launch");
+  return ok();
+}
+
+}  // extern "C"

@@ -1,0 +1,114 @@
+"""Shared helpers of the GPU parity tests: device upload, error metrics.
+
+Nothing here computes any part of the method; the expected values always come
+from ``oracle`` on the same seeded inputs.
+"""
+import sys
+
+import numpy as np
+
+
+def log(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def torch_dt(dtype):
+    import torch
+    return torch.bfloat16 if dtype == "bf16" else torch.float32
+
+
+def dev(a, dtype=None):
+    """Upload a numpy array; float arrays go to the given dtype (bf16/f32)."""
+    import torch
+    a = np.ascontiguousarray(a)
+    if a.dtype.kind in "iu":
+        return torch.from_numpy(a.astype(np.int32)).cuda()
+    t = torch.from_numpy(a.astype(np.float32))
+    return t.to(torch_dt(dtype or "f32")).cuda()
+
+
+def host(t):
+    """Device tensor -> float64 / int64 numpy (exact upcast)."""
+    import torch
+    t = t.detach()
+    if t.dtype in (torch.int32, torch.int64, torch.int16, torch.uint8):
+        return t.cpu().numpy().astype(np.int64)
+    return t.float().cpu().numpy().astype(np.float64)
+
+
+def upload_weights(W, dtype):
+    return {k: (dev(v, dtype) if k not in ("g1", "g2") else dev(v, "f32")) for k, v in W.items()}
+
+
+def rel_err(got, ref):
+    """max |got - ref| / max(|ref|, rms(ref row)) over all elements."""
+    got = np.asarray(got, np.float64)
+    ref = np.asarray(ref, np.float64)
+    if ref.size == 0:
+        return 0.0
+    rms = np.sqrt(np.mean(ref * ref, axis=-1, keepdims=True))
+    den = np.maximum(np.abs(ref), rms)
+    den = np.where(den == 0, 1.0, den)
+    return float(np.max(np.abs(got - ref) / den))
+
+
+def view_ws(workspace, offset, rows, cols, dtype):
+    """A typed view of a region of the layer workspace."""
+    import torch
+    es = 2 if dtype == "bf16" else 4
+    nbytes = rows * cols * es
+    raw = workspace[offset:offset + nbytes]
+    return raw.view(torch_dt(dtype)).view(rows, cols)
+
+
+def view_ws_f32(workspace, offset, rows):
+    import torch
+    return workspace[offset:offset + rows * 4].view(torch.float32)
+
+
+def count_band(b, wg, wu, eps):
+    """Per-row range of near-zero counts consistent with fp32 evaluation.
+
+    b: the MLP input (RMS-normalised) in float64, wg/wu: [I, d] weights.  An
+    activation is ambiguous when its reference magnitude lies within the
+    error an fp32 evaluation can make of it: the gate and up products carry
+    about sqrt(K) * 2^-24 of the sum of absolute terms (times a safety factor
+    of 8), and exp / division / the row scale add a few ulps of |act|.  The
+    decision of every other activation is fixed, so a correct kernel's count
+    lies in [c_min, c_max].  Returns (c_min, c_max, c_ref).
+    """
+    K = b.shape[1]
+    u32 = 2.0 ** -24
+    gam = 8.0 * np.sqrt(K) * u32
+    g = b @ wg.T
+    u = b @ wu.T
+    dg = gam * (np.abs(b) @ np.abs(wg).T) + 4 * u32 * np.abs(g)
+    du = gam * (np.abs(b) @ np.abs(wu).T) + 4 * u32 * np.abs(u)
+    sig = 1.0 / (1.0 + np.exp(-g))
+    s = g * sig
+    ds = np.abs(sig * (1.0 + g * (1.0 - sig)))     # |d silu / dg|
+    act = s * u
+    da = ds * dg * np.abs(u) + np.abs(s) * du + 16 * u32 * np.abs(act)
+    a = np.abs(act)
+    c_min = np.sum(a < eps - da, axis=-1)
+    c_max = np.sum(a < eps + da, axis=-1)
+    c_ref = np.sum(a < eps, axis=-1)
+    return c_min, c_max, c_ref
+
+
+def check_counts(cnt_gpu, b, wg, wu, eps, d_ff, frac_tol=1e-3):
+    """Gate: every row's count within the fp32-consistent band; the fraction
+    difference to the fp64 count within frac_tol except where the band shows
+    rounding ties.  Returns (max |diff| in counts, number of ambiguous ties)."""
+    c_min, c_max, c_ref = count_band(b, wg, wu, eps)
+    cnt_gpu = np.asarray(cnt_gpu, np.int64)
+    bad = np.nonzero((cnt_gpu < c_min) | (cnt_gpu > c_max))[0]
+    assert bad.size == 0, "rows %s: count %s outside [%s, %s]" % (
+        bad[:5], cnt_gpu[bad[:5]], c_min[bad[:5]], c_max[bad[:5]])
+    diff = np.abs(cnt_gpu - c_ref)
+    ties = int(np.sum(c_max - c_min))
+    over = diff / float(d_ff) > frac_tol
+    # a fraction difference above tolerance is only allowed where ties explain it
+    assert np.all(diff[over] <= (c_max - c_min)[over])
+    return int(diff.max()) if diff.size else 0, ties

@@ -1,0 +1,301 @@
+"""GPU parity of each C-ABI entry point against the oracle, at small sizes.
+
+Sizes span several GEMM tiles (256 rows) and attention tiles (128 queries,
+64 keys) with ragged tails.  Tolerances: boundary indices, offsets, routes
+and copied rows bit-exact; sparsity fractions within 1e-3 (teacher-forced at
+the MLP input); hidden states within 2e-2 max relative error for bf16
+(error / max(|ref|, rms of the reference row)) and 1e-4 for fp32.
+"""
+import json
+import os
+from fractions import Fraction
+
+import numpy as np
+import pytest
+
+from conftest import GOLDEN
+from gpu_util import check_counts, dev, host, log, rel_err, upload_weights, view_ws, view_ws_f32
+from oracle.detect import detect_batch, detect_boundary
+from oracle.layer import attention_seq, layer_forward, rms_norm, silu
+from oracle.route import repack_rows, route_batch
+from oracle.sparsity import near_zero_count
+
+pytestmark = pytest.mark.gpu
+
+BF16_TOL = 2e-2
+F32_TOL = 1e-4
+FRAC_TOL = 1e-3
+
+
+@pytest.fixture(scope="module")
+def S():
+    import torch
+    from paper_2607_14557_amd import seer
+    seer.load_library()
+    torch.cuda.init()
+    return seer
+
+
+def _i32(n):
+    import torch
+    return torch.empty(n, dtype=torch.int32, device="cuda")
+
+
+# ---------------------------------------------------------------------------
+# SNR boundary scan
+
+def test_detect_golden_cases(S):
+    import torch
+    with open(os.path.join(GOLDEN, "detector_cases.json")) as f:
+        cases = json.load(f)["cases"]
+    for c in cases:
+        log("detect golden: %s" % c["name"])
+        n = len(c["counts"])
+        cnt = dev(np.array(c["counts"], np.int32))
+        bnd, keep = _i32(1), _i32(1)
+        prm = S.seer_snr_params(c["tau"][0], c["tau"][1], c["gamma"][0], c["gamma"][1], c["lookahead"])
+        S.seer_step0_detect(cnt, dev(np.array([0, n])), dev(np.array([0])), dev(np.array([n])), 1,
+                            c["d_ff"], prm, bnd, keep)
+        torch.cuda.synchronize()
+        assert (int(bnd[0]), int(keep[0])) == (c["boundary"], c["keep_len"]), c["name"]
+
+
+@pytest.mark.parametrize("lookahead,tau,gamma", [(3, (3, 100), (3, 5)), (2, (1, 50), (1, 2)),
+                                                 (5, (7, 100), (4, 5)), (1, (3, 100), (3, 5))])
+def test_detect_random_batch_vs_oracle(S, lookahead, tau, gamma):
+    import torch
+    rng = np.random.default_rng(100 + lookahead)
+    B, I = 64, 997
+    pre = rng.integers(0, 40, size=B)
+    win = rng.integers(1, 300, size=B)
+    win[:3] = [1, 2, lookahead]                    # windows too short for any candidate
+    lens = pre + win + rng.integers(0, 5, size=B)  # a little slack after the window
+    cu = np.concatenate([[0], np.cumsum(lens)])
+    counts = rng.integers(0, 120, size=int(cu[-1]))
+    for b in range(B):                             # plant steps in most windows
+        if b % 4:
+            j = int(cu[b] + pre[b] + rng.integers(0, max(1, win[b])))
+            counts[j:cu[b + 1]] += int(rng.integers(0, 80))
+    counts = np.minimum(counts, I)
+    bnd, keep = _i32(B), _i32(B)
+    log("detect random lookahead=%d" % lookahead)
+    S.seer_step0_detect(dev(counts.astype(np.int32)), dev(cu), dev(pre), dev(win), B, I,
+                        S.seer_snr_params(tau[0], tau[1], gamma[0], gamma[1], lookahead), bnd, keep)
+    torch.cuda.synchronize()
+    eb, ek = detect_batch(counts, cu, pre, win, I, Fraction(*tau), Fraction(*gamma), lookahead)
+    np.testing.assert_array_equal(host(bnd), eb)
+    np.testing.assert_array_equal(host(keep), ek)
+
+
+# ---------------------------------------------------------------------------
+# routing + compaction
+
+def _repack_case(S, policy, granule, B=13, d=64, seed=0, capacity=None):
+    import torch
+    rng = np.random.default_rng(seed)
+    win_off = rng.integers(5, 41, size=B)
+    win_len = np.full(B, 200)
+    keep = rng.integers(1, 201, size=B)
+    keep[:3] = [2, 3, 4]
+    keep[3:6] = [60, 61, 63]
+    lens = win_off + win_len
+    cu_src = np.concatenate([[0], np.cumsum(lens)])
+    T = int(cu_src[-1])
+    src1 = rng.standard_normal((T, d)).astype(np.float32)
+    src2 = rng.standard_normal((T, d)).astype(np.float32)
+    full_cap = int(np.sum(win_off + win_len.max()))
+    if capacity is None:
+        capacity = ((full_cap + granule - 1) // granule) * granule + granule
+    s1, s2 = dev(src1, "bf16"), dev(src2, "bf16")
+    sentinel = -7.0
+    d1 = torch.full((capacity, d), sentinel, dtype=torch.bfloat16, device="cuda")
+    d2 = torch.full((capacity, d), sentinel, dtype=torch.bfloat16, device="cuda")
+    cu_dst, used = _i32(B + 1), _i32(B)
+    route = torch.empty(B, 3, dtype=torch.int32, device="cuda")
+    ctrl = torch.zeros(16, dtype=torch.int32, device="cuda")
+    ctrl_h = torch.zeros(16, dtype=torch.int32).pin_memory()
+    desc = S.seer_repack_desc(policy, 1, 5, granule, d * 2, capacity, 0, 0)
+    S.seer_batch_repack(desc, [s1, s2], [d1, d2], dev(cu_src), dev(win_off), dev(win_len),
+                        dev(keep), B, cu_dst, used, route, ctrl, ctrl_h)
+    torch.cuda.synchronize()
+    return dict(win_off=win_off, win_len=win_len, keep=keep, cu_src=cu_src, s=[s1, s2], d=[d1, d2],
+                cu_dst=cu_dst, used=used, route=route, ctrl=ctrl, ctrl_h=ctrl_h, capacity=capacity)
+
+
+@pytest.mark.parametrize("policy", [0, 1, 2])
+@pytest.mark.parametrize("granule", [1, 256])
+def test_repack_vs_oracle(S, policy, granule):
+    import torch
+    log("repack policy=%d granule=%d" % (policy, granule))
+    r = _repack_case(S, policy, granule, seed=policy * 10 + granule)
+    rt = route_batch(r["keep"], r["win_len"], policy, Fraction(1, 5))
+    route = host(r["route"])
+    np.testing.assert_array_equal(route[:, 0], rt.path)
+    np.testing.assert_array_equal(route[:, 1], rt.group)
+    np.testing.assert_array_equal(route[:, 2], rt.alloc)
+    for bi in range(2):
+        src = host(r["s"][bi])
+        exp, cu_e, used_e, cap = repack_rows(src, r["cu_src"], r["win_off"], r["keep"], rt.alloc, granule)
+        np.testing.assert_array_equal(host(r["cu_dst"]), cu_e)
+        np.testing.assert_array_equal(host(r["used"]), used_e)
+        got = host(r["d"][bi])
+        np.testing.assert_array_equal(got[:cap], exp)
+        assert np.all(got[cap:] == -7.0), "rows past the routed capacity must be untouched"
+    ctrl = host(r["ctrl"])
+    assert list(ctrl[:9]) == [cu_e[-1], cap, int(np.sum(rt.path == 0)), int(np.sum(rt.path == 1)),
+                              int(np.sum(rt.path == 2)), len(rt.groups), int(rt.alloc.max()), 0, 1]
+    np.testing.assert_array_equal(host(r["ctrl_h"]), ctrl)
+
+
+def test_repack_overflow_reports_status(S):
+    log("repack overflow")
+    r = _repack_case(S, 0, 1, seed=3, capacity=50)
+    ctrl = host(r["ctrl"])
+    assert ctrl[7] == S.SEER_EWORKSPACE and ctrl[8] == 1
+    assert np.all(host(r["cu_dst"]) == 0)
+    assert np.all(host(r["d"][0]) == -7.0), "nothing may be written on overflow"
+
+
+# ---------------------------------------------------------------------------
+# one layer, bf16 and fp32
+
+def _rand_layer(rng, d, I, std):
+    return {"wq": rng.standard_normal((d, d)) * std, "wk": rng.standard_normal((d, d)) * std,
+            "wv": rng.standard_normal((d, d)) * std, "wo": rng.standard_normal((d, d)) * std,
+            "wg": rng.standard_normal((I, d)) * std, "wu": rng.standard_normal((I, d)) * std,
+            "wd": rng.standard_normal((d, I)) * std,
+            "g1": np.ones(d), "g2": np.ones(d)}
+
+
+def _round(W, dtype):
+    from workloads.generate import round_to_dtype
+    return {k: (round_to_dtype(v, dtype).astype(np.float64) if k not in ("g1", "g2") else v)
+            for k, v in W.items()}
+
+
+class _Layer:
+    """One prepacked layer + workspace driven through the C ABI."""
+
+    def __init__(self, S, d, H, dh, I, dtype, rows_ub, W):
+        import torch
+        from paper_2607_14557_amd.runner import dims_for
+        self.S = S
+        self.dims = dims_for(d, H, dh, I, dtype)
+        self.dtype = dtype
+        self.rows_ub = rows_ub
+        self.packed = torch.empty(S.seer_prepacked_bytes(self.dims), dtype=torch.uint8, device="cuda")
+        S.seer_prepack_weights(self.dims, upload_weights(W, dtype), self.packed)
+        self.ws = torch.empty(S.seer_layer_workspace_bytes(self.dims, rows_ub), dtype=torch.uint8,
+                              device="cuda")
+        self.off = S.seer_layer_workspace_offsets(self.dims, rows_ub)
+
+    def run(self, x, cu, batch, seqused=None, eps=None):
+        import torch
+        out = torch.zeros_like(x)
+        cnt = _i32(self.rows_ub) if eps is not None else None
+        self.S.seer_layer_forward_varlen(self.dims, self.packed, x, out, self.rows_ub, cu, seqused,
+                                         batch, 0.0 if eps is None else eps, cnt, self.ws)
+        torch.cuda.synchronize()
+        return out, cnt
+
+    def inter(self, name, rows, cols=None):
+        idx = {"qkv": 0, "o": 1, "h1": 2, "act": 3, "inv1": 4, "inv2": 5}[name]
+        if name.startswith("inv"):
+            return view_ws_f32(self.ws, self.off[idx], rows)
+        return view_ws(self.ws, self.off[idx], rows, cols, self.dtype)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_layer_vs_oracle_ragged(S, dtype):
+    d, H, dh, I = (512, 4, 128, 1024) if dtype == "bf16" else (256, 4, 64, 688)
+    tol = BF16_TOL if dtype == "bf16" else F32_TOL
+    rng = np.random.default_rng(42)
+    W = _round(_rand_layer(rng, d, I, 0.02), dtype)
+    lens = [300, 77, 513, 1, 129]
+    cu = np.concatenate([[0], np.cumsum(lens)])
+    T = int(cu[-1])
+    rows_ub = T + 5
+    x = np.zeros((rows_ub, d))
+    x[:T] = rng.standard_normal((T, d))
+    xd = dev(x, dtype)
+    x = host(xd)                                    # exact values the GPU sees
+    eps = 0.01 * 0.0004 * d
+    log("layer %s ragged lens=%s" % (dtype, lens))
+    L = _Layer(S, d, H, dh, I, dtype, rows_ub, W)
+    y, cnt = L.run(xd, dev(cu), len(lens), eps=eps)
+    y = host(y)
+    y_ref, cnt_ref = layer_forward(x[:T], cu, W, H, 1e-5, act_eps=eps)
+    e = rel_err(y[:T], y_ref)
+    log("  y rel err %.3e" % e)
+    assert e <= tol
+    assert np.all(y[T:] == 0.0), "rows past cu[B] must not be written"
+    # teacher-forced stages
+    qkv = host(L.inter("qkv", T, 3 * d))
+    a = rms_norm(x[:T], W["g1"], 1e-5)
+    qkv_ref = np.concatenate([a @ W["wq"].T, a @ W["wk"].T, a @ W["wv"].T], axis=1)
+    assert rel_err(qkv, qkv_ref) <= tol
+    o = host(L.inter("o", T, d))
+    for b in range(len(lens)):
+        s = slice(cu[b], cu[b + 1])
+        o_ref = attention_seq(qkv[s, :d], qkv[s, d:2 * d], qkv[s, 2 * d:], H)
+        eo = rel_err(o[s], o_ref)
+        assert eo <= tol, "attention seq %d err %.3e" % (b, eo)
+    h1 = host(L.inter("h1", T, d))
+    assert rel_err(h1, x[:T] + o @ W["wo"].T) <= tol
+    bnorm = rms_norm(h1, W["g2"], 1e-5)
+    act_ref = silu(bnorm @ W["wg"].T) * (bnorm @ W["wu"].T)
+    act = host(L.inter("act", T, I))
+    assert rel_err(act, act_ref) <= tol
+    dmax, ties = check_counts(host(cnt)[:T], bnorm, W["wg"], W["wu"], eps, I, FRAC_TOL)
+    log("  count max diff (teacher-forced) %d of %d, rounding ties %d; untethered %d" %
+        (dmax, I, ties, np.abs(host(cnt)[:T] - cnt_ref).max()))
+    if dtype == "f32":
+        # the fp32 activations are stored unrounded: the kernel's count must be
+        # exactly the count of its own activations
+        np.testing.assert_array_equal(host(cnt)[:T], near_zero_count(act, eps))
+    assert rel_err(y[:T], h1 + act @ W["wd"].T) <= tol
+
+
+def test_layer_static_padding_equals_cut_layout_bitwise(S):
+    """Pad rows masked by seqused leave the kept rows bit-identical."""
+    import torch
+    d, H, dh, I = 512, 4, 128, 1024
+    rng = np.random.default_rng(7)
+    W = _round(_rand_layer(rng, d, I, 0.02), "bf16")
+    used = [200, 65, 130]
+    alloc = [256, 128, 130]
+    cu_pad = np.concatenate([[0], np.cumsum(alloc)])
+    cu_cut = np.concatenate([[0], np.cumsum(used)])
+    xs = [rng.standard_normal((u, d)) for u in used]
+    x_pad = np.zeros((int(cu_pad[-1]), d))
+    for b in range(3):
+        x_pad[cu_pad[b]:cu_pad[b] + used[b]] = xs[b]
+    x_cut = np.concatenate(xs)
+    rows_ub = int(cu_pad[-1])
+    L = _Layer(S, d, H, dh, I, "bf16", rows_ub, W)
+    log("layer static padding vs cut")
+    y_pad, c_pad = L.run(dev(x_pad, "bf16"), dev(cu_pad), 3, seqused=dev(np.array(used)), eps=0.002)
+    y_cut, c_cut = L.run(dev(np.concatenate([x_cut, np.zeros((rows_ub - len(x_cut), d))]), "bf16"),
+                         dev(cu_cut), 3, eps=0.002)
+    yp, yc = host(y_pad), host(y_cut)
+    cp, cc = host(c_pad), host(c_cut)
+    for b in range(3):
+        np.testing.assert_array_equal(yp[cu_pad[b]:cu_pad[b] + used[b]], yc[cu_cut[b]:cu_cut[b + 1]])
+        np.testing.assert_array_equal(cp[cu_pad[b]:cu_pad[b] + used[b]], cc[cu_cut[b]:cu_cut[b + 1]])
+        assert np.all(yp[cu_pad[b] + used[b]:cu_pad[b + 1]] == 0.0)
+        assert np.all(cp[cu_pad[b] + used[b]:cu_pad[b + 1]] == I)
+
+
+def test_layer_deterministic(S):
+    d, H, dh, I = 512, 4, 128, 1024
+    rng = np.random.default_rng(9)
+    W = _round(_rand_layer(rng, d, I, 0.02), "bf16")
+    lens = [333, 190]
+    cu = np.concatenate([[0], np.cumsum(lens)])
+    x = dev(rng.standard_normal((int(cu[-1]), d)), "bf16")
+    L = _Layer(S, d, H, dh, I, "bf16", int(cu[-1]), W)
+    log("layer determinism")
+    y1, c1 = L.run(x, dev(cu), 2, eps=0.002)
+    y2, c2 = L.run(x, dev(cu), 2, eps=0.002)
+    np.testing.assert_array_equal(host(y1), host(y2))
+    np.testing.assert_array_equal(host(c1), host(c2))

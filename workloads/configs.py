@@ -74,6 +74,9 @@ TAU_PAD = Fraction(1, 5)
 
 LLADA8B = LayerShape(d_model=4096, n_heads=32, head_dim=128, d_ff=12288)
 TINY = LayerShape(d_model=256, n_heads=4, head_dim=64, d_ff=688)
+# Smallest shape the bf16 kernels take (head_dim 128): parity cases that
+# still span several GEMM tiles and attention tiles with ragged tails.
+SMALL_BF16 = LayerShape(d_model=512, n_heads=4, head_dim=128, d_ff=1024)
 
 
 def act_eps_for(shape: LayerShape, weight_std: float = 0.02, kappa: float = 0.01) -> float:
@@ -109,6 +112,16 @@ WORKLOADS = {
         boundary=("uniform", 64, 1024), seed=5005, act_eps=act_eps_for(LLADA8B),
         trunc_steps=63),
 }
+
+# Parity-test workloads at reduced size (not benchmark lines).
+WORKLOADS["small_bf16_ragged"] = Workload(
+    name="small_bf16_ragged", shape=SMALL_BF16, n_layers=1, l_det=0, batch=5,
+    n_visual=100, n_prompt=27, window=160, dtype="bf16",
+    boundary=("uniform", 12, 140), seed=606, act_eps=act_eps_for(SMALL_BF16))
+WORKLOADS["small_bf16_stack"] = Workload(
+    name="small_bf16_stack", shape=SMALL_BF16, n_layers=3, l_det=1, batch=3,
+    n_visual=150, n_prompt=20, window=200, dtype="bf16",
+    boundary=("uniform", 20, 180), seed=707, act_eps=act_eps_for(SMALL_BF16))
 
 WORKLOAD_ORDER = ["tiny_f32", "llada_b1", "llada_b16_ragged",
                   "llada32_multicrop_b8", "llada32_video_b4"]
