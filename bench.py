@@ -1,0 +1,303 @@
+#!/usr/bin/env python3
+"""Benchmark of the Seer hot path on one MI355X.
+
+One bench step is one pass of the whole path over one batch:
+  step 0   the full-window layer with the fused near-zero count (the
+           detection layer; the LLaDA-8B-shaped layer, B=16 ragged batch of
+           [729 visual ; 64 prompt ; 1024 window] rows),
+           the SNR boundary scan,
+           routing + compaction of the step-input embeddings and of the
+           in-flight residual (one launch),
+  step 1   one truncated denoising step: the layer on the compacted batch.
+Everything is queued on one HIP stream with no host synchronisation inside
+the step (kernels read row counts from device memory; grids are sized from
+the full-window bound).
+
+value = effective generated tokens per second = (sum of kept window lengths)
+x (2 denoising steps per bench step) / step time.  The untruncated step (the
+same layer over the full window) is timed separately for the speedup.
+
+The roofline object is for the dominant kernel of every truncated step, the
+gate/up GEMM with the SwiGLU epilogue, timed live with HIP events recorded
+around it inside the timed steps.  The CPU baseline times the oracle (fp64
+NumPy) on a bounded sample of the same batch on this host.
+
+Prints exactly one JSON line on stdout; progress goes to stderr.
+"""
+import argparse
+import ctypes
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "effective gen tokens/sec per denoising step (B=16 ragged); MFMA util %"
+PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 matrix peak
+PEAK_HBM_GBS = 8000.0
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+class Hip:
+    """HIP events through the runtime torch already loaded (same soname)."""
+
+    def __init__(self):
+        self.L = ctypes.CDLL("libamdhip64.so.7")
+        self.L.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+        self.L.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+        self.L.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p,
+                                               ctypes.c_void_p]
+        self.L.hipEventSynchronize.argtypes = [ctypes.c_void_p]
+        self.L.hipEventDestroy.argtypes = [ctypes.c_void_p]
+
+    def event(self):
+        e = ctypes.c_void_p()
+        if self.L.hipEventCreate(ctypes.byref(e)) != 0:
+            raise RuntimeError("hipEventCreate failed")
+        return e.value
+
+    def record(self, e, stream):
+        if self.L.hipEventRecord(e, stream) != 0:
+            raise RuntimeError("hipEventRecord failed")
+
+    def ms(self, a, b):
+        f = ctypes.c_float()
+        if self.L.hipEventElapsedTime(ctypes.byref(f), a, b) != 0:
+            raise RuntimeError("hipEventElapsedTime failed")
+        return float(f.value)
+
+
+def cpu_baseline(w, layers, batch, seconds):
+    """Oracle (fp64 NumPy) on the first sequences of the batch, ~`seconds` of work."""
+    import numpy as np
+    import oracle
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 0) for i in threadpool_info()] or [os.cpu_count()])
+    except Exception:
+        cores = os.cpu_count()
+    sh = w.shape
+    t0 = time.perf_counter()
+    toks = 0
+    nseq = 0
+    S = w.seq_len_full
+    for b in range(w.batch):
+        x = batch.x[b * S:(b + 1) * S]
+        res = oracle.run_pipeline(layers, x, [0, S], batch.win_off[b:b + 1], batch.win_len[b:b + 1],
+                                  sh.n_heads, sh.d_ff, w.rms_eps, w.act_eps, w.l_det)
+        toks += 2 * int(res.keep_len[0])
+        nseq += 1
+        if time.perf_counter() - t0 >= seconds:
+            break
+    dt = time.perf_counter() - t0
+    return {"value": toks / dt, "unit": "tokens/s", "cores": int(cores), "kind": "oracle",
+            "sample": "oracle step 0 (full-window layer + count + SNR scan + routing/compaction) and "
+                      "one truncated step, fp64 NumPy, on the first %d of %d sequences (%.1f s)"
+                      % (nseq, w.batch, dt)}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="llada_b16_ragged")
+    ap.add_argument("--policy", default="hybrid", choices=["hybrid", "naive_pad", "varlen_only"])
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU: this build has no multi-GPU path "
+              "(requested --gpus %d, WORLD_SIZE %d)" % (args.gpus, world), file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    from paper_2607_14557_amd import seer as S
+    from paper_2607_14557_amd.runner import dims_for
+    from workloads import WORKLOADS
+    from workloads.generate import make_workload
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    S.load_library()
+    w = WORKLOADS[args.workload]
+    if w.n_layers != 1 or w.dtype != "bf16":
+        raise SystemExit("bench.py times single-layer bf16 workloads")
+    sh = w.shape
+    d, I = sh.d_model, sh.d_ff
+    policy = {"hybrid": S.SEER_ROUTE_HYBRID, "naive_pad": S.SEER_ROUTE_NAIVE_PAD,
+              "varlen_only": S.SEER_ROUTE_VARLEN_ONLY}[args.policy]
+
+    log("generating workload %s" % w.name)
+    t0 = time.perf_counter()
+    layers, batch = make_workload(w)
+    log("  inputs ready in %.1f s" % (time.perf_counter() - t0))
+    dev = torch.device("cuda:0")
+    dims = dims_for(d, sh.n_heads, sh.head_dim, I, "bf16", w.rms_eps)
+    T = w.rows_full
+    granule = 256
+    cap = ((T + granule - 1) // granule) * granule
+    stream = torch.cuda.current_stream()
+    sp = stream.cuda_stream
+
+    wdev = {k: torch.from_numpy(np.asarray(v, np.float32)).to(
+        torch.bfloat16 if k not in ("g1", "g2") else torch.float32).to(dev) for k, v in layers[0].items()}
+    packed = torch.empty(S.seer_prepacked_bytes(dims), dtype=torch.uint8, device=dev)
+    S.seer_prepack_weights(dims, wdev, packed, stream=sp)
+    del wdev
+    ws_bytes = S.seer_layer_workspace_bytes(dims, cap)
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
+    x_full = torch.from_numpy(batch.x).to(torch.bfloat16).to(dev)
+    i32 = lambda a: torch.from_numpy(np.asarray(a, np.int32)).to(dev)
+    cu_full, win_off, win_len = i32(batch.cu_seqlens), i32(batch.win_off), i32(batch.win_len)
+    y_full = torch.empty(T, d, dtype=torch.bfloat16, device=dev)
+    counts = torch.empty(T, dtype=torch.int32, device=dev)
+    bnd = torch.empty(w.batch, dtype=torch.int32, device=dev)
+    keep = torch.empty(w.batch, dtype=torch.int32, device=dev)
+    x_t = torch.zeros(cap, d, dtype=torch.bfloat16, device=dev)
+    h_t = torch.zeros(cap, d, dtype=torch.bfloat16, device=dev)
+    y_t = torch.zeros(cap, d, dtype=torch.bfloat16, device=dev)
+    cu_t = torch.empty(w.batch + 1, dtype=torch.int32, device=dev)
+    used = torch.empty(w.batch, dtype=torch.int32, device=dev)
+    route = torch.empty(w.batch, 3, dtype=torch.int32, device=dev)
+    ctrl = torch.zeros(16, dtype=torch.int32, device=dev)
+    snr = S.seer_snr_params(3, 100, 3, 5, 3)
+    desc = S.seer_repack_desc(policy, 1, 5, granule, d * 2, cap, 0, 0)
+
+    hip = Hip()
+    n_ev = args.warmup + args.steps
+    ev_full = [[hip.event() for _ in range(8)] for _ in range(n_ev)]
+    ev_trunc = [[hip.event() for _ in range(8)] for _ in range(n_ev)]
+    ev_mid = [[hip.event() for _ in range(2)] for _ in range(n_ev)]
+
+    def step(i):
+        S.seer_layer_forward_varlen_timed(dims, packed, x_full, y_full, T, cu_full, None, w.batch,
+                                          w.act_eps, counts, ws, ev_full[i], stream=sp)
+        S.seer_step0_detect(counts, cu_full, win_off, win_len, w.batch, I, snr, bnd, keep, stream=sp)
+        S.seer_batch_repack(desc, [x_full, y_full], [x_t, h_t], cu_full, win_off, win_len, keep,
+                            w.batch, cu_t, used, route, ctrl, None, stream=sp)
+        hip.record(ev_mid[i][0], sp)
+        S.seer_layer_forward_varlen_timed(dims, packed, x_t, y_t, cap, cu_t, used, w.batch, 0.0,
+                                          None, ws, ev_trunc[i], stream=sp)
+        hip.record(ev_mid[i][1], sp)
+
+    log("warmup %d steps" % args.warmup)
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    keep_h = keep.cpu().numpy()
+    used_h = used.cpu().numpy()
+    route_h = route.cpu().numpy()
+    ctrl_h = ctrl.cpu().numpy()
+    if not np.array_equal(bnd.cpu().numpy(), batch.planted):
+        log("WARNING: detected boundaries differ from the planted ones")
+    sum_keep = int(keep_h.sum())
+    rows_alg = int(used_h.sum())          # prefix + kept window rows (no padding)
+    rows_exec = int(ctrl_h[0])            # rows the truncated kernels process
+
+    log("timing %d steps" % args.steps)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.warmup, n_ev):
+        step(i)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_step = wall * 1e3 / args.steps
+
+    rng = range(args.warmup, n_ev)
+    kern = ["rms1", "qkv", "attn", "o", "rms2", "gateup", "down"]
+
+    def kernel_ms(evs):
+        return {k: float(np.mean([hip.ms(evs[i][j], evs[i][j + 1]) for i in rng]))
+                for j, k in enumerate(kern)}
+
+    kf, kt = kernel_ms(ev_full), kernel_ms(ev_trunc)
+    t_full_layer = float(np.mean([hip.ms(ev_full[i][0], ev_full[i][7]) for i in rng]))
+    t_trunc = float(np.mean([hip.ms(ev_mid[i][0], ev_mid[i][1]) for i in rng]))
+    t_mid = float(np.mean([hip.ms(ev_full[i][7], ev_mid[i][0]) for i in rng]))
+
+    # untruncated denoising step (same layer over the full window, no count) for the speedup
+    log("timing the untruncated step")
+    for _ in range(3):
+        S.seer_layer_forward_varlen(dims, packed, x_full, y_full, T, cu_full, None, w.batch, 0.0,
+                                    None, ws, stream=sp)
+    e0, e1 = hip.event(), hip.event()
+    reps = max(5, args.steps // 2)
+    hip.record(e0, sp)
+    for _ in range(reps):
+        S.seer_layer_forward_varlen(dims, packed, x_full, y_full, T, cu_full, None, w.batch, 0.0,
+                                    None, ws, stream=sp)
+    hip.record(e1, sp)
+    torch.cuda.synchronize()
+    t_full = hip.ms(e0, e1) / reps
+
+    gemm_flop_row = {"qkv": 2 * 3 * d * d, "o": 2 * d * d, "gateup": 2 * 2 * I * d, "down": 2 * I * d}
+    seqlens_full = np.diff(batch.cu_seqlens).astype(np.int64)
+    seqlens_t = used_h.astype(np.int64)
+    attn_flop = lambda lens: int(np.sum(4 * lens * lens * d))
+
+    def tflops(flop, ms):
+        return flop / (ms * 1e-3) / 1e12
+
+    kernels = {}
+    for tag, kms, rows, lens in (("full", kf, T, seqlens_full), ("trunc", kt, rows_alg, seqlens_t)):
+        for k in ("qkv", "o", "gateup", "down"):
+            kernels["%s_%s" % (tag, k)] = {"ms": round(kms[k], 4),
+                                           "tflops": round(tflops(rows * gemm_flop_row[k], kms[k]), 1)}
+        kernels["%s_attn" % tag] = {"ms": round(kms["attn"], 4),
+                                    "tflops": round(tflops(attn_flop(lens), kms["attn"]), 1)}
+        kernels["%s_rms" % tag] = {"ms": round(kms["rms1"] + kms["rms2"], 4)}
+    gemm_ms_t = sum(kt[k] for k in ("qkv", "o", "gateup", "down"))
+    gemm_flop_t = rows_alg * sum(gemm_flop_row.values())
+
+    dom_flop = rows_alg * gemm_flop_row["gateup"]
+    dom_ms = kt["gateup"]
+    achieved = tflops(dom_flop, dom_ms)
+    roofline = {"bound": "mfma", "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS,
+                "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                "kernel": "gemm_bf16_kernel<EPI_SWIGLU> (truncated-step gate/up GEMM)",
+                "flop_per_launch": dom_flop, "launch_ms": round(dom_ms, 4)}
+
+    value = 2 * sum_keep / (ms_step * 1e-3)
+    out = {
+        "metric": METRIC, "value": round(value, 1), "unit": "tokens/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic (seeded; random-init LLaDA-8B-shaped layer, planted EOS suffixes)",
+        "config": {"workload": w.name, "batch": w.batch, "visual_prefix": w.n_visual,
+                   "prompt": w.n_prompt, "window": w.window, "layers": w.n_layers,
+                   "d_model": d, "heads": sh.n_heads, "head_dim": sh.head_dim, "d_ff": I,
+                   "policy": args.policy, "denoising_steps_per_bench_step": 2,
+                   "sum_keep_len": sum_keep, "rows_full": T, "rows_trunc": rows_alg,
+                   "rows_trunc_executed": rows_exec},
+        "roofline": roofline,
+        "trunc_step_ms": round(t_trunc, 4),
+        "full_step_ms": round(t_full, 4),
+        "speedup_trunc_vs_full": round(t_full / t_trunc, 3),
+        "trunc_step_tokens_per_s": round(sum_keep / (t_trunc * 1e-3), 1),
+        "full_step_tokens_per_s": round(sum_keep / (t_full * 1e-3), 1),
+        "step0_layer_ms": round(t_full_layer, 4),
+        "detect_repack_ms": round(t_mid, 4),
+        "trunc_gemm_mfma_util": round(tflops(gemm_flop_t, gemm_ms_t) / PEAK_BF16_TFLOPS, 4),
+        "kernels": kernels,
+        "paper_context": "up to ~31x end-to-end tokens/s (MMaDA, InfoVQA) on 1x NVIDIA A100 "
+                         "(context only, different hardware and workload)",
+    }
+    if not args.no_cpu_baseline:
+        log("CPU baseline (oracle on host cores)")
+        out["cpu_baseline"] = cpu_baseline(w, layers, batch, args.cpu_seconds)
+    else:
+        out["cpu_baseline"] = None
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

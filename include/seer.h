@@ -142,6 +142,21 @@ int seer_layer_forward_varlen(const seer_dims* dims, const void* w_packed,
                               void* workspace, size_t workspace_bytes,
                               hipStream_t stream);
 
+/* As seer_layer_forward_varlen, recording events[k] (created by the caller)
+ * on `stream` around its kernels for live per-kernel timing:
+ *   events[0] -> [1] RMS statistics of x       [1] -> [2] QKV GEMM
+ *   events[2] -> [3] attention                 [3] -> [4] O GEMM + residual
+ *   events[4] -> [5] RMS statistics of h1 (+ zeroing act_count)
+ *   events[5] -> [6] gate/up GEMM + SwiGLU (+ count)
+ *   events[6] -> [7] down GEMM + residual
+ * Errors: as seer_layer_forward_varlen, EINVAL if events or an entry is NULL. */
+int seer_layer_forward_varlen_timed(const seer_dims* dims, const void* w_packed,
+                                    const void* x_in, void* x_out, int32_t total_rows_ub,
+                                    const int32_t* cu_seqlens, const int32_t* seqused,
+                                    int32_t batch, float act_eps, int32_t* act_count,
+                                    void* workspace, size_t workspace_bytes,
+                                    hipStream_t stream, hipEvent_t events[8]);
+
 /* SNR criterion parameters as exact rationals: tau_jump = tau_num/tau_den,
  * gamma = gamma_num/gamma_den; lookahead = size of the window W_i.
  * The paper's defaults are {3, 100, 3, 5, 3}. */

@@ -101,7 +101,7 @@ __global__ __launch_bounds__(NT, 2) void attn_bf16_kernel(AttnParams p) {
   // ---- K/V tile staging -------------------------------------------------------
   // K: thread loads 16-byte chunks id = tid + 256*i: key id/16, dim chunk id%16.
   // V: thread loads keys 4*(tid/16) .. +3 at dim chunk tid%16, transposes 4x8.
-  uint4 kreg[4], vreg[4];
+  u32x4_t kreg[4], vreg[4];
   const int vkq = tid >> 4;
   const int vdc = tid & 15;
   auto load_tile = [&](int kbase) {
@@ -110,13 +110,13 @@ __global__ __launch_bounds__(NT, 2) void attn_bf16_kernel(AttnParams p) {
       const int id = tid + NT * i;
       int key = kbase + (id >> 4);
       key = key < used ? key : used - 1;
-      kreg[i] = *reinterpret_cast<const uint4*>(qkv + (size_t)(s0 + key) * ld + p.d + h * DH + (id & 15) * 8);
+      kreg[i] = *reinterpret_cast<const u32x4_t*>(qkv + (size_t)(s0 + key) * ld + p.d + h * DH + (id & 15) * 8);
     }
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       int key = kbase + vkq * 4 + i;
       key = key < used ? key : used - 1;
-      vreg[i] = *reinterpret_cast<const uint4*>(qkv + (size_t)(s0 + key) * ld + 2 * p.d + h * DH + vdc * 8);
+      vreg[i] = *reinterpret_cast<const u32x4_t*>(qkv + (size_t)(s0 + key) * ld + 2 * p.d + h * DH + vdc * 8);
     }
   };
   auto store_tile = [&]() {
@@ -125,17 +125,17 @@ __global__ __launch_bounds__(NT, 2) void attn_bf16_kernel(AttnParams p) {
       const int id = tid + NT * i;
       const int key = id >> 4;
       const int ch = (id & 15) ^ (key & 15);
-      *reinterpret_cast<uint4*>(k_lds + key * K_ROW + ch * 16) = kreg[i];
+      *reinterpret_cast<u32x4_t*>(k_lds + key * K_ROW + ch * 16) = kreg[i];
     }
-    const uint32_t* w = reinterpret_cast<const uint32_t*>(vreg);  // w[4*i + e/2] = key i, dims e, e+1
+    // vreg[i][e/2] holds dims e, e+1 (low, high half) of key i
     const int pos = vpos(vkq * 4);
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
       const int sh = (e & 1) * 16;
-      const uint32_t k0 = (w[0 * 4 + e / 2] >> sh) & 0xffffu;
-      const uint32_t k1 = (w[1 * 4 + e / 2] >> sh) & 0xffffu;
-      const uint32_t k2 = (w[2 * 4 + e / 2] >> sh) & 0xffffu;
-      const uint32_t k3 = (w[3 * 4 + e / 2] >> sh) & 0xffffu;
+      const uint32_t k0 = (vreg[0][e / 2] >> sh) & 0xffffu;
+      const uint32_t k1 = (vreg[1][e / 2] >> sh) & 0xffffu;
+      const uint32_t k2 = (vreg[2][e / 2] >> sh) & 0xffffu;
+      const uint32_t k3 = (vreg[3][e / 2] >> sh) & 0xffffu;
       const int dim = vdc * 8 + e;
       const int ch = (pos >> 3) ^ swz8(dim);
       uint2 v;

@@ -10,6 +10,11 @@ typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8_t;
 typedef __attribute__((__vector_size__(16 * sizeof(float)))) float f32x16_t;
 typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4_t;
 
+// 16-byte register type for global <-> LDS staging.  A native vector type
+// (not HIP's struct uint4): arrays of it stay in registers after unrolling,
+// where struct copies become private-memory memcpys.
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+
 typedef __attribute__((address_space(3))) void lds_void_t;
 typedef __attribute__((address_space(3))) uint8_t lds_u8_t;
 typedef __attribute__((address_space(1))) void glb_void_t;

@@ -5,10 +5,12 @@
 // contractions of the denoising step (the L*d^2 term of the complexity
 // equation, Sec. 3.1).  Tiling: 256x256 block tile, K step 64, four waves in
 // a 2x2 grid, each wave owning a 128x128 sub-tile as 4x4 tiles of the
-// 32x32x16 bf16 MFMA.  Operand tiles move HBM -> LDS with direct-to-LDS
-// 16-byte loads into a two-stage ring; the 16-byte chunks of each 128-byte
+// 32x32x16 bf16 MFMA.  The next K step's operand tiles are loaded into
+// registers while the current one is multiplied out of LDS, then written to
+// the other half of a two-stage LDS ring; the 16-byte chunks of each 128-byte
 // LDS row are XOR-swizzled so that the MFMA fragment reads of 16 consecutive
-// rows land in distinct banks.
+// rows land in distinct banks.  Fragments of the next 16-wide K slice are read
+// from LDS before the current slice's MFMAs are issued.
 //
 // Epilogues:
 //   SCALE   C = bf16(acc * rowscale[r])         folded RMSNorm before QKV
@@ -58,14 +60,18 @@ template <int EPI>
 __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmParams p) {
   __shared__ __attribute__((aligned(1024))) uint8_t smem[2 * STAGE_BYTES];
 
+  // Tile geometry follows the real row count read on the device, so that the
+  // blocks carrying work are spread over every XCD; surplus blocks of the
+  // upper-bound grid exit at once.
   const int M = rows_from(p.m_ptr, p.m_ub);
-  const int tiles_m = (p.m_ub + BM - 1) / BM;
+  const int tiles_m = (M + BM - 1) / BM;
   const int tiles_n = p.N / BN;
+  const int ntiles = tiles_m * tiles_n;
+  if ((int)blockIdx.x >= ntiles) return;
   int tm, tn;
-  tile_of(blockIdx.x, gridDim.x, tiles_m, tiles_n, tm, tn);
+  tile_of(blockIdx.x, ntiles, tiles_m, tiles_n, tm, tn);
   const int m0 = tm * BM;
   const int n0 = tn * BN;
-  if (m0 >= M) return;
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -73,41 +79,31 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmParams p) {
   const int wm = wave >> 1;
   const int wn = wave & 1;
 
-  // ---- global -> LDS load geometry ---------------------------------------
-  // Wave w fills tile rows [64w, 64w+64) of A and of B, eight rows per
-  // instruction; lane l of instruction j writes LDS chunk (l & 7) of row
-  // 64w + 8j + (l >> 3), which holds logical K-chunk (l & 7) ^ swz(row).
-  const uint16_t* A = static_cast<const uint16_t*>(p.A);
-  const uint16_t* Bm = static_cast<const uint16_t*>(p.B);
   uint16_t* C = static_cast<uint16_t*>(p.C);
   const uint16_t* R = static_cast<const uint16_t*>(p.R);
-  const uint16_t* a_ptr[8];
-  const uint16_t* b_ptr[8];
-#pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    const int row = wave * 64 + j * 8 + (lane >> 3);
-    const int lc = (lane & 7) ^ (lane >> 3) ^ (j & 1);
-    int ga = m0 + row;
-    ga = ga < M ? ga : M - 1;
-    a_ptr[j] = A + (size_t)ga * p.lda + lc * 8;
-    b_ptr[j] = Bm + (size_t)(n0 + row) * p.ldb + lc * 8;
-  }
-  lds_u8_t* lds = (lds_u8_t*)smem;
 
-  auto issue_stage = [&](int stage, int k0) {
-    lds_u8_t* sa = lds + stage * STAGE_BYTES + wave * 64 * ROW_BYTES;
-    lds_u8_t* sb = sa + BM * ROW_BYTES;
+  // ---- global -> register -> LDS staging -----------------------------------
+  // Thread t moves 16-byte chunks c = t + 256 i (i < 8) of each 256x64 operand
+  // tile: tile row c / 8, K-chunk c % 8 -- eight consecutive threads read one
+  // 128-byte row segment.  In LDS the chunk lands at position chunk ^ swz(row).
+  const int srow = tid >> 3;          // + 32 i
+  const int schunk = tid & 7;
+  // 32-bit byte offsets from the uniform bases (operands are < 4 GiB); rows of
+  // A past M re-read row M-1 (never stored).  swz(row) is the same for
+  // row = srow + 32 i, so the LDS slot is one base plus an immediate.
+  const char* Ab = static_cast<const char*>(p.A);
+  const char* Bb = static_cast<const char*>(p.B);
+  uint32_t a_off[8];
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      __builtin_amdgcn_global_load_lds((const glb_void_t*)(a_ptr[j] + k0),
-                                       (lds_void_t*)(sa + j * 8 * ROW_BYTES), 16, 0, 0);
-    }
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      __builtin_amdgcn_global_load_lds((const glb_void_t*)(b_ptr[j] + k0),
-                                       (lds_void_t*)(sb + j * 8 * ROW_BYTES), 16, 0, 0);
-    }
-  };
+  for (int i = 0; i < 8; ++i) {
+    int ga = m0 + srow + 32 * i;
+    ga = ga < M ? ga : M - 1;
+    a_off[i] = (uint32_t)ga * (uint32_t)p.lda * 2u + (uint32_t)schunk * 16u;
+  }
+  const uint32_t b_off = (uint32_t)(n0 + srow) * (uint32_t)p.ldb * 2u + (uint32_t)schunk * 16u;
+  const uint32_t b_step = 32u * (uint32_t)p.ldb * 2u;
+  const int s_off = srow * ROW_BYTES + ((schunk ^ swz(srow)) << 4);
+  u32x4_t ra[8], rb[8];
 
   f32x16_t acc[4][4];
 #pragma unroll
@@ -122,34 +118,79 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmParams p) {
   const int fr = lane & 31;
   const int fsw = swz(fr);
   const int fhalf = lane >> 5;
+  const int a_row0 = (wm * 128 + fr) * ROW_BYTES;
+  const int b_row0 = BM * ROW_BYTES + (wn * 128 + fr) * ROW_BYTES;
+
+  bf16x8_t af[2][4], bfr[2][4];
 
   const int KT = p.K / BK;
-  issue_stage(0, 0);
+  {
+      const char* ak_ = Ab + (size_t)(0) * 2;
+      const char* bk_ = Bb + (size_t)(0) * 2;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) ra[i] = *reinterpret_cast<const u32x4_t*>(ak_ + a_off[i]);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) rb[i] = *reinterpret_cast<const u32x4_t*>(bk_ + b_off + i * b_step);
+    }
+  {
+      uint8_t* sa_ = smem + (0) * STAGE_BYTES + s_off;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) *reinterpret_cast<u32x4_t*>(sa_ + i * 32 * ROW_BYTES) = ra[i];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) *reinterpret_cast<u32x4_t*>(sa_ + (BM + i * 32) * ROW_BYTES) = rb[i];
+    }
+  __syncthreads();
   for (int kt = 0; kt < KT; ++kt) {
-    __syncthreads();  // stage kt landed; stage kt+1 is free
-    if (kt + 1 < KT) issue_stage((kt + 1) & 1, (kt + 1) * BK);
-    const uint8_t* sa = smem + (kt & 1) * STAGE_BYTES;
-    const uint8_t* sb = sa + BM * ROW_BYTES;
+    // Unconditional (no branch for the compiler to merge the load into): the
+    // last iteration re-reads the final K tile into the idle stage.
+    const int knext = (kt + 1 < KT ? kt + 1 : kt) * BK;
+    {
+      const char* ak_ = Ab + (size_t)(knext) * 2;
+      const char* bk_ = Bb + (size_t)(knext) * 2;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) ra[i] = *reinterpret_cast<const u32x4_t*>(ak_ + a_off[i]);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) rb[i] = *reinterpret_cast<const u32x4_t*>(bk_ + b_off + i * b_step);
+    }
+    const uint8_t* st = smem + (kt & 1) * STAGE_BYTES;
+    {
+      const int chunk_ = ((2 * (0) + fhalf) ^ fsw) << 4;
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        af[0][i] = as_bf16x8(*reinterpret_cast<const uint4*>(st + a_row0 + i * 32 * ROW_BYTES + chunk_));
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        bfr[0][j] = as_bf16x8(*reinterpret_cast<const uint4*>(st + b_row0 + j * 32 * ROW_BYTES + chunk_));
+    }
+    // keep the scheduler from sinking the loads into the LDS writes below
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks) {
-      const int chunk = ((2 * ks + fhalf) ^ fsw) * 16;
-      bf16x8_t af[4], bf[4];
+      const int cur = ks & 1;
+      if (ks + 1 < 4) {
+      const int chunk_ = ((2 * (ks + 1) + fhalf) ^ fsw) << 4;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int row = wm * 128 + i * 32 + fr;
-        af[i] = as_bf16x8(*reinterpret_cast<const uint4*>(sa + row * ROW_BYTES + chunk));
-      }
+      for (int i = 0; i < 4; ++i)
+        af[cur ^ 1][i] = as_bf16x8(*reinterpret_cast<const uint4*>(st + a_row0 + i * 32 * ROW_BYTES + chunk_));
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int row = wn * 128 + j * 32 + fr;
-        bf[j] = as_bf16x8(*reinterpret_cast<const uint4*>(sb + row * ROW_BYTES + chunk));
-      }
+      for (int j = 0; j < 4; ++j)
+        bfr[cur ^ 1][j] = as_bf16x8(*reinterpret_cast<const uint4*>(st + b_row0 + j * 32 * ROW_BYTES + chunk_));
+    }
 #pragma unroll
       for (int i = 0; i < 4; ++i)
 #pragma unroll
         for (int j = 0; j < 4; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bf[j], acc[i][j], 0, 0, 0);
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[cur][i], bfr[cur][j], acc[i][j], 0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
     }
+    {
+      uint8_t* sa_ = smem + (((kt + 1) & 1)) * STAGE_BYTES + s_off;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) *reinterpret_cast<u32x4_t*>(sa_ + i * 32 * ROW_BYTES) = ra[i];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) *reinterpret_cast<u32x4_t*>(sa_ + (BM + i * 32) * ROW_BYTES) = rb[i];
+    }
+    __syncthreads();
   }
 
   // ---- epilogue -----------------------------------------------------------

@@ -130,11 +130,11 @@ int seer_layer_workspace_offsets(const seer_dims* dims, int32_t max_rows, size_t
   return ok();
 }
 
-int seer_layer_forward_varlen(const seer_dims* dims, const void* w_packed, const void* x_in,
+static int layer_forward_impl(const seer_dims* dims, const void* w_packed, const void* x_in,
                               void* x_out, int32_t total_rows_ub, const int32_t* cu_seqlens,
                               const int32_t* seqused, int32_t batch, float act_eps,
                               int32_t* act_count, void* workspace, size_t workspace_bytes,
-                              hipStream_t stream) {
+                              hipStream_t stream, hipEvent_t* ev) {
   int rc = check_dims(dims);
   if (rc) return rc;
   if (!w_packed || !x_in || !x_out || !cu_seqlens || !workspace)
@@ -165,10 +165,13 @@ int seer_layer_forward_varlen(const seer_dims* dims, const void* w_packed, const
   const uint8_t* wb = static_cast<const uint8_t*>(w_packed);
   auto gemm = bf16 ? seer::launch_gemm_bf16 : seer::launch_gemm_f32;
 
+  auto mark = [&](int k) { return ev ? hipEventRecord(ev[k], stream) : hipSuccess; };
+  if (mark(0) != hipSuccess) return hip_fail("event record");
   // 1. RMSNorm statistics of the layer input
   if (seer::launch_rms_inv(bf16, x_in, d, d, m_ptr, R, dims->rms_eps, inv1, stream))
     return hip_fail("rms launch");
   // 2. QKV projection, RMSNorm folded in as a row scale
+  if (mark(1) != hipSuccess) return hip_fail("event record");
   {
     seer::GemmParams g{};
     g.A = x_in; g.B = wb + P.qkv * es; g.C = qkv; g.rs = inv1;
@@ -177,6 +180,7 @@ int seer_layer_forward_varlen(const seer_dims* dims, const void* w_packed, const
     if (gemm(seer::EPI_SCALE, g, stream)) return hip_fail("qkv gemm launch");
   }
   // 3. bidirectional varlen attention
+  if (mark(2) != hipSuccess) return hip_fail("event record");
   {
     seer::AttnParams a{};
     a.qkv = qkv; a.out = o; a.cu = cu_seqlens; a.used = seqused; a.B = batch;
@@ -186,6 +190,7 @@ int seer_layer_forward_varlen(const seer_dims* dims, const void* w_packed, const
       return hip_fail("attention launch");
   }
   // 4. output projection + residual
+  if (mark(3) != hipSuccess) return hip_fail("event record");
   {
     seer::GemmParams g{};
     g.A = o; g.B = wb + P.o * es; g.C = h1; g.R = x_in;
@@ -194,6 +199,7 @@ int seer_layer_forward_varlen(const seer_dims* dims, const void* w_packed, const
     if (gemm(seer::EPI_RESID, g, stream)) return hip_fail("o gemm launch");
   }
   // 5. RMSNorm statistics before the MLP
+  if (mark(4) != hipSuccess) return hip_fail("event record");
   if (seer::launch_rms_inv(bf16, h1, d, d, m_ptr, R, dims->rms_eps, inv2, stream))
     return hip_fail("rms launch");
   // 6. gate/up projection + SwiGLU (+ near-zero count)
@@ -210,10 +216,12 @@ int seer_layer_forward_varlen(const seer_dims* dims, const void* w_packed, const
       g.B2 = wb + (P.gu + (size_t)I * d) * es;
       g.N = I;
     }
+    if (mark(5) != hipSuccess) return hip_fail("event record");
     if (gemm(act_count ? seer::EPI_SWIGLU_COUNT : seer::EPI_SWIGLU, g, stream))
       return hip_fail("gate/up gemm launch");
   }
   // 7. down projection + residual
+  if (mark(6) != hipSuccess) return hip_fail("event record");
   {
     seer::GemmParams g{};
     g.A = act; g.B = wb + P.dn * es; g.C = x_out; g.R = h1;
@@ -221,7 +229,29 @@ int seer_layer_forward_varlen(const seer_dims* dims, const void* w_packed, const
     g.lda = I; g.ldb = I; g.ldc = d; g.ldr = d;
     if (gemm(seer::EPI_RESID, g, stream)) return hip_fail("down gemm launch");
   }
+  if (mark(7) != hipSuccess) return hip_fail("event record");
   return ok();
+}
+
+int seer_layer_forward_varlen(const seer_dims* dims, const void* w_packed, const void* x_in,
+                              void* x_out, int32_t total_rows_ub, const int32_t* cu_seqlens,
+                              const int32_t* seqused, int32_t batch, float act_eps,
+                              int32_t* act_count, void* workspace, size_t workspace_bytes,
+                              hipStream_t stream) {
+  return layer_forward_impl(dims, w_packed, x_in, x_out, total_rows_ub, cu_seqlens, seqused, batch,
+                            act_eps, act_count, workspace, workspace_bytes, stream, nullptr);
+}
+
+int seer_layer_forward_varlen_timed(const seer_dims* dims, const void* w_packed, const void* x_in,
+                                    void* x_out, int32_t total_rows_ub, const int32_t* cu_seqlens,
+                                    const int32_t* seqused, int32_t batch, float act_eps,
+                                    int32_t* act_count, void* workspace, size_t workspace_bytes,
+                                    hipStream_t stream, hipEvent_t* events) {
+  if (!events) return fail(SEER_EINVAL, "events is NULL");
+  for (int k = 0; k < 8; ++k)
+    if (!events[k]) return fail(SEER_EINVAL, "events[%d] is NULL", k);
+  return layer_forward_impl(dims, w_packed, x_in, x_out, total_rows_ub, cu_seqlens, seqused, batch,
+                            act_eps, act_count, workspace, workspace_bytes, stream, events);
 }
 
 int seer_step0_detect(const int32_t* act_count, const int32_t* cu_seqlens, const int32_t* win_off,

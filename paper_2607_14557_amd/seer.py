@@ -18,7 +18,8 @@ SEER_ROUTE_HYBRID, SEER_ROUTE_NAIVE_PAD, SEER_ROUTE_VARLEN_ONLY = 0, 1, 2
 SEER_PATH_STATIC, SEER_PATH_VARLEN, SEER_PATH_EAGER = 0, 1, 2
 
 EXPORTED = ("seer_prepacked_bytes", "seer_prepack_weights", "seer_layer_workspace_bytes",
-            "seer_layer_workspace_offsets", "seer_layer_forward_varlen", "seer_step0_detect", "seer_batch_repack",
+            "seer_layer_workspace_offsets", "seer_layer_forward_varlen",
+            "seer_layer_forward_varlen_timed", "seer_step0_detect", "seer_batch_repack",
             "seer_last_error", "seer_abi_version")
 
 
@@ -69,6 +70,9 @@ def load_library():
     global _lib
     if _lib is not None:
         return _lib
+    # torch first: its HIP runtime carries the same soname, so the library binds
+    # to the runtime that owns torch's streams and allocations.
+    import torch  # noqa: F401
     if not os.path.exists(LIB_PATH):
         raise RuntimeError("libseer.so is not built (%s); run `python -m paper_2607_14557_amd.build`"
                            % LIB_PATH)
@@ -86,6 +90,9 @@ def load_library():
     L.seer_layer_forward_varlen.argtypes = [ctypes.POINTER(seer_dims), _P, _P, _P, _I, _P, _P, _I,
                                             ctypes.c_float, _P, _P, ctypes.c_size_t, _P]
     L.seer_layer_forward_varlen.restype = ctypes.c_int
+    L.seer_layer_forward_varlen_timed.argtypes = L.seer_layer_forward_varlen.argtypes + [
+        ctypes.POINTER(_P)]
+    L.seer_layer_forward_varlen_timed.restype = ctypes.c_int
     L.seer_step0_detect.argtypes = [_P, _P, _P, _P, _I, _I, ctypes.POINTER(seer_snr_params), _P, _P, _P]
     L.seer_step0_detect.restype = ctypes.c_int
     L.seer_batch_repack.argtypes = [ctypes.POINTER(seer_repack_desc), ctypes.POINTER(_P),
@@ -161,6 +168,18 @@ def seer_layer_forward_varlen(dims, w_packed, x_in, x_out, total_rows_ub, cu_seq
         ctypes.byref(dims), _ptr(w_packed), _ptr(x_in), _ptr(x_out), int(total_rows_ub),
         _ptr(cu_seqlens), _ptr(seqused), int(batch), float(act_eps), _ptr(act_count),
         _ptr(workspace), nbytes, _stream(stream)))
+
+
+def seer_layer_forward_varlen_timed(dims, w_packed, x_in, x_out, total_rows_ub, cu_seqlens,
+                                    seqused, batch, act_eps, act_count, workspace, events,
+                                    workspace_bytes=None, stream=None):
+    """events: sequence of 8 raw hipEvent_t handles (ints)."""
+    nbytes = workspace_bytes if workspace_bytes is not None else workspace.numel() * workspace.element_size()
+    ev = (_P * 8)(*events)
+    _check(load_library().seer_layer_forward_varlen_timed(
+        ctypes.byref(dims), _ptr(w_packed), _ptr(x_in), _ptr(x_out), int(total_rows_ub),
+        _ptr(cu_seqlens), _ptr(seqused), int(batch), float(act_eps), _ptr(act_count),
+        _ptr(workspace), nbytes, _stream(stream), ev))
 
 
 def seer_step0_detect(act_count, cu_seqlens, win_off, win_len, batch, d_ff, params, boundary,
