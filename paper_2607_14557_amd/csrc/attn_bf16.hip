@@ -13,7 +13,10 @@
 // per-lane values and the probabilities already sit in the B-operand layout
 // of the next product O^T = V^T P^T -- no shuffle of P through LDS.  V is
 // transposed while it is written to LDS, with keys permuted inside each group
-// of 16 so that every lane's eight keys are one 16-byte read.
+// of 16 so that every lane's eight keys are one 16-byte read.  The P V product
+// runs in fp16: bf16 values of V convert to fp16 exactly (magnitudes inside
+// fp16's normal range) and the probabilities keep three more mantissa bits
+// than bf16 would give them.
 #include <math.h>
 
 #include "common.h"
@@ -132,10 +135,10 @@ __global__ __launch_bounds__(NT, 2) void attn_bf16_kernel(AttnParams p) {
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
       const int sh = (e & 1) * 16;
-      const uint32_t k0 = (vreg[0][e / 2] >> sh) & 0xffffu;
-      const uint32_t k1 = (vreg[1][e / 2] >> sh) & 0xffffu;
-      const uint32_t k2 = (vreg[2][e / 2] >> sh) & 0xffffu;
-      const uint32_t k3 = (vreg[3][e / 2] >> sh) & 0xffffu;
+      const uint32_t k0 = bf_to_h_bits((vreg[0][e / 2] >> sh) & 0xffffu);
+      const uint32_t k1 = bf_to_h_bits((vreg[1][e / 2] >> sh) & 0xffffu);
+      const uint32_t k2 = bf_to_h_bits((vreg[2][e / 2] >> sh) & 0xffffu);
+      const uint32_t k3 = bf_to_h_bits((vreg[3][e / 2] >> sh) & 0xffffu);
       const int dim = vdc * 8 + e;
       const int ch = (pos >> 3) ^ swz8(dim);
       uint2 v;
@@ -205,18 +208,18 @@ __global__ __launch_bounds__(NT, 2) void attn_bf16_kernel(AttnParams p) {
 #pragma unroll
       for (int hf = 0; hf < 2; ++hf) {
         uint4 pk;
-        pk.x = pack_bf2(s[i][hf * 8 + 0], s[i][hf * 8 + 1]);
-        pk.y = pack_bf2(s[i][hf * 8 + 2], s[i][hf * 8 + 3]);
-        pk.z = pack_bf2(s[i][hf * 8 + 4], s[i][hf * 8 + 5]);
-        pk.w = pack_bf2(s[i][hf * 8 + 6], s[i][hf * 8 + 7]);
-        const bf16x8_t pf = as_bf16x8(pk);
+        pk.x = pack_h2(s[i][hf * 8 + 0], s[i][hf * 8 + 1]);
+        pk.y = pack_h2(s[i][hf * 8 + 2], s[i][hf * 8 + 3]);
+        pk.z = pack_h2(s[i][hf * 8 + 4], s[i][hf * 8 + 5]);
+        pk.w = pack_h2(s[i][hf * 8 + 6], s[i][hf * 8 + 7]);
+        const f16x8_t pf = as_f16x8(pk);
         const int chunk = i * 4 + hf * 2 + fhalf;
 #pragma unroll
         for (int dt = 0; dt < 4; ++dt) {
           const int dim = dt * 32 + fr;
           const int ch = chunk ^ swz8(dim);
-          const bf16x8_t vf = as_bf16x8(*reinterpret_cast<const uint4*>(v_lds + dim * V_ROW + ch * 16));
-          o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf, o[dt], 0, 0, 0);
+          const f16x8_t vf = as_f16x8(*reinterpret_cast<const uint4*>(v_lds + dim * V_ROW + ch * 16));
+          o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_f16(vf, pf, o[dt], 0, 0, 0);
         }
       }
     }

@@ -7,6 +7,7 @@
 namespace seer {
 
 typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8_t;
+typedef __attribute__((__vector_size__(8 * sizeof(_Float16)))) _Float16 f16x8_t;
 typedef __attribute__((__vector_size__(16 * sizeof(float)))) float f32x16_t;
 typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4_t;
 
@@ -40,6 +41,24 @@ __device__ __forceinline__ uint32_t pack_bf2(float lo, float hi) {
 
 __device__ __forceinline__ bf16x8_t as_bf16x8(uint4 v) {
   return __builtin_bit_cast(bf16x8_t, v);
+}
+
+__device__ __forceinline__ f16x8_t as_f16x8(uint4 v) {
+  return __builtin_bit_cast(f16x8_t, v);
+}
+
+// fp32 -> fp16, round to nearest even.
+__device__ __forceinline__ uint32_t f2h_bits(float f) {
+  return static_cast<uint32_t>(__builtin_bit_cast(uint16_t, static_cast<_Float16>(f)));
+}
+
+__device__ __forceinline__ uint32_t pack_h2(float lo, float hi) {
+  return f2h_bits(lo) | (f2h_bits(hi) << 16);
+}
+
+// bf16 bits -> fp16 bits (exact for magnitudes in fp16's normal range).
+__device__ __forceinline__ uint32_t bf_to_h_bits(uint32_t bf) {
+  return f2h_bits(__uint_as_float(bf << 16));
 }
 
 __device__ __forceinline__ float silu(float z) {

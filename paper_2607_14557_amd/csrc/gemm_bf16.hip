@@ -14,7 +14,9 @@
 //
 // Epilogues:
 //   SCALE   C = bf16(acc * rowscale[r])         folded RMSNorm before QKV
-//   RESID   C = bf16(R[r,c] + acc)              residual after O and down
+//   RESID   C = bf16(R[r,c] + acc)              residual add
+//   RESID_DUAL  as RESID, plus an fp32 copy     residual after O (h1 kept in fp32)
+//   RESID_R32   C = bf16(R32[r,c] + acc)        residual after down, fp32 h1
 //   SWIGLU  act = silu(acc_g * s) * (acc_u * s) gate/up with folded RMSNorm;
 //           the packed weight interleaves 32 gate rows with 32 up rows, so a
 //           wave holds matching gate and up columns in its registers
@@ -197,7 +199,7 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmParams p) {
   // Accumulator register r of a 32x32 tile holds row 8*(r/4) + 4*(lane/32) + r%4
   // and column lane%32.
   const int row_base = m0 + wm * 128 + fhalf * 4;
-  if constexpr (EPI == EPI_SCALE || EPI == EPI_RESID) {
+  if constexpr (EPI == EPI_SCALE || EPI == EPI_RESID || EPI == EPI_RESID_DUAL || EPI == EPI_RESID_R32) {
     const int col_base = n0 + wn * 128 + fr;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
@@ -210,11 +212,26 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmParams p) {
 #pragma unroll
             for (int j = 0; j < 4; ++j)
               C[(size_t)row * p.ldc + col_base + j * 32] = f2bf(acc[i][j][r] * s);
-          } else {
+          } else if constexpr (EPI == EPI_RESID) {
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
               const size_t c = col_base + j * 32;
               C[(size_t)row * p.ldc + c] = f2bf(bf2f(R[(size_t)row * p.ldr + c]) + acc[i][j][r]);
+            }
+          } else if constexpr (EPI == EPI_RESID_DUAL) {
+            float* C2 = static_cast<float*>(p.C2);
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+              const size_t c = col_base + j * 32;
+              const float v = bf2f(R[(size_t)row * p.ldr + c]) + acc[i][j][r];
+              C[(size_t)row * p.ldc + c] = f2bf(v);
+              C2[(size_t)row * p.ldc + c] = v;
+            }
+          } else {
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+              const size_t c = col_base + j * 32;
+              C[(size_t)row * p.ldc + c] = f2bf(p.R32[(size_t)row * p.ldr + c] + acc[i][j][r]);
             }
           }
         }
@@ -261,6 +278,10 @@ int launch_gemm_bf16(int epi, const GemmParams& p, hipStream_t s) {
     case EPI_SWIGLU: hipLaunchKernelGGL(gemm_bf16_kernel<EPI_SWIGLU>, grid, block, 0, s, p); break;
     case EPI_SWIGLU_COUNT:
       hipLaunchKernelGGL(gemm_bf16_kernel<EPI_SWIGLU_COUNT>, grid, block, 0, s, p); break;
+    case EPI_RESID_DUAL:
+      hipLaunchKernelGGL(gemm_bf16_kernel<EPI_RESID_DUAL>, grid, block, 0, s, p); break;
+    case EPI_RESID_R32:
+      hipLaunchKernelGGL(gemm_bf16_kernel<EPI_RESID_R32>, grid, block, 0, s, p); break;
     default: return -1;
   }
   return hipGetLastError() == hipSuccess ? 0 : -1;

@@ -6,7 +6,12 @@
 
 namespace seer {
 
-enum Epilogue { EPI_SCALE = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_SWIGLU_COUNT = 3 };
+// SCALE: C = acc * rs[r]; RESID: C = R + acc; SWIGLU(_COUNT): gate/up pairs;
+// RESID_DUAL: C = bf16(R + acc) and C2 = fp32(R + acc); RESID_R32: C = bf16(R32 + acc).
+enum Epilogue {
+  EPI_SCALE = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_SWIGLU_COUNT = 3,
+  EPI_RESID_DUAL = 4, EPI_RESID_R32 = 5
+};
 
 // C[M,N] = A[M,K] * B[N,K]^T with a fused epilogue.  M is read on the device
 // from m_ptr (clamped to m_ub, the bound the grid is sized from).
@@ -14,7 +19,9 @@ struct GemmParams {
   const void* A;
   const void* B;
   void* C;
-  const void* R;      // residual rows (RESID), same element type as C
+  const void* R;      // residual rows (RESID*), same element type as C
+  void* C2;           // fp32 copy of the output (RESID_DUAL)
+  const float* R32;   // fp32 residual rows (RESID_R32), leading dimension ldr
   const float* rs;    // per-row scale (SCALE, SWIGLU*)
   int* cnt;           // per-row near-zero count (SWIGLU_COUNT)
   float eps;

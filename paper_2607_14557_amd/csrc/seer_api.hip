@@ -61,7 +61,7 @@ int check_dims(const seer_dims* d) {
 }
 
 struct WsLayout {
-  size_t qkv, o, h1, act, inv1, inv2, total;
+  size_t qkv, o, h1, act, inv1, inv2, h1f, total;
 };
 
 WsLayout ws_layout(const seer_dims* d, int rows) {
@@ -75,6 +75,9 @@ WsLayout ws_layout(const seer_dims* d, int rows) {
   L.act = off; off = up256(off + R * d->d_ff * es);
   L.inv1 = off; off = up256(off + R * 4);
   L.inv2 = off; off = up256(off + R * 4);
+  // bf16 layers keep an fp32 copy of h1 for the final residual add
+  L.h1f = d->dtype == SEER_DTYPE_BF16 ? off : L.h1;
+  if (d->dtype == SEER_DTYPE_BF16) off = up256(off + R * d->d_model * 4);
   L.total = off;
   return L;
 }
@@ -120,13 +123,14 @@ size_t seer_layer_workspace_bytes(const seer_dims* dims, int32_t max_rows) {
   return ws_layout(dims, max_rows).total;
 }
 
-int seer_layer_workspace_offsets(const seer_dims* dims, int32_t max_rows, size_t offsets[6]) {
+int seer_layer_workspace_offsets(const seer_dims* dims, int32_t max_rows, size_t offsets[8]) {
   int rc = check_dims(dims);
   if (rc) return rc;
   if (!offsets || max_rows < 0) return fail(SEER_EINVAL, "offsets is NULL or max_rows < 0");
   const WsLayout L = ws_layout(dims, max_rows);
   offsets[0] = L.qkv; offsets[1] = L.o; offsets[2] = L.h1;
   offsets[3] = L.act; offsets[4] = L.inv1; offsets[5] = L.inv2;
+  offsets[6] = L.h1f; offsets[7] = L.total;
   return ok();
 }
 
@@ -159,6 +163,7 @@ static int layer_forward_impl(const seer_dims* dims, const void* w_packed, const
   void* act = ws + L.act;
   float* inv1 = reinterpret_cast<float*>(ws + L.inv1);
   float* inv2 = reinterpret_cast<float*>(ws + L.inv2);
+  float* h1f = reinterpret_cast<float*>(ws + L.h1f);
   const int* m_ptr = cu_seqlens + batch;
   const seer::PackedLayout P = seer::packed_layout(d, I, bf16);
   const size_t es = bf16 ? 2 : 4;
@@ -193,10 +198,10 @@ static int layer_forward_impl(const seer_dims* dims, const void* w_packed, const
   if (mark(3) != hipSuccess) return hip_fail("event record");
   {
     seer::GemmParams g{};
-    g.A = o; g.B = wb + P.o * es; g.C = h1; g.R = x_in;
+    g.A = o; g.B = wb + P.o * es; g.C = h1; g.R = x_in; g.C2 = h1f;
     g.m_ptr = m_ptr; g.m_ub = R; g.N = d; g.K = d;
     g.lda = d; g.ldb = d; g.ldc = d; g.ldr = d;
-    if (gemm(seer::EPI_RESID, g, stream)) return hip_fail("o gemm launch");
+    if (gemm(bf16 ? seer::EPI_RESID_DUAL : seer::EPI_RESID, g, stream)) return hip_fail("o gemm launch");
   }
   // 5. RMSNorm statistics before the MLP
   if (mark(4) != hipSuccess) return hip_fail("event record");
@@ -224,10 +229,10 @@ static int layer_forward_impl(const seer_dims* dims, const void* w_packed, const
   if (mark(6) != hipSuccess) return hip_fail("event record");
   {
     seer::GemmParams g{};
-    g.A = act; g.B = wb + P.dn * es; g.C = x_out; g.R = h1;
+    g.A = act; g.B = wb + P.dn * es; g.C = x_out; g.R = h1; g.R32 = h1f;
     g.m_ptr = m_ptr; g.m_ub = R; g.N = d; g.K = I;
     g.lda = I; g.ldb = I; g.ldc = d; g.ldr = d;
-    if (gemm(seer::EPI_RESID, g, stream)) return hip_fail("down gemm launch");
+    if (gemm(bf16 ? seer::EPI_RESID_R32 : seer::EPI_RESID, g, stream)) return hip_fail("down gemm launch");
   }
   if (mark(7) != hipSuccess) return hip_fail("event record");
   return ok();

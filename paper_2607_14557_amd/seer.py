@@ -154,8 +154,8 @@ def seer_layer_workspace_bytes(dims, max_rows):
 
 
 def seer_layer_workspace_offsets(dims, max_rows):
-    """Returns the six byte offsets as a list."""
-    off = (ctypes.c_size_t * 6)()
+    """Returns the eight byte offsets as a list."""
+    off = (ctypes.c_size_t * 8)()
     _check(load_library().seer_layer_workspace_offsets(ctypes.byref(dims), int(max_rows), off))
     return list(off)
 

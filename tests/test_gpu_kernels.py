@@ -199,9 +199,11 @@ class _Layer:
         return out, cnt
 
     def inter(self, name, rows, cols=None):
-        idx = {"qkv": 0, "o": 1, "h1": 2, "act": 3, "inv1": 4, "inv2": 5}[name]
+        idx = {"qkv": 0, "o": 1, "h1": 2, "act": 3, "inv1": 4, "inv2": 5, "h1f": 6}[name]
         if name.startswith("inv"):
             return view_ws_f32(self.ws, self.off[idx], rows)
+        if name == "h1f":
+            return view_ws(self.ws, self.off[idx], rows, cols, "f32")
         return view_ws(self.ws, self.off[idx], rows, cols, self.dtype)
 
 
@@ -253,7 +255,15 @@ def test_layer_vs_oracle_ragged(S, dtype):
         # the fp32 activations are stored unrounded: the kernel's count must be
         # exactly the count of its own activations
         np.testing.assert_array_equal(host(cnt)[:T], near_zero_count(act, eps))
-    assert rel_err(y[:T], h1 + act @ W["wd"].T) <= tol
+    # the final residual add uses the unrounded h1
+    h1f = host(L.inter("h1f", T, d))
+    assert rel_err(h1f, x[:T] + o @ W["wo"].T) <= (1e-5 if dtype == "bf16" else tol)
+    e_dn = rel_err(y[:T], h1f + act @ W["wd"].T)
+    log("  stage errors (teacher-forced): qkv %.2e attn %.2e act %.2e down %.2e" %
+        (rel_err(qkv, qkv_ref), max(rel_err(o[cu[b]:cu[b + 1]], attention_seq(
+            qkv[cu[b]:cu[b + 1], :d], qkv[cu[b]:cu[b + 1], d:2 * d], qkv[cu[b]:cu[b + 1], 2 * d:], H))
+            for b in range(len(lens))), rel_err(act, act_ref), e_dn))
+    assert e_dn <= tol
 
 
 def test_layer_static_padding_equals_cut_layout_bitwise(S):
