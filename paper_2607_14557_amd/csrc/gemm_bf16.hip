@@ -105,8 +105,6 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmParams p) {
   const uint32_t b_off = (uint32_t)(n0 + srow) * (uint32_t)p.ldb * 2u + (uint32_t)schunk * 16u;
   const uint32_t b_step = 32u * (uint32_t)p.ldb * 2u;
   const int s_off = srow * ROW_BYTES + ((schunk ^ swz(srow)) << 4);
-  u32x4_t ra[8], rb[8];
-
   f32x16_t acc[4][4];
 #pragma unroll
   for (int i = 0; i < 4; ++i)
@@ -123,77 +121,96 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmParams p) {
   const int a_row0 = (wm * 128 + fr) * ROW_BYTES;
   const int b_row0 = BM * ROW_BYTES + (wn * 128 + fr) * ROW_BYTES;
 
+  // Software pipeline, two K tiles of look-ahead: while tile t is multiplied
+  // out of LDS stage t%2, tile t+1 (loaded into registers one iteration
+  // earlier) is written into stage (t+1)%2 between the MFMAs, and the loads of
+  // tile t+2 are in flight.  Two register sets alternate, so the loop is
+  // unrolled by two; K/64 is even for every shape the bf16 path accepts.
+  u32x4_t ra0[8], rb0[8], ra1[8], rb1[8];
   bf16x8_t af[2][4], bfr[2][4];
-
   const int KT = p.K / BK;
+
+#define SEER_GLOAD(RA, RB, T)                                                       \
+  {                                                                                 \
+    const int t_ = (T) < KT ? (T) : KT - 1;                                         \
+    const char* ak_ = Ab + (size_t)t_ * (BK * 2);                                   \
+    const char* bk_ = Bb + (size_t)t_ * (BK * 2);                                   \
+    _Pragma("unroll") for (int i = 0; i < 8; ++i)                                   \
+      RA[i] = *reinterpret_cast<const u32x4_t*>(ak_ + a_off[i]);                    \
+    _Pragma("unroll") for (int i = 0; i < 8; ++i)                                   \
+      RB[i] = *reinterpret_cast<const u32x4_t*>(bk_ + b_off + i * b_step);          \
+  }
+#define SEER_LSTORE2(RA, RB, STG, I0)                                               \
+  {                                                                                 \
+    uint8_t* sa_ = smem + (STG) * STAGE_BYTES + s_off;                              \
+    *reinterpret_cast<u32x4_t*>(sa_ + ((I0) + 0) * 32 * ROW_BYTES) = RA[(I0) + 0];  \
+    *reinterpret_cast<u32x4_t*>(sa_ + ((I0) + 1) * 32 * ROW_BYTES) = RA[(I0) + 1];  \
+    *reinterpret_cast<u32x4_t*>(sa_ + (BM + ((I0) + 0) * 32) * ROW_BYTES) = RB[(I0) + 0];  \
+    *reinterpret_cast<u32x4_t*>(sa_ + (BM + ((I0) + 1) * 32) * ROW_BYTES) = RB[(I0) + 1];  \
+  }
+#define SEER_FLOAD(ST, KS, BUF)                                                     \
+  {                                                                                 \
+    const int chunk_ = ((2 * (KS) + fhalf) ^ fsw) << 4;                             \
+    _Pragma("unroll") for (int i = 0; i < 4; ++i)                                   \
+      af[BUF][i] = __builtin_bit_cast(bf16x8_t,                                     \
+          *reinterpret_cast<const u32x4_t*>((ST) + a_row0 + i * 32 * ROW_BYTES + chunk_)); \
+    _Pragma("unroll") for (int j = 0; j < 4; ++j)                                   \
+      bfr[BUF][j] = __builtin_bit_cast(bf16x8_t,                                    \
+          *reinterpret_cast<const u32x4_t*>((ST) + b_row0 + j * 32 * ROW_BYTES + chunk_)); \
+  }
+  // One K tile: 4 slices x 16 MFMAs; slice ks+1's fragments are read while
+  // slice ks multiplies; two rows of the staged next tile go to LDS per slice.
+#define SEER_TILE(T, RA, RB)                                                        \
+  {                                                                                 \
+    const uint8_t* st_ = smem + ((T) & 1) * STAGE_BYTES;                            \
+    SEER_FLOAD(st_, 0, 0);                                                          \
+    _Pragma("unroll") for (int ks = 0; ks < 4; ++ks) {                              \
+      const int cur = ks & 1;                                                       \
+      if (ks + 1 < 4) SEER_FLOAD(st_, ks + 1, cur ^ 1);                             \
+      _Pragma("unroll") for (int i = 0; i < 4; ++i)                                 \
+        _Pragma("unroll") for (int j = 0; j < 4; ++j)                               \
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[cur][i], bfr[cur][j], acc[i][j], 0, 0, 0); \
+      SEER_LSTORE2(RA, RB, ((T) + 1) & 1, 2 * ks);                                  \
+      /* per slice: 4 global loads, 8 LDS reads, 4 LDS writes between 16 MFMAs */   \
+      _Pragma("unroll") for (int g = 0; g < 4; ++g) {                               \
+        __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);                          \
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                          \
+      }                                                                             \
+      _Pragma("unroll") for (int g = 0; g < 4; ++g) {                               \
+        __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);                          \
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                          \
+      }                                                                             \
+      _Pragma("unroll") for (int g = 0; g < 4; ++g) {                               \
+        __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);                          \
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                          \
+      }                                                                             \
+      __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);                            \
+    }                                                                               \
+  }
+
+  // prologue: tile 0 -> stage 0, tile 1 in registers (set 1), tile 2 loading (set 0)
+  SEER_GLOAD(ra0, rb0, 0);
+  SEER_GLOAD(ra1, rb1, 1);
   {
-      const char* ak_ = Ab + (size_t)(0) * 2;
-      const char* bk_ = Bb + (size_t)(0) * 2;
+    uint8_t* sa_ = smem + s_off;
 #pragma unroll
-      for (int i = 0; i < 8; ++i) ra[i] = *reinterpret_cast<const u32x4_t*>(ak_ + a_off[i]);
+    for (int i = 0; i < 8; ++i) *reinterpret_cast<u32x4_t*>(sa_ + i * 32 * ROW_BYTES) = ra0[i];
 #pragma unroll
-      for (int i = 0; i < 8; ++i) rb[i] = *reinterpret_cast<const u32x4_t*>(bk_ + b_off + i * b_step);
-    }
-  {
-      uint8_t* sa_ = smem + (0) * STAGE_BYTES + s_off;
-#pragma unroll
-      for (int i = 0; i < 8; ++i) *reinterpret_cast<u32x4_t*>(sa_ + i * 32 * ROW_BYTES) = ra[i];
-#pragma unroll
-      for (int i = 0; i < 8; ++i) *reinterpret_cast<u32x4_t*>(sa_ + (BM + i * 32) * ROW_BYTES) = rb[i];
-    }
+    for (int i = 0; i < 8; ++i) *reinterpret_cast<u32x4_t*>(sa_ + (BM + i * 32) * ROW_BYTES) = rb0[i];
+  }
   __syncthreads();
-  for (int kt = 0; kt < KT; ++kt) {
-    // Unconditional (no branch for the compiler to merge the load into): the
-    // last iteration re-reads the final K tile into the idle stage.
-    const int knext = (kt + 1 < KT ? kt + 1 : kt) * BK;
-    {
-      const char* ak_ = Ab + (size_t)(knext) * 2;
-      const char* bk_ = Bb + (size_t)(knext) * 2;
-#pragma unroll
-      for (int i = 0; i < 8; ++i) ra[i] = *reinterpret_cast<const u32x4_t*>(ak_ + a_off[i]);
-#pragma unroll
-      for (int i = 0; i < 8; ++i) rb[i] = *reinterpret_cast<const u32x4_t*>(bk_ + b_off + i * b_step);
-    }
-    const uint8_t* st = smem + (kt & 1) * STAGE_BYTES;
-    {
-      const int chunk_ = ((2 * (0) + fhalf) ^ fsw) << 4;
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-        af[0][i] = as_bf16x8(*reinterpret_cast<const uint4*>(st + a_row0 + i * 32 * ROW_BYTES + chunk_));
-#pragma unroll
-      for (int j = 0; j < 4; ++j)
-        bfr[0][j] = as_bf16x8(*reinterpret_cast<const uint4*>(st + b_row0 + j * 32 * ROW_BYTES + chunk_));
-    }
-    // keep the scheduler from sinking the loads into the LDS writes below
-    __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-    for (int ks = 0; ks < 4; ++ks) {
-      const int cur = ks & 1;
-      if (ks + 1 < 4) {
-      const int chunk_ = ((2 * (ks + 1) + fhalf) ^ fsw) << 4;
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-        af[cur ^ 1][i] = as_bf16x8(*reinterpret_cast<const uint4*>(st + a_row0 + i * 32 * ROW_BYTES + chunk_));
-#pragma unroll
-      for (int j = 0; j < 4; ++j)
-        bfr[cur ^ 1][j] = as_bf16x8(*reinterpret_cast<const uint4*>(st + b_row0 + j * 32 * ROW_BYTES + chunk_));
-    }
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[cur][i], bfr[cur][j], acc[i][j], 0, 0, 0);
-      __builtin_amdgcn_sched_barrier(0);
-    }
-    {
-      uint8_t* sa_ = smem + (((kt + 1) & 1)) * STAGE_BYTES + s_off;
-#pragma unroll
-      for (int i = 0; i < 8; ++i) *reinterpret_cast<u32x4_t*>(sa_ + i * 32 * ROW_BYTES) = ra[i];
-#pragma unroll
-      for (int i = 0; i < 8; ++i) *reinterpret_cast<u32x4_t*>(sa_ + (BM + i * 32) * ROW_BYTES) = rb[i];
-    }
+  for (int kt = 0; kt < KT; kt += 2) {
+    SEER_GLOAD(ra0, rb0, kt + 2);
+    SEER_TILE(kt, ra1, rb1);
+    __syncthreads();
+    SEER_GLOAD(ra1, rb1, kt + 3);
+    SEER_TILE(kt + 1, ra0, rb0);
     __syncthreads();
   }
+#undef SEER_GLOAD
+#undef SEER_LSTORE2
+#undef SEER_FLOAD
+#undef SEER_TILE
 
   // ---- epilogue -----------------------------------------------------------
   // Accumulator register r of a 32x32 tile holds row 8*(r/4) + 4*(lane/32) + r%4
