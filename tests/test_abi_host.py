@@ -1,0 +1,141 @@
+"""Host-side checks of the C ABI (no GPU): the library loads, exports every
+function include/seer.h declares, and rejects bad arguments with the
+documented status codes before launching anything."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from conftest import ROOT
+
+HEADER = os.path.join(ROOT, "include", "seer.h")
+
+
+@pytest.fixture(scope="module")
+def S():
+    from paper_2607_14557_amd import seer
+    if not os.path.exists(seer.LIB_PATH):
+        pytest.skip("libseer.so not built")
+    seer.load_library()
+    return seer
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(seer_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_every_declared_symbol_is_exported(S):
+    names = declared_functions()
+    assert len(names) >= 9
+    lib = ctypes.CDLL(S.LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), n
+    assert set(names) == set(S.EXPORTED)
+    assert S.seer_abi_version() == 100
+
+
+def dims(S, d=4096, h=32, dh=128, i=12288, dtype=1):
+    return S.seer_dims(d, h, dh, i, dtype, 1e-5)
+
+
+def test_dims_validation(S):
+    assert S.seer_prepacked_bytes(dims(S)) == 436207616
+    assert S.seer_prepacked_bytes(dims(S, dh=64)) == 0
+    assert "head_dim" in S.seer_last_error()
+    assert S.seer_prepacked_bytes(dims(S, d=4000, h=32, dh=125)) == 0     # bf16 needs d % 256
+    assert S.seer_prepacked_bytes(dims(S, d=256, h=4, dh=64, i=688, dtype=2)) > 0
+    assert S.seer_prepacked_bytes(dims(S, dtype=7)) == 0
+
+
+def test_workspace_layout_is_consistent(S):
+    d = dims(S)
+    a = S.seer_layer_workspace_bytes(d, 1000)
+    b = S.seer_layer_workspace_bytes(d, 2000)
+    assert 0 < a < b
+    off = S.seer_layer_workspace_offsets(d, 2000)
+    assert off == sorted(off) and off[7] == b and all(o % 256 == 0 for o in off)
+    # bf16: qkv, o, h1 (bf16), act, two fp32 statistics, h1 fp32
+    assert b >= 2000 * (3 * 4096 * 2 + 4096 * 2 * 2 + 12288 * 2 + 8 + 4096 * 4)
+
+
+FAKE = 1 << 20   # a non-null, aligned address that is never dereferenced
+
+
+def call_layer(S, d, **kw):
+    a = dict(w=FAKE, x_in=FAKE, x_out=FAKE + 4096, rows=100, cu=FAKE, used=None, batch=1,
+             eps=0.0, cnt=None, ws=FAKE, ws_bytes=1 << 40)
+    a.update(kw)
+    L = S.load_library()
+    return L.seer_layer_forward_varlen(ctypes.byref(d), a["w"], a["x_in"], a["x_out"], a["rows"],
+                                       a["cu"], a["used"], a["batch"], a["eps"], a["cnt"], a["ws"],
+                                       a["ws_bytes"], 0)
+
+
+def test_layer_forward_argument_errors(S):
+    d = dims(S)
+    assert call_layer(S, d, w=None) == S.SEER_EINVAL
+    assert call_layer(S, d, cu=None) == S.SEER_EINVAL
+    assert call_layer(S, d, batch=0) == S.SEER_EINVAL
+    assert call_layer(S, d, rows=0) == S.SEER_EINVAL
+    assert call_layer(S, d, x_out=FAKE) == S.SEER_EINVAL          # aliasing
+    assert call_layer(S, d, ws=FAKE + 8) == S.SEER_EINVAL         # misaligned workspace
+    assert call_layer(S, d, ws_bytes=1024) == S.SEER_EWORKSPACE
+    assert "workspace" in S.seer_last_error()
+    assert call_layer(S, d, cnt=FAKE, eps=-1.0) == S.SEER_EINVAL
+    assert call_layer(S, dims(S, dh=64)) == S.SEER_EINVAL              # 32 x 64 != 4096
+    assert call_layer(S, dims(S, h=64, dh=64)) == S.SEER_EUNSUPPORTED  # bf16 needs head_dim 128
+    L = S.load_library()
+    ev = (ctypes.c_void_p * 8)(*([FAKE] * 7 + [None]))
+    rc = L.seer_layer_forward_varlen_timed(ctypes.byref(d), FAKE, FAKE, FAKE + 4096, 100, FAKE, None,
+                                           1, 0.0, None, FAKE, 1 << 40, 0, ev)
+    assert rc == S.SEER_EINVAL and "events[7]" in S.seer_last_error()
+
+
+def test_detect_argument_errors(S):
+    L = S.load_library()
+    good = S.seer_snr_params(3, 100, 3, 5, 3)
+
+    def call(p=good, batch=1, dff=100, cnt=FAKE):
+        return L.seer_step0_detect(cnt, FAKE, FAKE, FAKE, batch, dff, ctypes.byref(p), FAKE, FAKE, 0)
+
+    assert call(cnt=None) == S.SEER_EINVAL
+    assert call(batch=0) == S.SEER_EINVAL
+    assert call(dff=0) == S.SEER_EINVAL
+    assert call(p=S.seer_snr_params(3, 0, 3, 5, 3)) == S.SEER_EINVAL
+    assert call(p=S.seer_snr_params(-1, 100, 3, 5, 3)) == S.SEER_EINVAL
+    assert call(p=S.seer_snr_params(3, 100, 3, 5, 0)) == S.SEER_EINVAL
+
+
+def test_repack_argument_errors(S):
+    L = S.load_library()
+    P = ctypes.c_void_p
+
+    def call(desc, batch=4, n=1, src=FAKE, dst=FAKE * 2):
+        sa = (P * max(n, 1))(*([src] * max(n, 1)))
+        da = (P * max(n, 1))(*([dst] * max(n, 1)))
+        return L.seer_batch_repack(ctypes.byref(desc), sa, da, n, FAKE, FAKE, FAKE, FAKE, batch, FAKE,
+                                   FAKE, FAKE, None, None, 0)
+
+    ok = dict(policy=0, tau_pad_num=1, tau_pad_den=5, granule=256, row_bytes=8192,
+              dst_capacity_rows=100, max_batch_hint=0, reserved=0)
+
+    def desc(**kw):
+        a = dict(ok)
+        a.update(kw)
+        return S.seer_repack_desc(*[a[k] for k in ("policy", "tau_pad_num", "tau_pad_den", "granule",
+                                                   "row_bytes", "dst_capacity_rows", "max_batch_hint",
+                                                   "reserved")])
+
+    assert call(desc(policy=3)) == S.SEER_EINVAL
+    assert call(desc(tau_pad_den=0)) == S.SEER_EINVAL
+    assert call(desc(granule=0)) == S.SEER_EINVAL
+    assert call(desc(row_bytes=100)) == S.SEER_EINVAL
+    assert call(desc(), batch=0) == S.SEER_EINVAL
+    assert call(desc(), batch=5000) == S.SEER_EUNSUPPORTED
+    assert call(desc(), n=0) == S.SEER_EINVAL
+    assert call(desc(), n=5) == S.SEER_EINVAL
+    assert call(desc(), dst=FAKE) == S.SEER_EINVAL              # src aliases dst
+    assert call(desc(), src=FAKE + 8) == S.SEER_EINVAL          # misaligned
