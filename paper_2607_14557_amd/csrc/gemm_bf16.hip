@@ -214,74 +214,99 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmParams p) {
 
   // ---- epilogue -----------------------------------------------------------
   // Accumulator register r of a 32x32 tile holds row 8*(r/4) + 4*(lane/32) + r%4
-  // and column lane%32.
-  const int row_base = m0 + wm * 128 + fhalf * 4;
-  if constexpr (EPI == EPI_SCALE || EPI == EPI_RESID || EPI == EPI_RESID_DUAL || EPI == EPI_RESID_R32) {
-    const int col_base = n0 + wn * 128 + fr;
+  // and column lane%32.  Each wave stages one 32-row slab of its 128x128 tile
+  // at a time through a private LDS region (fp32, padded pitch), then every
+  // lane moves 8 consecutive outputs of a row: residual loads and bf16 / fp32
+  // stores are 16-byte vector accesses, 16 lanes per 256-byte row segment.
+  // For SWIGLU the gate/up pairs are combined in registers first (and the
+  // near-zero count taken there), so the slab holds 64 activation columns.
+  constexpr int EP = 132;                       // slab pitch in floats
+  constexpr bool kGlu = (EPI == EPI_SWIGLU || EPI == EPI_SWIGLU_COUNT);
+  constexpr int SC = kGlu ? 64 : 128;           // slab columns
+  float* slab = reinterpret_cast<float*>(smem) + wave * (32 * EP);
+  const int row_w = m0 + wm * 128;              // first row of the wave tile
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
+  for (int i = 0; i < 4; ++i) {
+    // -- registers -> slab
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int row = row_base + i * 32 + (r >> 2) * 8 + (r & 3);
-        if (row < M) {
-          if constexpr (EPI == EPI_SCALE) {
-            const float s = p.rs[row];
-#pragma unroll
-            for (int j = 0; j < 4; ++j)
-              C[(size_t)row * p.ldc + col_base + j * 32] = f2bf(acc[i][j][r] * s);
-          } else if constexpr (EPI == EPI_RESID) {
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-              const size_t c = col_base + j * 32;
-              C[(size_t)row * p.ldc + c] = f2bf(bf2f(R[(size_t)row * p.ldr + c]) + acc[i][j][r]);
-            }
-          } else if constexpr (EPI == EPI_RESID_DUAL) {
-            float* C2 = static_cast<float*>(p.C2);
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-              const size_t c = col_base + j * 32;
-              const float v = bf2f(R[(size_t)row * p.ldr + c]) + acc[i][j][r];
-              C[(size_t)row * p.ldc + c] = f2bf(v);
-              C2[(size_t)row * p.ldc + c] = v;
-            }
-          } else {
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-              const size_t c = col_base + j * 32;
-              C[(size_t)row * p.ldc + c] = f2bf(p.R32[(size_t)row * p.ldr + c] + acc[i][j][r]);
-            }
-          }
-        }
-      }
-    }
-  } else {
-    const int acol_base = (n0 + wn * 128) / 2 + fr;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int row = row_base + i * 32 + (r >> 2) * 8 + (r & 3);
+    for (int r = 0; r < 16; ++r) {
+      const int lr = (r >> 2) * 8 + fhalf * 4 + (r & 3);
+      if constexpr (kGlu) {
+        const int row = row_w + i * 32 + lr;
         const bool ok = row < M;
-        const float s = ok ? p.rs[row] : 0.0f;
-        float a[2];
-#pragma unroll
-        for (int q = 0; q < 2; ++q) {
-          const float g = acc[i][2 * q][r] * s;
-          const float u = acc[i][2 * q + 1][r] * s;
-          a[q] = silu(g) * u;
-          if (ok) C[(size_t)row * p.ldc + acol_base + q * 32] = f2bf(a[q]);
-        }
+        const float sc = ok ? p.rs[row] : 0.0f;
+        const float av0 = silu(acc[i][0][r] * sc) * (acc[i][1][r] * sc);
+        const float av1 = silu(acc[i][2][r] * sc) * (acc[i][3][r] * sc);
+        slab[lr * EP + fr] = av0;
+        slab[lr * EP + 32 + fr] = av1;
         if constexpr (EPI == EPI_SWIGLU_COUNT) {
-          const uint64_t m0b = __ballot(fabsf(a[0]) < p.eps);
-          const uint64_t m1b = __ballot(fabsf(a[1]) < p.eps);
+          const uint64_t m0b = __ballot(fabsf(av0) < p.eps);
+          const uint64_t m1b = __ballot(fabsf(av1) < p.eps);
           if ((lane & 31) == 0 && ok) {
             const int sh = fhalf * 32;
             const int c = __popcll((m0b >> sh) & 0xffffffffull) + __popcll((m1b >> sh) & 0xffffffffull);
             atomicAdd(p.cnt + row, c);
           }
         }
+      } else {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) slab[lr * EP + j * 32 + fr] = acc[i][j][r];
       }
     }
+    __syncthreads();
+    // -- slab -> global, 8 consecutive outputs per lane
+    constexpr int CPR = SC / 8;                 // 8-wide chunks per row
+    constexpr int ITERS = 32 * CPR / 64;
+#pragma unroll
+    for (int it = 0; it < ITERS; ++it) {
+      const int c = it * 64 + lane;
+      const int lr = c / CPR;
+      const int c8 = (c % CPR) * 8;
+      const int row = row_w + i * 32 + lr;
+      if (row < M) {
+        const float* src = slab + lr * EP + c8;
+        float v[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v[e] = src[e];
+        if constexpr (kGlu) {
+          const size_t o = (size_t)row * p.ldc + (n0 + wn * 128) / 2 + c8;
+          u32x4_t pk;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) pk[e] = pack_bf2(v[2 * e], v[2 * e + 1]);
+          *reinterpret_cast<u32x4_t*>(C + o) = pk;
+        } else {
+          const int col = n0 + wn * 128 + c8;
+          const size_t o = (size_t)row * p.ldc + col;
+          if constexpr (EPI == EPI_SCALE) {
+            const float sc = p.rs[row];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) v[e] *= sc;
+          } else if constexpr (EPI == EPI_RESID || EPI == EPI_RESID_DUAL) {
+            const u32x4_t rv = *reinterpret_cast<const u32x4_t*>(R + (size_t)row * p.ldr + col);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              v[2 * e] += __uint_as_float(rv[e] << 16);
+              v[2 * e + 1] += __uint_as_float(rv[e] & 0xffff0000u);
+            }
+          } else {
+            const f32x4_t* r32 = reinterpret_cast<const f32x4_t*>(p.R32 + (size_t)row * p.ldr + col);
+            const f32x4_t r0 = r32[0], r1 = r32[1];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) { v[e] += r0[e]; v[4 + e] += r1[e]; }
+          }
+          u32x4_t pk;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) pk[e] = pack_bf2(v[2 * e], v[2 * e + 1]);
+          *reinterpret_cast<u32x4_t*>(C + o) = pk;
+          if constexpr (EPI == EPI_RESID_DUAL) {
+            f32x4_t* c2 = reinterpret_cast<f32x4_t*>(static_cast<float*>(p.C2) + o);
+            c2[0] = f32x4_t{v[0], v[1], v[2], v[3]};
+            c2[1] = f32x4_t{v[4], v[5], v[6], v[7]};
+          }
+        }
+      }
+    }
+    __syncthreads();
   }
 }
 
