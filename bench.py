@@ -40,6 +40,31 @@ PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 matrix peak
 PEAK_HBM_GBS = 8000.0
 
 
+# HBM traffic of the dominant kernel per launch, from two rocprofv3 --pmc passes
+# (FETCH_SIZE, then WRITE_SIZE, KiB per dispatch) over this workload, each
+# scaled by what the same counter reads for a streaming kernel of known size
+# (the --copy-calibration dispatches).  Valid only for the kernel sources it
+# was taken on: when their hash differs the figure is reported as null.
+TRAFFIC_SOURCES = ("paper_2607_14557_amd/csrc/gemm_bf16.hip", "paper_2607_14557_amd/csrc/kernels.h",
+                   "paper_2607_14557_amd/csrc/common.h")
+TRAFFIC = None
+
+
+def sources_sha256():
+    import hashlib
+    h = hashlib.sha256()
+    for f in TRAFFIC_SOURCES:
+        with open(os.path.join(ROOT, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def measured_traffic(rows_exec):
+    if TRAFFIC is None or TRAFFIC["sources_sha256"] != sources_sha256() or TRAFFIC["rows"] != rows_exec:
+        return None
+    return TRAFFIC["fetch_bytes"] + TRAFFIC["write_bytes"]
+
+
 def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
@@ -111,6 +136,9 @@ def main():
     ap.add_argument("--policy", default="hybrid", choices=["hybrid", "naive_pad", "varlen_only"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="after timing, run a 1 GiB fill and a 1 GiB read+write streaming kernel "
+                         "(the known-size dispatches that scale the HBM byte counters)")
     ap.add_argument("--no-untruncated", action="store_true",
                     help="skip the separate untruncated-step timing (it launches the gate/up GEMM "
                          "kernel at the full-window size, which a per-kernel profile would mix in)")
@@ -269,8 +297,12 @@ def main():
     dom_flop = rows_alg * gemm_flop_row["gateup"]
     dom_ms = kt["gateup"]
     achieved = tflops(dom_flop, dom_ms)
+    traffic = measured_traffic(rows_exec)
+    # compulsory bytes: both weight halves once, the A rows once, the activation rows written once
+    alg_bytes = 2 * (2 * I * d + rows_exec * d + rows_exec * I)
     roofline = {"bound": "mfma", "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS,
-                "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": traffic,
+                "traffic_unit": "bytes per launch (HBM, counters)", "compulsory_bytes": alg_bytes,
                 "kernel": "gemm_bf16_kernel<EPI_SWIGLU> (truncated-step gate/up GEMM)",
                 "flop_per_launch": dom_flop, "launch_ms": round(dom_ms, 4)}
 
@@ -299,6 +331,14 @@ def main():
         "paper_context": "up to ~31x end-to-end tokens/s (MMaDA, InfoVQA) on 1x NVIDIA A100 "
                          "(context only, different hardware and workload)",
     }
+    if args.copy_calibration:
+        n = 1 << 28                       # int32 elements: 1 GiB
+        log("calibration: 1 GiB fill, then 1 GiB read + 1 GiB write")
+        a = torch.ones(n, dtype=torch.int32, device=dev)
+        b = torch.empty_like(a)
+        torch.neg(a, out=b)
+        torch.cuda.synchronize()
+        del a, b
     if not args.no_cpu_baseline:
         log("CPU baseline (oracle on host cores)")
         out["cpu_baseline"] = cpu_baseline(w, layers, batch, args.cpu_seconds)

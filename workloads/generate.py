@@ -167,6 +167,20 @@ def make_batch(w: Workload, eos: np.ndarray) -> Batch:
                  planted=planted, eos=eos)
 
 
+def make_stack_batch(w: Workload, device) -> Batch:
+    """Host batch of a deep stack whose weights come from layer_weights_torch.
+
+    The EOS direction is taken from the detection layer's device-drawn gate
+    and up weights (read back to the host), so the planted suffix matches the
+    weights the stack actually runs with.
+    """
+    det = layer_weights_torch(w, w.l_det, device)
+    wg = det["wg"].float().cpu().numpy()
+    wu = det["wu"].float().cpu().numpy()
+    del det
+    return make_batch(w, eos_vector(wg, wu, w.eos_amplitude, w.dtype))
+
+
 def make_workload(w: Workload, with_weights: bool = True):
     """Host-side inputs: (list of per-layer weight dicts, Batch).
 
