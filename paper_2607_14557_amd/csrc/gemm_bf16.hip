@@ -130,15 +130,15 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmParams p) {
   bf16x8_t af[2][4], bfr[2][4];
   const int KT = p.K / BK;
 
-#define SEER_GLOAD(RA, RB, T)                                                       \
+#define SEER_GLOAD(RA, RB, T, P)                                                    \
   {                                                                                 \
     const int t_ = (T) < KT ? (T) : KT - 1;                                         \
     const char* ak_ = Ab + (size_t)t_ * (BK * 2);                                   \
     const char* bk_ = Bb + (size_t)t_ * (BK * 2);                                   \
-    _Pragma("unroll") for (int i = 0; i < 8; ++i)                                   \
+    _Pragma("unroll") for (int i = 2 * (P); i < 2 * (P) + 2; ++i) {                 \
       RA[i] = *reinterpret_cast<const u32x4_t*>(ak_ + a_off[i]);                    \
-    _Pragma("unroll") for (int i = 0; i < 8; ++i)                                   \
       RB[i] = *reinterpret_cast<const u32x4_t*>(bk_ + b_off + i * b_step);          \
+    }                                                                               \
   }
 #define SEER_LSTORE2(RA, RB, STG, I0)                                               \
   {                                                                                 \
@@ -151,33 +151,41 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmParams p) {
 #define SEER_FLOAD(ST, KS, BUF)                                                     \
   {                                                                                 \
     const int chunk_ = ((2 * (KS) + fhalf) ^ fsw) << 4;                             \
-    _Pragma("unroll") for (int i = 0; i < 4; ++i)                                   \
+    _Pragma("unroll") for (int i = 0; i < 4; ++i) {                                 \
       af[BUF][i] = __builtin_bit_cast(bf16x8_t,                                     \
           *reinterpret_cast<const u32x4_t*>((ST) + a_row0 + i * 32 * ROW_BYTES + chunk_)); \
-    _Pragma("unroll") for (int j = 0; j < 4; ++j)                                   \
-      bfr[BUF][j] = __builtin_bit_cast(bf16x8_t,                                    \
-          *reinterpret_cast<const u32x4_t*>((ST) + b_row0 + j * 32 * ROW_BYTES + chunk_)); \
+      bfr[BUF][i] = __builtin_bit_cast(bf16x8_t,                                    \
+          *reinterpret_cast<const u32x4_t*>((ST) + b_row0 + i * 32 * ROW_BYTES + chunk_)); \
+    }                                                                               \
   }
-  // One K tile: 4 slices x 16 MFMAs; slice ks+1's fragments are read while
-  // slice ks multiplies; two rows of the staged next tile go to LDS per slice.
-#define SEER_TILE(T, RA, RB)                                                        \
+  // One K tile of 4 slices x 16 MFMAs.  Each slice is its own scheduling
+  // region (sched_barrier fences), holding: the 8 fragment reads of the next
+  // slice, issued first and paired with the first MFMAs so they have the whole
+  // slice to land; 4 global loads of tile T+2; 4 LDS writes of tile T+1.  Slice
+  // 0's own fragments are read in a region of their own at the top.
+#define SEER_TILE(T, RA, RB, RN, RNB)                                               \
   {                                                                                 \
     const uint8_t* st_ = smem + ((T) & 1) * STAGE_BYTES;                            \
     SEER_FLOAD(st_, 0, 0);                                                          \
+    __builtin_amdgcn_sched_barrier(0);                                              \
     _Pragma("unroll") for (int ks = 0; ks < 4; ++ks) {                              \
       const int cur = ks & 1;                                                       \
       if (ks + 1 < 4) SEER_FLOAD(st_, ks + 1, cur ^ 1);                             \
+      SEER_GLOAD(RN, RNB, (T) + 2, ks);                                             \
       _Pragma("unroll") for (int i = 0; i < 4; ++i)                                 \
         _Pragma("unroll") for (int j = 0; j < 4; ++j)                               \
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[cur][i], bfr[cur][j], acc[i][j], 0, 0, 0); \
       SEER_LSTORE2(RA, RB, ((T) + 1) & 1, 2 * ks);                                  \
-      /* per slice: 4 global loads, 8 LDS reads, 4 LDS writes between 16 MFMAs */   \
-      _Pragma("unroll") for (int g = 0; g < 4; ++g) {                               \
-        __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);                          \
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                          \
+      if (ks + 1 < 4) {                                                             \
+        _Pragma("unroll") for (int g = 0; g < 4; ++g) {                             \
+          __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);                        \
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                        \
+        }                                                                           \
+      } else {                                                                      \
+        __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);                          \
       }                                                                             \
       _Pragma("unroll") for (int g = 0; g < 4; ++g) {                               \
-        __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);                          \
+        __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);                          \
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                          \
       }                                                                             \
       _Pragma("unroll") for (int g = 0; g < 4; ++g) {                               \
@@ -185,12 +193,16 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmParams p) {
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                          \
       }                                                                             \
       __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);                            \
+      __builtin_amdgcn_sched_barrier(0);                                            \
     }                                                                               \
   }
 
-  // prologue: tile 0 -> stage 0, tile 1 in registers (set 1), tile 2 loading (set 0)
-  SEER_GLOAD(ra0, rb0, 0);
-  SEER_GLOAD(ra1, rb1, 1);
+  // prologue: tile 0 -> stage 0, tile 1 in registers (set 1); tile 2 is loaded
+  // into set 0 by the slices of tile 0
+#pragma unroll
+  for (int q = 0; q < 4; ++q) SEER_GLOAD(ra0, rb0, 0, q);
+#pragma unroll
+  for (int q = 0; q < 4; ++q) SEER_GLOAD(ra1, rb1, 1, q);
   {
     uint8_t* sa_ = smem + s_off;
 #pragma unroll
@@ -200,11 +212,9 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmParams p) {
   }
   __syncthreads();
   for (int kt = 0; kt < KT; kt += 2) {
-    SEER_GLOAD(ra0, rb0, kt + 2);
-    SEER_TILE(kt, ra1, rb1);
+    SEER_TILE(kt, ra1, rb1, ra0, rb0);
     __syncthreads();
-    SEER_GLOAD(ra1, rb1, kt + 3);
-    SEER_TILE(kt + 1, ra0, rb0);
+    SEER_TILE(kt + 1, ra0, rb0, ra1, rb1);
     __syncthreads();
   }
 #undef SEER_GLOAD
