@@ -5,12 +5,12 @@
 // contractions of the denoising step (the L*d^2 term of the complexity
 // equation, Sec. 3.1).  Tiling: 256x256 block tile, K step 64, four waves in
 // a 2x2 grid, each wave owning a 128x128 sub-tile as 4x4 tiles of the
-// 32x32x16 bf16 MFMA.  The next K step's operand tiles are loaded into
-// registers while the current one is multiplied out of LDS, then written to
-// the other half of a two-stage LDS ring; the 16-byte chunks of each 128-byte
-// LDS row are XOR-swizzled so that the MFMA fragment reads of 16 consecutive
-// rows land in distinct banks.  Fragments of the next 16-wide K slice are read
-// from LDS before the current slice's MFMAs are issued.
+// 32x32x16 bf16 MFMA.  Operand tiles move global -> registers -> LDS through
+// a two-stage LDS ring with two K tiles of look-ahead; the 16-byte chunks of
+// each 128-byte LDS row are XOR-swizzled so that the MFMA fragment reads of
+// 16 consecutive rows land in distinct banks.  Every 16-wide K slice is its
+// own scheduling region in which the next slice's fragments are read first,
+// so LDS latency hides behind a whole slice of MFMAs.
 //
 // Epilogues:
 //   SCALE   C = bf16(acc * rowscale[r])         folded RMSNorm before QKV
@@ -159,46 +159,59 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmParams p) {
     }                                                                               \
   }
   // One K tile of 4 slices x 16 MFMAs.  Each slice is its own scheduling
-  // region (sched_barrier fences), holding: the 8 fragment reads of the next
-  // slice, issued first and paired with the first MFMAs so they have the whole
-  // slice to land; 4 global loads of tile T+2; 4 LDS writes of tile T+1.  Slice
-  // 0's own fragments are read in a region of their own at the top.
+  // region (sched_barrier fences) holding the 8 fragment reads of the next
+  // slice -- issued first, paired with the first MFMAs, so they have the whole
+  // slice to land -- 4 global loads of tile T+2 and its share of the LDS writes
+  // of tile T+1.  All of tile T+1 is written during slices 0-2, then one
+  // barrier: it publishes tile T+1 (so slice 3 can already read slice 0 of
+  // tile T+1 from the other stage) and, since every read of stage T%2 has been
+  // issued and waited for by then, it also orders those reads before tile T+2
+  // overwrites the stage during the next tile.
 #define SEER_TILE(T, RA, RB, RN, RNB)                                               \
   {                                                                                 \
     const uint8_t* st_ = smem + ((T) & 1) * STAGE_BYTES;                            \
-    SEER_FLOAD(st_, 0, 0);                                                          \
-    __builtin_amdgcn_sched_barrier(0);                                              \
+    const uint8_t* sn_ = smem + (((T) + 1) & 1) * STAGE_BYTES;                      \
     _Pragma("unroll") for (int ks = 0; ks < 4; ++ks) {                              \
       const int cur = ks & 1;                                                       \
-      if (ks + 1 < 4) SEER_FLOAD(st_, ks + 1, cur ^ 1);                             \
+      SEER_FLOAD(ks < 3 ? st_ : sn_, ks < 3 ? ks + 1 : 0, cur ^ 1);                 \
       SEER_GLOAD(RN, RNB, (T) + 2, ks);                                             \
       _Pragma("unroll") for (int i = 0; i < 4; ++i)                                 \
         _Pragma("unroll") for (int j = 0; j < 4; ++j)                               \
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[cur][i], bfr[cur][j], acc[i][j], 0, 0, 0); \
-      SEER_LSTORE2(RA, RB, ((T) + 1) & 1, 2 * ks);                                  \
-      if (ks + 1 < 4) {                                                             \
-        _Pragma("unroll") for (int g = 0; g < 4; ++g) {                             \
-          __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);                        \
-          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                        \
-        }                                                                           \
-      } else {                                                                      \
-        __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);                          \
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[cur][j], af[cur][i], acc[i][j], 0, 0, 0); \
+      if (ks < 2) SEER_LSTORE2(RA, RB, ((T) + 1) & 1, 2 * ks);                      \
+      if (ks == 2) {                                                                \
+        SEER_LSTORE2(RA, RB, ((T) + 1) & 1, 4);                                     \
+        SEER_LSTORE2(RA, RB, ((T) + 1) & 1, 6);                                     \
+      }                                                                             \
+      _Pragma("unroll") for (int g = 0; g < 4; ++g) {                               \
+        __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);                          \
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                          \
       }                                                                             \
       _Pragma("unroll") for (int g = 0; g < 4; ++g) {                               \
         __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);                          \
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                          \
       }                                                                             \
-      _Pragma("unroll") for (int g = 0; g < 4; ++g) {                               \
-        __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);                          \
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                          \
+      if (ks < 2) {                                                                 \
+        _Pragma("unroll") for (int g = 0; g < 4; ++g) {                             \
+          __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);                        \
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                        \
+        }                                                                           \
+        __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);                          \
+      } else if (ks == 2) {                                                         \
+        _Pragma("unroll") for (int g = 0; g < 8; ++g) {                             \
+          __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);                        \
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                        \
+        }                                                                           \
+      } else {                                                                      \
+        __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);                          \
       }                                                                             \
-      __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);                            \
       __builtin_amdgcn_sched_barrier(0);                                            \
+      if (ks == 2) __syncthreads();                                                 \
     }                                                                               \
   }
 
-  // prologue: tile 0 -> stage 0, tile 1 in registers (set 1); tile 2 is loaded
-  // into set 0 by the slices of tile 0
+  // prologue: tile 0 -> stage 0 and its first slice into registers, tile 1 in
+  // registers (set 1); tile 2 is loaded into set 0 by the slices of tile 0
 #pragma unroll
   for (int q = 0; q < 4; ++q) SEER_GLOAD(ra0, rb0, 0, q);
 #pragma unroll
@@ -211,11 +224,10 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmParams p) {
     for (int i = 0; i < 8; ++i) *reinterpret_cast<u32x4_t*>(sa_ + (BM + i * 32) * ROW_BYTES) = rb0[i];
   }
   __syncthreads();
+  SEER_FLOAD(smem, 0, 0);
   for (int kt = 0; kt < KT; kt += 2) {
     SEER_TILE(kt, ra1, rb1, ra0, rb0);
-    __syncthreads();
     SEER_TILE(kt + 1, ra0, rb0, ra1, rb1);
-    __syncthreads();
   }
 #undef SEER_GLOAD
 #undef SEER_LSTORE2
@@ -223,100 +235,83 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmParams p) {
 #undef SEER_TILE
 
   // ---- epilogue -----------------------------------------------------------
-  // Accumulator register r of a 32x32 tile holds row 8*(r/4) + 4*(lane/32) + r%4
-  // and column lane%32.  Each wave stages one 32-row slab of its 128x128 tile
-  // at a time through a private LDS region (fp32, padded pitch), then every
-  // lane moves 8 consecutive outputs of a row: residual loads and bf16 / fp32
-  // stores are 16-byte vector accesses, 16 lanes per 256-byte row segment.
-  // For SWIGLU the gate/up pairs are combined in registers first (and the
-  // near-zero count taken there), so the slab holds 64 activation columns.
-  constexpr int EP = 132;                       // slab pitch in floats
+  // The MFMAs take the B fragment as the matrix-core row operand, so tile
+  // (i, j) accumulates the transposed 32x32 block: register r holds output
+  // row m0 + 128 wm + 32 i + lane%32 and column n0 + 128 wn + 32 j + 8 (r/4) +
+  // 4 (lane/32) + r%4.  Each lane owns one row and four consecutive columns
+  // per register quad, written straight from registers as one 8-byte bf16
+  // store (16 contiguous bytes per row over a lane pair).  For SWIGLU the
+  // gate/up tiles (j = 2h, 2h+1) sit in the same lane and register; the
+  // near-zero count is a per-lane tally of its row, folded over the lane pair.
   constexpr bool kGlu = (EPI == EPI_SWIGLU || EPI == EPI_SWIGLU_COUNT);
-  constexpr int SC = kGlu ? 64 : 128;           // slab columns
-  float* slab = reinterpret_cast<float*>(smem) + wave * (32 * EP);
-  const int row_w = m0 + wm * 128;              // first row of the wave tile
+  const int cq = 4 * fhalf;
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    // -- registers -> slab
+    const int row = m0 + wm * 128 + i * 32 + fr;
+    const bool ok = row < M;
+    if constexpr (kGlu) {
+      const float sc = ok ? p.rs[row] : 0.0f;
+      int nz = 0;
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int lr = (r >> 2) * 8 + fhalf * 4 + (r & 3);
-      if constexpr (kGlu) {
-        const int row = row_w + i * 32 + lr;
-        const bool ok = row < M;
-        const float sc = ok ? p.rs[row] : 0.0f;
-        const float av0 = silu(acc[i][0][r] * sc) * (acc[i][1][r] * sc);
-        const float av1 = silu(acc[i][2][r] * sc) * (acc[i][3][r] * sc);
-        slab[lr * EP + fr] = av0;
-        slab[lr * EP + 32 + fr] = av1;
-        if constexpr (EPI == EPI_SWIGLU_COUNT) {
-          const uint64_t m0b = __ballot(fabsf(av0) < p.eps);
-          const uint64_t m1b = __ballot(fabsf(av1) < p.eps);
-          if ((lane & 31) == 0 && ok) {
-            const int sh = fhalf * 32;
-            const int c = __popcll((m0b >> sh) & 0xffffffffull) + __popcll((m1b >> sh) & 0xffffffffull);
-            atomicAdd(p.cnt + row, c);
+      for (int h = 0; h < 2; ++h) {
+        const int col = (n0 + wn * 128) / 2 + 32 * h + cq;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          float a[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            a[e] = silu(acc[i][2 * h][4 * q + e] * sc) * (acc[i][2 * h + 1][4 * q + e] * sc);
+            // |a| < eps as the sign bit of |a| - eps: rounding keeps the sign of a
+            // difference and equality gives +0 (no compare, no SGPR hazard)
+            if constexpr (EPI == EPI_SWIGLU_COUNT) nz += __float_as_uint(fabsf(a[e]) - p.eps) >> 31;
+          }
+          if (ok) {
+            uint2 pk;
+            pk.x = pack_bf2(a[0], a[1]);
+            pk.y = pack_bf2(a[2], a[3]);
+            *reinterpret_cast<uint2*>(C + (size_t)row * p.ldc + col + 8 * q) = pk;
           }
         }
-      } else {
-#pragma unroll
-        for (int j = 0; j < 4; ++j) slab[lr * EP + j * 32 + fr] = acc[i][j][r];
       }
-    }
-    __syncthreads();
-    // -- slab -> global, 8 consecutive outputs per lane
-    constexpr int CPR = SC / 8;                 // 8-wide chunks per row
-    constexpr int ITERS = 32 * CPR / 64;
+      if constexpr (EPI == EPI_SWIGLU_COUNT) {
+        nz += __shfl_xor(nz, 32, kWave);
+        if (ok && fhalf == 0) atomicAdd(p.cnt + row, nz);
+      }
+    } else if (ok) {
+      float sc = 1.0f;
+      if constexpr (EPI == EPI_SCALE) sc = p.rs[row];
 #pragma unroll
-    for (int it = 0; it < ITERS; ++it) {
-      const int c = it * 64 + lane;
-      const int lr = c / CPR;
-      const int c8 = (c % CPR) * 8;
-      const int row = row_w + i * 32 + lr;
-      if (row < M) {
-        const float* src = slab + lr * EP + c8;
-        float v[8];
+      for (int j = 0; j < 4; ++j) {
 #pragma unroll
-        for (int e = 0; e < 8; ++e) v[e] = src[e];
-        if constexpr (kGlu) {
-          const size_t o = (size_t)row * p.ldc + (n0 + wn * 128) / 2 + c8;
-          u32x4_t pk;
+        for (int q = 0; q < 4; ++q) {
+          const int col = n0 + wn * 128 + 32 * j + 8 * q + cq;
+          float v[4];
 #pragma unroll
-          for (int e = 0; e < 4; ++e) pk[e] = pack_bf2(v[2 * e], v[2 * e + 1]);
-          *reinterpret_cast<u32x4_t*>(C + o) = pk;
-        } else {
-          const int col = n0 + wn * 128 + c8;
-          const size_t o = (size_t)row * p.ldc + col;
+          for (int e = 0; e < 4; ++e) v[e] = acc[i][j][4 * q + e];
           if constexpr (EPI == EPI_SCALE) {
-            const float sc = p.rs[row];
 #pragma unroll
-            for (int e = 0; e < 8; ++e) v[e] *= sc;
+            for (int e = 0; e < 4; ++e) v[e] *= sc;
           } else if constexpr (EPI == EPI_RESID || EPI == EPI_RESID_DUAL) {
-            const u32x4_t rv = *reinterpret_cast<const u32x4_t*>(R + (size_t)row * p.ldr + col);
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-              v[2 * e] += __uint_as_float(rv[e] << 16);
-              v[2 * e + 1] += __uint_as_float(rv[e] & 0xffff0000u);
-            }
+            const uint2 rv = *reinterpret_cast<const uint2*>(R + (size_t)row * p.ldr + col);
+            v[0] += __uint_as_float(rv.x << 16);
+            v[1] += __uint_as_float(rv.x & 0xffff0000u);
+            v[2] += __uint_as_float(rv.y << 16);
+            v[3] += __uint_as_float(rv.y & 0xffff0000u);
           } else {
-            const f32x4_t* r32 = reinterpret_cast<const f32x4_t*>(p.R32 + (size_t)row * p.ldr + col);
-            const f32x4_t r0 = r32[0], r1 = r32[1];
+            const f32x4_t r32 = *reinterpret_cast<const f32x4_t*>(p.R32 + (size_t)row * p.ldr + col);
 #pragma unroll
-            for (int e = 0; e < 4; ++e) { v[e] += r0[e]; v[4 + e] += r1[e]; }
+            for (int e = 0; e < 4; ++e) v[e] += r32[e];
           }
-          u32x4_t pk;
-#pragma unroll
-          for (int e = 0; e < 4; ++e) pk[e] = pack_bf2(v[2 * e], v[2 * e + 1]);
-          *reinterpret_cast<u32x4_t*>(C + o) = pk;
-          if constexpr (EPI == EPI_RESID_DUAL) {
-            f32x4_t* c2 = reinterpret_cast<f32x4_t*>(static_cast<float*>(p.C2) + o);
-            c2[0] = f32x4_t{v[0], v[1], v[2], v[3]};
-            c2[1] = f32x4_t{v[4], v[5], v[6], v[7]};
-          }
+          const size_t o = (size_t)row * p.ldc + col;
+          uint2 pk;
+          pk.x = pack_bf2(v[0], v[1]);
+          pk.y = pack_bf2(v[2], v[3]);
+          *reinterpret_cast<uint2*>(C + o) = pk;
+          if constexpr (EPI == EPI_RESID_DUAL)
+            *reinterpret_cast<f32x4_t*>(static_cast<float*>(p.C2) + o) = f32x4_t{v[0], v[1], v[2], v[3]};
         }
       }
     }
-    __syncthreads();
   }
 }
 
