@@ -106,6 +106,8 @@ size_t seer_layer_workspace_bytes(const seer_dims* dims, int32_t max_rows);
  * max_rows (the layout depends on that bound).  Element type dims.dtype
  * unless noted:
  *   offsets[0] qkv  [max_rows, 3*d_model]   q | k | v after the folded RMSNorm
+ *                                           (bf16 layers: v is stored as fp16,
+ *                                           the type of the attention's P V product)
  *   offsets[1] o    [max_rows, d_model]     attention output (pre projection)
  *   offsets[2] h1   [max_rows, d_model]     x + o Wo^T
  *   offsets[3] act  [max_rows, d_ff]        silu(gate) * up

@@ -11,12 +11,15 @@
 // waves.  Scores are computed transposed, S^T = K Q^T (32x32x16 bf16 MFMA), so
 // that each lane owns one query column: the online-softmax statistics are
 // per-lane values and the probabilities already sit in the B-operand layout
-// of the next product O^T = V^T P^T -- no shuffle of P through LDS.  V is
-// transposed while it is written to LDS, with keys permuted inside each group
-// of 16 so that every lane's eight keys are one 16-byte read.  The P V product
-// runs in fp16: bf16 values of V convert to fp16 exactly (magnitudes inside
-// fp16's normal range) and the probabilities keep three more mantissa bits
-// than bf16 would give them.
+// of the next product O^T = V^T P^T -- no shuffle of P through LDS.  V arrives
+// in fp16 (the QKV projection stores it so) and is transposed while it is
+// written to LDS, with keys permuted inside each group of 16 so that every
+// lane's eight keys are one 16-byte read; sixteen lanes fill one V^T row and
+// the two rows a lane pair writes at once have opposite parity, so the
+// transposing writes are free of bank conflicts.  The P V product runs in
+// fp16: the probabilities keep three more mantissa bits than bf16 would give.
+// The running maximum is moved only when a tile raises it by more than 2^8
+// (log2 units), so the O rescale is rare and P stays <= 256, exact in fp16.
 #include <math.h>
 
 #include "common.h"
@@ -77,8 +80,9 @@ __global__ __launch_bounds__(NT, 2) void attn_bf16_kernel(AttnParams p) {
   const int wave = tid >> 6;
   const int fr = lane & 31;
   const int fhalf = lane >> 5;
-  const size_t ld = (size_t)3 * p.d;
-  const uint16_t* qkv = static_cast<const uint16_t*>(p.qkv);
+  const uint32_t ld = 3u * (uint32_t)p.d;
+  // rows of this sequence; every offset below is < rows_ub * 3 d (checked on the host)
+  const uint16_t* seq = static_cast<const uint16_t*>(p.qkv) + (size_t)s0 * ld;
   uint16_t* out = static_cast<uint16_t*>(p.out);
 
   const int q_row = t * QT + wave * 32 + fr;            // query row inside the sequence
@@ -87,9 +91,9 @@ __global__ __launch_bounds__(NT, 2) void attn_bf16_kernel(AttnParams p) {
   // Q as the B operand of S^T = K Q^T: lane holds query fr, dims 16*ks + 8*fhalf .. +8.
   bf16x8_t qf[8];
   {
-    const uint16_t* qp = qkv + (size_t)(s0 + q_src) * ld + h * DH + fhalf * 8;
+    const uint16_t* qp = seq + (uint32_t)q_src * ld + h * DH + fhalf * 8;
 #pragma unroll
-    for (int ks = 0; ks < 8; ++ks) qf[ks] = as_bf16x8(*reinterpret_cast<const uint4*>(qp + ks * 16));
+    for (int ks = 0; ks < 8; ++ks) qf[ks] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const u32x4_t*>(qp + ks * 16));
   }
 
   f32x16_t o[4];
@@ -102,26 +106,48 @@ __global__ __launch_bounds__(NT, 2) void attn_bf16_kernel(AttnParams p) {
   const float c = p.scale * 1.4426950408889634f;
 
   // ---- K/V tile staging -------------------------------------------------------
-  // K: thread loads 16-byte chunks id = tid + 256*i: key id/16, dim chunk id%16.
-  // V: thread loads keys 4*(tid/16) .. +3 at dim chunk tid%16, transposes 4x8.
+  // K: thread moves 16-byte chunks id = tid + 256 i: key id/16, dim chunk id%16.
+  // V (fp16): thread moves keys 4 kq .. +3 (kq = tid%16) of dim chunk vc = tid/16
+  // and writes them transposed, one dim row per 8-byte write.
+  const int kq = tid & 15;
+  const int vc = tid >> 4;
+  uint32_t k_off[4], v_off[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int id = tid + NT * i;
+    k_off[i] = (uint32_t)(id >> 4) * ld + (uint32_t)(p.d + h * DH + (id & 15) * 8);
+    v_off[i] = (uint32_t)(4 * kq + i) * ld + (uint32_t)(2 * p.d + h * DH + vc * 8);
+  }
   u32x4_t kreg[4], vreg[4];
-  const int vkq = tid >> 4;
-  const int vdc = tid & 15;
   auto load_tile = [&](int kbase) {
+    const uint16_t* tb = seq + (size_t)kbase * ld;
+    if (kbase + KT <= used) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int id = tid + NT * i;
-      int key = kbase + (id >> 4);
-      key = key < used ? key : used - 1;
-      kreg[i] = *reinterpret_cast<const u32x4_t*>(qkv + (size_t)(s0 + key) * ld + p.d + h * DH + (id & 15) * 8);
-    }
+      for (int i = 0; i < 4; ++i) kreg[i] = *reinterpret_cast<const u32x4_t*>(tb + k_off[i]);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      int key = kbase + vkq * 4 + i;
-      key = key < used ? key : used - 1;
-      vreg[i] = *reinterpret_cast<const u32x4_t*>(qkv + (size_t)(s0 + key) * ld + 2 * p.d + h * DH + vdc * 8);
+      for (int i = 0; i < 4; ++i) vreg[i] = *reinterpret_cast<const u32x4_t*>(tb + v_off[i]);
+    } else {
+      // last tile: keys at or past `used` re-read key used-1 (masked below)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int id = tid + NT * i;
+        int key = kbase + (id >> 4);
+        key = key < used ? key : used - 1;
+        kreg[i] = *reinterpret_cast<const u32x4_t*>(seq + (uint32_t)key * ld + (p.d + h * DH + (id & 15) * 8));
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        int key = kbase + 4 * kq + i;
+        key = key < used ? key : used - 1;
+        vreg[i] = *reinterpret_cast<const u32x4_t*>(seq + (uint32_t)key * ld + (2 * p.d + h * DH + vc * 8));
+      }
     }
   };
+  // Lanes with an odd dim chunk walk their eight dims in the order e ^ 1, so the
+  // two V^T rows written by one instruction have opposite parity.
+  const int vflip = vc & 1;
+  const uint32_t vsel = vflip ? 0x07060302u : 0x05040100u;   // high or low fp16 of each word
+  const int vp = vpos(4 * kq);
   auto store_tile = [&]() {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
@@ -130,21 +156,17 @@ __global__ __launch_bounds__(NT, 2) void attn_bf16_kernel(AttnParams p) {
       const int ch = (id & 15) ^ (key & 15);
       *reinterpret_cast<u32x4_t*>(k_lds + key * K_ROW + ch * 16) = kreg[i];
     }
-    // vreg[i][e/2] holds dims e, e+1 (low, high half) of key i
-    const int pos = vpos(vkq * 4);
+    // vreg[i] word w holds dims 2w (low half) and 2w+1 (high half) of key 4 kq + i
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const int sh = (e & 1) * 16;
-      const uint32_t k0 = bf_to_h_bits((vreg[0][e / 2] >> sh) & 0xffffu);
-      const uint32_t k1 = bf_to_h_bits((vreg[1][e / 2] >> sh) & 0xffffu);
-      const uint32_t k2 = bf_to_h_bits((vreg[2][e / 2] >> sh) & 0xffffu);
-      const uint32_t k3 = bf_to_h_bits((vreg[3][e / 2] >> sh) & 0xffffu);
-      const int dim = vdc * 8 + e;
-      const int ch = (pos >> 3) ^ swz8(dim);
+    for (int j = 0; j < 8; ++j) {
+      const int w = j >> 1;
+      const uint32_t sel = (j & 1) ? (vsel ^ 0x02020202u) : vsel;
       uint2 v;
-      v.x = k0 | (k1 << 16);
-      v.y = k2 | (k3 << 16);
-      *reinterpret_cast<uint2*>(v_lds + dim * V_ROW + ch * 16 + (pos & 7) * 2) = v;
+      v.x = __builtin_amdgcn_perm(vreg[1][w], vreg[0][w], sel);
+      v.y = __builtin_amdgcn_perm(vreg[3][w], vreg[2][w], sel);
+      const int dim = vc * 8 + (j ^ vflip);
+      const int ch = (vp >> 3) ^ swz8(dim);
+      *reinterpret_cast<uint2*>(v_lds + dim * V_ROW + ch * 16 + (vp & 7) * 2) = v;
     }
   };
 
@@ -168,57 +190,67 @@ __global__ __launch_bounds__(NT, 2) void attn_bf16_kernel(AttnParams p) {
 #pragma unroll
       for (int ks = 0; ks < 8; ++ks) {
         const int ch = (2 * ks + fhalf) ^ (key & 15);
-        const bf16x8_t kf = as_bf16x8(*reinterpret_cast<const uint4*>(k_lds + key * K_ROW + ch * 16));
+        const bf16x8_t kf = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const u32x4_t*>(k_lds + key * K_ROW + ch * 16));
         s[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ks], s[i], 0, 0, 0);
       }
     }
-    // mask, running max
-    float mt = -INFINITY;
+    // keys at or past `used` only occur in the last tile
+    if (kbase + KT > used) {
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int key = kbase + i * 32 + (r >> 2) * 8 + fhalf * 4 + (r & 3);
+          if (key >= used) s[i][r] = -INFINITY;
+        }
+    }
+    float mt = s[0][0];
 #pragma unroll
     for (int i = 0; i < 2; ++i)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int key = kbase + i * 32 + (r >> 2) * 8 + fhalf * 4 + (r & 3);
-        if (key >= used) s[i][r] = -INFINITY;
-        mt = fmaxf(mt, s[i][r]);
-      }
+      for (int r = 0; r < 16; ++r) mt = fmaxf(mt, s[i][r]);
     mt = fmaxf(mt, __shfl_xor(mt, 32, kWave));
-    const float m_new = fmaxf(m_run, mt);
-    const float alpha = exp2f((m_run - m_new) * c);
-    m_run = m_new;
-    const float mc = m_new * c;
+    // Move the reference maximum only when some lane's tile maximum exceeds it
+    // by more than 2^8 in the exponent (always on the first tile).
+    if (__any((mt - m_run) * c > 8.0f)) {
+      const float m_new = fmaxf(m_run, mt);
+      const float alpha = __builtin_amdgcn_exp2f((m_run - m_new) * c);
+      m_run = m_new;
+      l_run *= alpha;
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) o[i][r] *= alpha;
+    }
+    const float mc = m_run * c;
     float lsum = 0.0f;
 #pragma unroll
     for (int i = 0; i < 2; ++i)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const float e = exp2f(s[i][r] * c - mc);
+        const float e = __builtin_amdgcn_exp2f(s[i][r] * c - mc);
         s[i][r] = e;
         lsum += e;
       }
-    l_run = l_run * alpha + lsum;
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) o[i][r] *= alpha;
+    l_run += lsum;
 
     // O^T += V^T P^T over four 16-key slices.
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
 #pragma unroll
       for (int hf = 0; hf < 2; ++hf) {
-        uint4 pk;
-        pk.x = pack_h2(s[i][hf * 8 + 0], s[i][hf * 8 + 1]);
-        pk.y = pack_h2(s[i][hf * 8 + 2], s[i][hf * 8 + 3]);
-        pk.z = pack_h2(s[i][hf * 8 + 4], s[i][hf * 8 + 5]);
-        pk.w = pack_h2(s[i][hf * 8 + 6], s[i][hf * 8 + 7]);
-        const f16x8_t pf = as_f16x8(pk);
+        u32x4_t pk;
+        pk[0] = pack_h2(s[i][hf * 8 + 0], s[i][hf * 8 + 1]);
+        pk[1] = pack_h2(s[i][hf * 8 + 2], s[i][hf * 8 + 3]);
+        pk[2] = pack_h2(s[i][hf * 8 + 4], s[i][hf * 8 + 5]);
+        pk[3] = pack_h2(s[i][hf * 8 + 6], s[i][hf * 8 + 7]);
+        const f16x8_t pf = __builtin_bit_cast(f16x8_t, pk);
         const int chunk = i * 4 + hf * 2 + fhalf;
 #pragma unroll
         for (int dt = 0; dt < 4; ++dt) {
           const int dim = dt * 32 + fr;
           const int ch = chunk ^ swz8(dim);
-          const f16x8_t vf = as_f16x8(*reinterpret_cast<const uint4*>(v_lds + dim * V_ROW + ch * 16));
+          const f16x8_t vf = __builtin_bit_cast(f16x8_t, *reinterpret_cast<const u32x4_t*>(v_lds + dim * V_ROW + ch * 16));
           o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_f16(vf, pf, o[dt], 0, 0, 0);
         }
       }
@@ -250,6 +282,8 @@ __global__ __launch_bounds__(NT, 2) void attn_bf16_kernel(AttnParams p) {
 
 int launch_attn_bf16(const AttnParams& p, hipStream_t s) {
   if (p.head_dim != DH) return -1;
+  // element offsets inside the qkv rows are 32-bit
+  if ((uint64_t)p.rows_ub * 3u * (uint64_t)p.d >= (1ull << 32)) return -1;
   dim3 grid((p.rows_ub + QT - 1) / QT + p.B, p.n_heads), block(NT);
   hipLaunchKernelGGL(attn_bf16_kernel, grid, block, 0, s, p);
   return hipGetLastError() == hipSuccess ? 0 : -1;

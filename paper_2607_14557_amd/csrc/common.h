@@ -48,13 +48,16 @@ __device__ __forceinline__ f16x8_t as_f16x8(uint4 v) {
   return __builtin_bit_cast(f16x8_t, v);
 }
 
+typedef _Float16 f16x2_t __attribute__((ext_vector_type(2)));
+
 // fp32 -> fp16, round to nearest even.
 __device__ __forceinline__ uint32_t f2h_bits(float f) {
   return static_cast<uint32_t>(__builtin_bit_cast(uint16_t, static_cast<_Float16>(f)));
 }
 
+// A pair in one v_cvt_pk_f16_f32.
 __device__ __forceinline__ uint32_t pack_h2(float lo, float hi) {
-  return f2h_bits(lo) | (f2h_bits(hi) << 16);
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{lo, hi}, f16x2_t));
 }
 
 // bf16 bits -> fp16 bits (exact for magnitudes in fp16's normal range).

@@ -13,7 +13,8 @@
 // so LDS latency hides behind a whole slice of MFMAs.
 //
 // Epilogues:
-//   SCALE   C = bf16(acc * rowscale[r])         folded RMSNorm before QKV
+//   SCALE   C = bf16(acc * rowscale[r])         folded RMSNorm before QKV;
+//           column tiles from f16_col0 on (V) are stored as fp16 instead
 //   RESID   C = bf16(R[r,c] + acc)              residual add
 //   RESID_DUAL  as RESID, plus an fp32 copy     residual after O (h1 kept in fp32)
 //   RESID_R32   C = bf16(R32[r,c] + acc)        residual after down, fp32 h1
@@ -280,6 +281,7 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmParams p) {
     } else if (ok) {
       float sc = 1.0f;
       if constexpr (EPI == EPI_SCALE) sc = p.rs[row];
+      const bool to_f16 = EPI == EPI_SCALE && p.f16_col0 > 0 && n0 >= p.f16_col0;   // block-uniform
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
 #pragma unroll
@@ -304,8 +306,8 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmParams p) {
           }
           const size_t o = (size_t)row * p.ldc + col;
           uint2 pk;
-          pk.x = pack_bf2(v[0], v[1]);
-          pk.y = pack_bf2(v[2], v[3]);
+          pk.x = to_f16 ? pack_h2(v[0], v[1]) : pack_bf2(v[0], v[1]);
+          pk.y = to_f16 ? pack_h2(v[2], v[3]) : pack_bf2(v[2], v[3]);
           *reinterpret_cast<uint2*>(C + o) = pk;
           if constexpr (EPI == EPI_RESID_DUAL)
             *reinterpret_cast<f32x4_t*>(static_cast<float*>(p.C2) + o) = f32x4_t{v[0], v[1], v[2], v[3]};

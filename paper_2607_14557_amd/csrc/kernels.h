@@ -32,6 +32,9 @@ struct GemmParams {
   int lda, ldb, ldc, ldr;
   // fp32 SwiGLU only: the up-projection weight as a second [N, K] operand
   const void* B2;
+  // bf16 SCALE only: output columns >= f16_col0 are stored as fp16 (the V
+  // third of the QKV projection); 0 means none
+  int f16_col0;
 };
 
 // bf16 operands; requires N % 256 == 0, K % 64 == 0, 16-byte aligned rows.

@@ -182,6 +182,7 @@ static int layer_forward_impl(const seer_dims* dims, const void* w_packed, const
     g.A = x_in; g.B = wb + P.qkv * es; g.C = qkv; g.rs = inv1;
     g.m_ptr = m_ptr; g.m_ub = R; g.N = 3 * d; g.K = d;
     g.lda = d; g.ldb = d; g.ldc = 3 * d;
+    g.f16_col0 = bf16 ? 2 * d : 0;     // V goes to the attention's fp16 PV product
     if (gemm(seer::EPI_SCALE, g, stream)) return hip_fail("qkv gemm launch");
   }
   // 3. bidirectional varlen attention

@@ -204,7 +204,13 @@ class _Layer:
             return view_ws_f32(self.ws, self.off[idx], rows)
         if name == "h1f":
             return view_ws(self.ws, self.off[idx], rows, cols, "f32")
-        return view_ws(self.ws, self.off[idx], rows, cols, self.dtype)
+        t = view_ws(self.ws, self.off[idx], rows, cols, self.dtype)
+        if name == "qkv" and self.dtype == "bf16":
+            # bf16 layers store the v third in fp16 (the type of the P V product)
+            import torch
+            d = cols // 3
+            t = torch.cat([t[:, :2 * d].float(), t[:, 2 * d:].contiguous().view(torch.float16).float()], dim=1)
+        return t
 
 
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
