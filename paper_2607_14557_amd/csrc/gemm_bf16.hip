@@ -23,6 +23,8 @@
 //           wave holds matching gate and up columns in its registers
 //   SWIGLU_COUNT  as SWIGLU, plus the per-row count of |act| < eps on the
 //           fp32 values (wave ballot + popcount, one atomic per row and wave)
+#include <type_traits>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -30,11 +32,10 @@ namespace seer {
 
 namespace {
 
-constexpr int BM = 256, BN = 256, BK = 64;
+constexpr int BM = 256, BK = 64;
 constexpr int NT = 256;
 constexpr int GROUP_M = 8;
 constexpr int ROW_BYTES = BK * 2;                   // 128 bytes per tile row
-constexpr int STAGE_BYTES = (BM + BN) * ROW_BYTES;  // 64 KiB
 
 __device__ __forceinline__ int swz(int r) { return (r & 7) ^ ((r >> 3) & 1); }
 
@@ -59,8 +60,47 @@ __device__ __forceinline__ void tile_of(int bid, int nblk, int tiles_m, int tile
 
 }  // namespace
 
+// Instruction order inside one K slice (masks: 0x008 MFMA, 0x020 VMEM,
+// 0x100 LDS read, 0x200 LDS write).  Per slice: the next slice's 8 fragment
+// reads, a quarter of the next-next tile's global loads (4) and the LDS
+// writes of the next tile (4; 8 in slice 2, none in slice 3), spread between
+// the 16 MFMAs.
+__device__ __forceinline__ void seer_slice_schedule(int ks) {
+#pragma unroll
+  for (int g = 0; g < 4; ++g) {
+    __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+  }
+#pragma unroll
+  for (int g = 0; g < 4; ++g) {
+    __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+  }
+  if (ks < 2) {
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
+  } else if (ks == 2) {
+#pragma unroll
+    for (int g = 0; g < 8; ++g) {
+      __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    }
+  } else {
+    __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
+  }
+}
+
 template <int EPI>
 __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmParams p) {
+  constexpr int BN = 256;
+  constexpr int NJ = BN / 64;                       // 32-column MFMA tiles per wave
+  constexpr int NB = BN / 32;                       // B chunks per thread per K tile
+  constexpr int BP = NB / 4;                        // ... per slice
+  constexpr int STAGE_BYTES = (BM + BN) * ROW_BYTES;
   __shared__ __attribute__((aligned(1024))) uint8_t smem[2 * STAGE_BYTES];
 
   // Tile geometry follows the real row count read on the device, so that the
@@ -86,9 +126,10 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmParams p) {
   const uint16_t* R = static_cast<const uint16_t*>(p.R);
 
   // ---- global -> register -> LDS staging -----------------------------------
-  // Thread t moves 16-byte chunks c = t + 256 i (i < 8) of each 256x64 operand
-  // tile: tile row c / 8, K-chunk c % 8 -- eight consecutive threads read one
-  // 128-byte row segment.  In LDS the chunk lands at position chunk ^ swz(row).
+  // Thread t moves 16-byte chunks c = t + 256 i of the 256x64 A tile (i < 8)
+  // and of the BNx64 B tile (i < NB): tile row c / 8, K-chunk c % 8 -- eight
+  // consecutive threads read one 128-byte row segment.  In LDS the chunk lands
+  // at position chunk ^ swz(row).
   const int srow = tid >> 3;          // + 32 i
   const int schunk = tid & 7;
   // 32-bit byte offsets from the uniform bases (operands are < 4 GiB); rows of
@@ -106,11 +147,11 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmParams p) {
   const uint32_t b_off = (uint32_t)(n0 + srow) * (uint32_t)p.ldb * 2u + (uint32_t)schunk * 16u;
   const uint32_t b_step = 32u * (uint32_t)p.ldb * 2u;
   const int s_off = srow * ROW_BYTES + ((schunk ^ swz(srow)) << 4);
-  f32x16_t acc[4][4];
+  f32x16_t acc[4][NJ];
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
+    for (int j = 0; j < NJ; ++j)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
@@ -120,15 +161,15 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmParams p) {
   const int fsw = swz(fr);
   const int fhalf = lane >> 5;
   const int a_row0 = (wm * 128 + fr) * ROW_BYTES;
-  const int b_row0 = BM * ROW_BYTES + (wn * 128 + fr) * ROW_BYTES;
+  const int b_row0 = BM * ROW_BYTES + (wn * (BN / 2) + fr) * ROW_BYTES;
 
   // Software pipeline, two K tiles of look-ahead: while tile t is multiplied
   // out of LDS stage t%2, tile t+1 (loaded into registers one iteration
   // earlier) is written into stage (t+1)%2 between the MFMAs, and the loads of
   // tile t+2 are in flight.  Two register sets alternate, so the loop is
   // unrolled by two; K/64 is even for every shape the bf16 path accepts.
-  u32x4_t ra0[8], rb0[8], ra1[8], rb1[8];
-  bf16x8_t af[2][4], bfr[2][4];
+  u32x4_t ra0[8], rb0[NB], ra1[8], rb1[NB];
+  bf16x8_t af[2][4], bfr[2][NJ];
   const int KT = p.K / BK;
 
 #define SEER_GLOAD(RA, RB, T, P)                                                    \
@@ -136,18 +177,18 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmParams p) {
     const int t_ = (T) < KT ? (T) : KT - 1;                                         \
     const char* ak_ = Ab + (size_t)t_ * (BK * 2);                                   \
     const char* bk_ = Bb + (size_t)t_ * (BK * 2);                                   \
-    _Pragma("unroll") for (int i = 2 * (P); i < 2 * (P) + 2; ++i) {                 \
+    _Pragma("unroll") for (int i = 2 * (P); i < 2 * (P) + 2; ++i)                   \
       RA[i] = *reinterpret_cast<const u32x4_t*>(ak_ + a_off[i]);                    \
+    _Pragma("unroll") for (int i = BP * (P); i < BP * (P) + BP; ++i)                \
       RB[i] = *reinterpret_cast<const u32x4_t*>(bk_ + b_off + i * b_step);          \
-    }                                                                               \
   }
-#define SEER_LSTORE2(RA, RB, STG, I0)                                               \
+#define SEER_LSTORE(RA, RB, STG, P)                                                 \
   {                                                                                 \
     uint8_t* sa_ = smem + (STG) * STAGE_BYTES + s_off;                              \
-    *reinterpret_cast<u32x4_t*>(sa_ + ((I0) + 0) * 32 * ROW_BYTES) = RA[(I0) + 0];  \
-    *reinterpret_cast<u32x4_t*>(sa_ + ((I0) + 1) * 32 * ROW_BYTES) = RA[(I0) + 1];  \
-    *reinterpret_cast<u32x4_t*>(sa_ + (BM + ((I0) + 0) * 32) * ROW_BYTES) = RB[(I0) + 0];  \
-    *reinterpret_cast<u32x4_t*>(sa_ + (BM + ((I0) + 1) * 32) * ROW_BYTES) = RB[(I0) + 1];  \
+    _Pragma("unroll") for (int i = 2 * (P); i < 2 * (P) + 2; ++i)                   \
+      *reinterpret_cast<u32x4_t*>(sa_ + i * 32 * ROW_BYTES) = RA[i];                \
+    _Pragma("unroll") for (int i = BP * (P); i < BP * (P) + BP; ++i)                \
+      *reinterpret_cast<u32x4_t*>(sa_ + (BM + i * 32) * ROW_BYTES) = RB[i];         \
   }
 #define SEER_FLOAD(ST, KS, BUF)                                                     \
   {                                                                                 \
@@ -155,19 +196,20 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmParams p) {
     _Pragma("unroll") for (int i = 0; i < 4; ++i) {                                 \
       af[BUF][i] = __builtin_bit_cast(bf16x8_t,                                     \
           *reinterpret_cast<const u32x4_t*>((ST) + a_row0 + i * 32 * ROW_BYTES + chunk_)); \
-      bfr[BUF][i] = __builtin_bit_cast(bf16x8_t,                                    \
-          *reinterpret_cast<const u32x4_t*>((ST) + b_row0 + i * 32 * ROW_BYTES + chunk_)); \
+      if (i < NJ)                                                                   \
+        bfr[BUF][i] = __builtin_bit_cast(bf16x8_t,                                  \
+            *reinterpret_cast<const u32x4_t*>((ST) + b_row0 + i * 32 * ROW_BYTES + chunk_)); \
     }                                                                               \
   }
-  // One K tile of 4 slices x 16 MFMAs.  Each slice is its own scheduling
-  // region (sched_barrier fences) holding the 8 fragment reads of the next
+  // One K tile of 4 slices x (4 NJ) MFMAs.  Each slice is its own scheduling
+  // region (sched_barrier fences) holding the fragment reads of the next
   // slice -- issued first, paired with the first MFMAs, so they have the whole
-  // slice to land -- 4 global loads of tile T+2 and its share of the LDS writes
-  // of tile T+1.  All of tile T+1 is written during slices 0-2, then one
-  // barrier: it publishes tile T+1 (so slice 3 can already read slice 0 of
-  // tile T+1 from the other stage) and, since every read of stage T%2 has been
-  // issued and waited for by then, it also orders those reads before tile T+2
-  // overwrites the stage during the next tile.
+  // slice to land -- the global loads of one quarter of tile T+2 and its share
+  // of the LDS writes of tile T+1.  All of tile T+1 is written during slices
+  // 0-2, then one barrier: it publishes tile T+1 (so slice 3 can already read
+  // slice 0 of tile T+1 from the other stage) and, since every read of stage
+  // T%2 has been issued and waited for by then, it also orders those reads
+  // before tile T+2 overwrites the stage during the next tile.
 #define SEER_TILE(T, RA, RB, RN, RNB)                                               \
   {                                                                                 \
     const uint8_t* st_ = smem + ((T) & 1) * STAGE_BYTES;                            \
@@ -177,35 +219,14 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmParams p) {
       SEER_FLOAD(ks < 3 ? st_ : sn_, ks < 3 ? ks + 1 : 0, cur ^ 1);                 \
       SEER_GLOAD(RN, RNB, (T) + 2, ks);                                             \
       _Pragma("unroll") for (int i = 0; i < 4; ++i)                                 \
-        _Pragma("unroll") for (int j = 0; j < 4; ++j)                               \
+        _Pragma("unroll") for (int j = 0; j < NJ; ++j)                              \
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[cur][j], af[cur][i], acc[i][j], 0, 0, 0); \
-      if (ks < 2) SEER_LSTORE2(RA, RB, ((T) + 1) & 1, 2 * ks);                      \
+      if (ks < 2) SEER_LSTORE(RA, RB, ((T) + 1) & 1, ks);                           \
       if (ks == 2) {                                                                \
-        SEER_LSTORE2(RA, RB, ((T) + 1) & 1, 4);                                     \
-        SEER_LSTORE2(RA, RB, ((T) + 1) & 1, 6);                                     \
+        SEER_LSTORE(RA, RB, ((T) + 1) & 1, 2);                                      \
+        SEER_LSTORE(RA, RB, ((T) + 1) & 1, 3);                                      \
       }                                                                             \
-      _Pragma("unroll") for (int g = 0; g < 4; ++g) {                               \
-        __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);                          \
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                          \
-      }                                                                             \
-      _Pragma("unroll") for (int g = 0; g < 4; ++g) {                               \
-        __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);                          \
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                          \
-      }                                                                             \
-      if (ks < 2) {                                                                 \
-        _Pragma("unroll") for (int g = 0; g < 4; ++g) {                             \
-          __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);                        \
-          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                        \
-        }                                                                           \
-        __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);                          \
-      } else if (ks == 2) {                                                         \
-        _Pragma("unroll") for (int g = 0; g < 8; ++g) {                             \
-          __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);                        \
-          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                        \
-        }                                                                           \
-      } else {                                                                      \
-        __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);                          \
-      }                                                                             \
+      seer_slice_schedule(ks);                                                  \
       __builtin_amdgcn_sched_barrier(0);                                            \
       if (ks == 2) __syncthreads();                                                 \
     }                                                                               \
@@ -217,13 +238,8 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmParams p) {
   for (int q = 0; q < 4; ++q) SEER_GLOAD(ra0, rb0, 0, q);
 #pragma unroll
   for (int q = 0; q < 4; ++q) SEER_GLOAD(ra1, rb1, 1, q);
-  {
-    uint8_t* sa_ = smem + s_off;
 #pragma unroll
-    for (int i = 0; i < 8; ++i) *reinterpret_cast<u32x4_t*>(sa_ + i * 32 * ROW_BYTES) = ra0[i];
-#pragma unroll
-    for (int i = 0; i < 8; ++i) *reinterpret_cast<u32x4_t*>(sa_ + (BM + i * 32) * ROW_BYTES) = rb0[i];
-  }
+  for (int q = 0; q < 4; ++q) SEER_LSTORE(ra0, rb0, 0, q);
   __syncthreads();
   SEER_FLOAD(smem, 0, 0);
   for (int kt = 0; kt < KT; kt += 2) {
@@ -231,31 +247,55 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmParams p) {
     SEER_TILE(kt + 1, ra0, rb0, ra1, rb1);
   }
 #undef SEER_GLOAD
-#undef SEER_LSTORE2
+#undef SEER_LSTORE
 #undef SEER_FLOAD
 #undef SEER_TILE
 
   // ---- epilogue -----------------------------------------------------------
   // The MFMAs take the B fragment as the matrix-core row operand, so tile
   // (i, j) accumulates the transposed 32x32 block: register r holds output
-  // row m0 + 128 wm + 32 i + lane%32 and column n0 + 128 wn + 32 j + 8 (r/4) +
+  // row m0 + 128 wm + 32 i + lane%32 and column n0 + (BN/2) wn + 32 j + 8 (r/4) +
   // 4 (lane/32) + r%4.  Each lane owns one row and four consecutive columns
   // per register quad, written straight from registers as one 8-byte bf16
   // store (16 contiguous bytes per row over a lane pair).  For SWIGLU the
   // gate/up tiles (j = 2h, 2h+1) sit in the same lane and register; the
   // near-zero count is a per-lane tally of its row, folded over the lane pair.
   constexpr bool kGlu = (EPI == EPI_SWIGLU || EPI == EPI_SWIGLU_COUNT);
+  constexpr bool kRes = (EPI == EPI_RESID || EPI == EPI_RESID_DUAL || EPI == EPI_RESID_R32);
   const int cq = 4 * fhalf;
+  // Residual operands of one 32-row block: 4 NJ quads per lane, all fetched
+  // before the block is added and stored.  Issued inside the store loop they
+  // would wait out one load latency per quad (the compiler cannot move a load
+  // of R past a store to C that might alias it).
+  using RQ = typename std::conditional<EPI == EPI_RESID_R32, f32x4_t, uint2>::type;
+  RQ rq[4 * NJ];
+  // Per row one base pointer; the quads of a lane sit at constant offsets
+  // (32 j + 8 q elements) from it.
+  const int col0 = n0 + wn * (BN / 2) + cq;
+  auto fetch = [&](int i, RQ* dst) {
+    int row = m0 + wm * 128 + i * 32 + fr;
+    row = row < M ? row : M - 1;             // rows past M are never stored
+    if constexpr (EPI == EPI_RESID_R32) {
+      const float* rb = p.R32 + (size_t)row * p.ldr + col0;
+#pragma unroll
+      for (int jq = 0; jq < 4 * NJ; ++jq) dst[jq] = *reinterpret_cast<const f32x4_t*>(rb + 8 * jq);
+    } else if constexpr (kRes) {
+      const uint16_t* rb = R + (size_t)row * p.ldr + col0;
+#pragma unroll
+      for (int jq = 0; jq < 4 * NJ; ++jq) dst[jq] = *reinterpret_cast<const uint2*>(rb + 8 * jq);
+    }
+  };
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const int row = m0 + wm * 128 + i * 32 + fr;
     const bool ok = row < M;
+    if constexpr (kRes) fetch(i, rq);
     if constexpr (kGlu) {
       const float sc = ok ? p.rs[row] : 0.0f;
       int nz = 0;
 #pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        const int col = (n0 + wn * 128) / 2 + 32 * h + cq;
+      for (int h = 0; h < NJ / 2; ++h) {
+        const int col = (n0 + wn * (BN / 2)) / 2 + 32 * h + cq;
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
           float a[4];
@@ -282,11 +322,14 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmParams p) {
       float sc = 1.0f;
       if constexpr (EPI == EPI_SCALE) sc = p.rs[row];
       const bool to_f16 = EPI == EPI_SCALE && p.f16_col0 > 0 && n0 >= p.f16_col0;   // block-uniform
+      const RQ* rr = rq;
+      uint16_t* cb = C + (size_t)row * p.ldc + col0;
+      float* c2b = EPI == EPI_RESID_DUAL ? static_cast<float*>(p.C2) + (size_t)row * p.ldc + col0 : nullptr;
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
+      for (int j = 0; j < NJ; ++j) {
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-          const int col = n0 + wn * 128 + 32 * j + 8 * q + cq;
+          const int cc = 32 * j + 8 * q;
           float v[4];
 #pragma unroll
           for (int e = 0; e < 4; ++e) v[e] = acc[i][j][4 * q + e];
@@ -294,23 +337,22 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmParams p) {
 #pragma unroll
             for (int e = 0; e < 4; ++e) v[e] *= sc;
           } else if constexpr (EPI == EPI_RESID || EPI == EPI_RESID_DUAL) {
-            const uint2 rv = *reinterpret_cast<const uint2*>(R + (size_t)row * p.ldr + col);
+            const uint2 rv = rr[4 * j + q];
             v[0] += __uint_as_float(rv.x << 16);
             v[1] += __uint_as_float(rv.x & 0xffff0000u);
             v[2] += __uint_as_float(rv.y << 16);
             v[3] += __uint_as_float(rv.y & 0xffff0000u);
           } else {
-            const f32x4_t r32 = *reinterpret_cast<const f32x4_t*>(p.R32 + (size_t)row * p.ldr + col);
+            const f32x4_t r32 = rr[4 * j + q];
 #pragma unroll
             for (int e = 0; e < 4; ++e) v[e] += r32[e];
           }
-          const size_t o = (size_t)row * p.ldc + col;
           uint2 pk;
           pk.x = to_f16 ? pack_h2(v[0], v[1]) : pack_bf2(v[0], v[1]);
           pk.y = to_f16 ? pack_h2(v[2], v[3]) : pack_bf2(v[2], v[3]);
-          *reinterpret_cast<uint2*>(C + o) = pk;
+          *reinterpret_cast<uint2*>(cb + cc) = pk;
           if constexpr (EPI == EPI_RESID_DUAL)
-            *reinterpret_cast<f32x4_t*>(static_cast<float*>(p.C2) + o) = f32x4_t{v[0], v[1], v[2], v[3]};
+            *reinterpret_cast<f32x4_t*>(c2b + cc) = f32x4_t{v[0], v[1], v[2], v[3]};
         }
       }
     }
@@ -319,7 +361,7 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmParams p) {
 
 int launch_gemm_bf16(int epi, const GemmParams& p, hipStream_t s) {
   const int tiles_m = (p.m_ub + BM - 1) / BM;
-  const int tiles_n = p.N / BN;
+  const int tiles_n = p.N / 256;
   dim3 grid(tiles_m * tiles_n), block(NT);
   switch (epi) {
     case EPI_SCALE: hipLaunchKernelGGL(gemm_bf16_kernel<EPI_SCALE>, grid, block, 0, s, p); break;

@@ -37,7 +37,7 @@ struct GemmParams {
   int f16_col0;
 };
 
-// bf16 operands; requires N % 256 == 0, K % 64 == 0, 16-byte aligned rows.
+// bf16 operands; requires N % 256 == 0, K % 128 == 0, 16-byte aligned rows.
 // For SWIGLU*, N is the packed 2*I and C has I columns.
 int launch_gemm_bf16(int epi, const GemmParams& p, hipStream_t s);
 
