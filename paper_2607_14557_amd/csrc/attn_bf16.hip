@@ -7,8 +7,8 @@
 // (the static-bucket padding of Sec. 3.5).
 //
 // Design: one workgroup = (sequence, 128-query tile, head); four waves of 32
-// queries.  K and V tiles of 64 keys are staged in LDS and shared by the four
-// waves.  Scores are computed transposed, S^T = K Q^T (32x32x16 bf16 MFMA), so
+// queries.  K and V tiles of 64 keys are staged in LDS, double-buffered, and
+// shared by the four waves.  Scores are computed transposed, S^T = K Q^T (32x32x16 bf16 MFMA), so
 // that each lane owns one query column: the online-softmax statistics are
 // per-lane values and the probabilities already sit in the B-operand layout
 // of the next product O^T = V^T P^T -- no shuffle of P through LDS.  V arrives
@@ -49,8 +49,9 @@ __device__ __forceinline__ int vpos(int k) {
 }  // namespace
 
 __global__ __launch_bounds__(NT, 2) void attn_bf16_kernel(AttnParams p) {
-  __shared__ __attribute__((aligned(16))) uint8_t k_lds[KT * K_ROW];
-  __shared__ __attribute__((aligned(16))) uint8_t v_lds[DH * V_ROW];
+  // two K/V buffers: tile t+1 is written into one while tile t is read from the other
+  __shared__ __attribute__((aligned(16))) uint8_t k_lds[2][KT * K_ROW];
+  __shared__ __attribute__((aligned(16))) uint8_t v_lds[2][DH * V_ROW];
 
   // ---- which (sequence, query tile) this block owns -------------------------
   int b = -1, t = 0;
@@ -148,13 +149,15 @@ __global__ __launch_bounds__(NT, 2) void attn_bf16_kernel(AttnParams p) {
   const int vflip = vc & 1;
   const uint32_t vsel = vflip ? 0x07060302u : 0x05040100u;   // high or low fp16 of each word
   const int vp = vpos(4 * kq);
-  auto store_tile = [&]() {
+  auto store_tile = [&](int buf) {
+    uint8_t* kl = k_lds[buf];
+    uint8_t* vl = v_lds[buf];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int id = tid + NT * i;
       const int key = id >> 4;
       const int ch = (id & 15) ^ (key & 15);
-      *reinterpret_cast<u32x4_t*>(k_lds + key * K_ROW + ch * 16) = kreg[i];
+      *reinterpret_cast<u32x4_t*>(kl + key * K_ROW + ch * 16) = kreg[i];
     }
     // vreg[i] word w holds dims 2w (low half) and 2w+1 (high half) of key 4 kq + i
 #pragma unroll
@@ -166,18 +169,27 @@ __global__ __launch_bounds__(NT, 2) void attn_bf16_kernel(AttnParams p) {
       v.y = __builtin_amdgcn_perm(vreg[3][w], vreg[2][w], sel);
       const int dim = vc * 8 + (j ^ vflip);
       const int ch = (vp >> 3) ^ swz8(dim);
-      *reinterpret_cast<uint2*>(v_lds + dim * V_ROW + ch * 16 + (vp & 7) * 2) = v;
+      *reinterpret_cast<uint2*>(vl + dim * V_ROW + ch * 16 + (vp & 7) * 2) = v;
     }
   };
 
   const int n_kv = (used + KT - 1) / KT;
   if (n_kv > 0) {
     load_tile(0);
-    store_tile();
+    store_tile(0);
   }
+  // Drain every global load issued so far (Q and tile 0) before the loop.  The
+  // wait-count insertion merges the loop entry with the back edge; with Q
+  // possibly in flight at entry it would make the first score MFMAs of every
+  // iteration wait for the next tile's loads.
+  __builtin_amdgcn_sched_barrier(0);
+  __builtin_amdgcn_s_waitcnt(0x0f70);       // vmcnt(0), other counters unconstrained
+  __builtin_amdgcn_sched_barrier(0);
   __syncthreads();
   for (int kt = 0; kt < n_kv; ++kt) {
     const int kbase = kt * KT;
+    const uint8_t* kl = k_lds[kt & 1];
+    const uint8_t* vl = v_lds[kt & 1];
     if (kt + 1 < n_kv) load_tile(kbase + KT);
 
     // S^T for 64 keys: two 32-key MFMA row tiles.
@@ -190,7 +202,7 @@ __global__ __launch_bounds__(NT, 2) void attn_bf16_kernel(AttnParams p) {
 #pragma unroll
       for (int ks = 0; ks < 8; ++ks) {
         const int ch = (2 * ks + fhalf) ^ (key & 15);
-        const bf16x8_t kf = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const u32x4_t*>(k_lds + key * K_ROW + ch * 16));
+        const bf16x8_t kf = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const u32x4_t*>(kl + key * K_ROW + ch * 16));
         s[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ks], s[i], 0, 0, 0);
       }
     }
@@ -250,16 +262,15 @@ __global__ __launch_bounds__(NT, 2) void attn_bf16_kernel(AttnParams p) {
         for (int dt = 0; dt < 4; ++dt) {
           const int dim = dt * 32 + fr;
           const int ch = chunk ^ swz8(dim);
-          const f16x8_t vf = __builtin_bit_cast(f16x8_t, *reinterpret_cast<const u32x4_t*>(v_lds + dim * V_ROW + ch * 16));
+          const f16x8_t vf = __builtin_bit_cast(f16x8_t, *reinterpret_cast<const u32x4_t*>(vl + dim * V_ROW + ch * 16));
           o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_f16(vf, pf, o[dt], 0, 0, 0);
         }
       }
     }
+    // Buffer (kt+1)&1 was last read in iteration kt-1, which every wave left
+    // through the barrier below; one barrier then publishes tile kt+1.
+    if (kt + 1 < n_kv) store_tile((kt + 1) & 1);
     __syncthreads();
-    if (kt + 1 < n_kv) {
-      store_tile();
-      __syncthreads();
-    }
   }
 
   // ---- normalise and store ----------------------------------------------------
