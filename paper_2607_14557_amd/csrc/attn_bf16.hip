@@ -192,19 +192,35 @@ __global__ __launch_bounds__(NT, 2) void attn_bf16_kernel(AttnParams p) {
     const uint8_t* vl = v_lds[kt & 1];
     if (kt + 1 < n_kv) load_tile(kbase + KT);
 
-    // S^T for 64 keys: two 32-key MFMA row tiles.
+    // S^T for 64 keys: two 32-key MFMA row tiles, walked over the 8 dim
+    // slices with the next slice's two K fragments read one step ahead.
     f32x16_t s[2];
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
+    for (int i = 0; i < 2; ++i)
 #pragma unroll
       for (int r = 0; r < 16; ++r) s[i][r] = 0.0f;
-      const int key = i * 32 + fr;
+    {
+      const uint8_t* krow = kl + fr * K_ROW;        // keys fr and 32 + fr
+      auto kread = [&](int ks, bf16x8_t* dst) {
+        const int ch = (2 * ks + fhalf) ^ (fr & 15);
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+          dst[i] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const u32x4_t*>(krow + i * 32 * K_ROW + ch * 16));
+      };
+      bf16x8_t kf[2][2];
+      __builtin_amdgcn_sched_barrier(0);
+      kread(0, kf[0]);
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int ks = 0; ks < 8; ++ks) {
-        const int ch = (2 * ks + fhalf) ^ (key & 15);
-        const bf16x8_t kf = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const u32x4_t*>(kl + key * K_ROW + ch * 16));
-        s[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ks], s[i], 0, 0, 0);
+        if (ks + 1 < 8) kread(ks + 1, kf[(ks + 1) & 1]);
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+          s[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[ks & 1][i], qf[ks], s[i], 0, 0, 0);
+        if (ks + 1 < 8) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
       }
+      __builtin_amdgcn_sched_barrier(0);
     }
     // keys at or past `used` only occur in the last tile
     if (kbase + KT > used) {
@@ -246,26 +262,39 @@ __global__ __launch_bounds__(NT, 2) void attn_bf16_kernel(AttnParams p) {
       }
     l_run += lsum;
 
-    // O^T += V^T P^T over four 16-key slices.
+    // O^T += V^T P^T over four 16-key slices x four 32-dim tiles; the V^T
+    // fragment of step n + 2 is read while step n multiplies.
+    {
+      f16x8_t pf[4];
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-#pragma unroll
-      for (int hf = 0; hf < 2; ++hf) {
+      for (int sl = 0; sl < 4; ++sl) {
+        const int i = sl >> 1, hf = sl & 1;
         u32x4_t pk;
         pk[0] = pack_h2(s[i][hf * 8 + 0], s[i][hf * 8 + 1]);
         pk[1] = pack_h2(s[i][hf * 8 + 2], s[i][hf * 8 + 3]);
         pk[2] = pack_h2(s[i][hf * 8 + 4], s[i][hf * 8 + 5]);
         pk[3] = pack_h2(s[i][hf * 8 + 6], s[i][hf * 8 + 7]);
-        const f16x8_t pf = __builtin_bit_cast(f16x8_t, pk);
-        const int chunk = i * 4 + hf * 2 + fhalf;
-#pragma unroll
-        for (int dt = 0; dt < 4; ++dt) {
-          const int dim = dt * 32 + fr;
-          const int ch = chunk ^ swz8(dim);
-          const f16x8_t vf = __builtin_bit_cast(f16x8_t, *reinterpret_cast<const u32x4_t*>(vl + dim * V_ROW + ch * 16));
-          o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_f16(vf, pf, o[dt], 0, 0, 0);
-        }
+        pf[sl] = __builtin_bit_cast(f16x8_t, pk);
       }
+      auto vread = [&](int n) {
+        const int sl = n >> 2, dt = n & 3;
+        const int dim = dt * 32 + fr;
+        const int ch = (2 * sl + fhalf) ^ swz8(dim);
+        return __builtin_bit_cast(f16x8_t, *reinterpret_cast<const u32x4_t*>(vl + dim * V_ROW + ch * 16));
+      };
+      f16x8_t vf[3];
+      __builtin_amdgcn_sched_barrier(0);
+      vf[0] = vread(0);
+      vf[1] = vread(1);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int n = 0; n < 16; ++n) {
+        if (n + 2 < 16) vf[(n + 2) % 3] = vread(n + 2);
+        o[n & 3] = __builtin_amdgcn_mfma_f32_32x32x16_f16(vf[n % 3], pf[n >> 2], o[n & 3], 0, 0, 0);
+        if (n + 2 < 16) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      }
+      __builtin_amdgcn_sched_barrier(0);
     }
     // Buffer (kt+1)&1 was last read in iteration kt-1, which every wave left
     // through the barrier below; one barrier then publishes tile kt+1.
