@@ -315,3 +315,89 @@ def test_layer_deterministic(S):
     y2, c2 = L.run(x, dev(cu), 2, eps=0.002)
     np.testing.assert_array_equal(host(y1), host(y2))
     np.testing.assert_array_equal(host(c1), host(c2))
+
+
+# ---------------------------------------------------------------------------
+# degenerate inputs: empty sequences and windows, the largest repack batch
+
+def test_layer_with_empty_sequences(S):
+    """Zero-length sequences between real ones, and a batch with no rows at all."""
+    import torch
+    d, H, dh, I = 512, 4, 128, 1024
+    rng = np.random.default_rng(7)
+    W = _round(_rand_layer(rng, d, I, 0.02), "bf16")
+    lens = [0, 130, 0, 1, 257, 0]
+    cu = np.concatenate([[0], np.cumsum(lens)])
+    T = int(cu[-1])
+    rows_ub = T + 3
+    xd = dev(np.concatenate([rng.standard_normal((T, d)), np.zeros((3, d))]), "bf16")
+    x = host(xd)
+    eps = 0.01 * 0.0004 * d
+    log("layer with empty sequences lens=%s" % lens)
+    L = _Layer(S, d, H, dh, I, "bf16", rows_ub, W)
+    y, cnt = L.run(xd, dev(cu), len(lens), eps=eps)
+    y = host(y)
+    y_ref, _ = layer_forward(x[:T], cu, W, H, 1e-5, act_eps=eps)
+    assert rel_err(y[:T], y_ref) <= BF16_TOL
+    assert np.all(y[T:] == 0.0)
+    bnorm = rms_norm(host(L.inter("h1", T, d)), W["g2"], 1e-5)
+    check_counts(host(cnt)[:T], bnorm, W["wg"], W["wu"], eps, I, FRAC_TOL)
+    # no rows: nothing is written, the counts stay zero
+    L0 = _Layer(S, d, H, dh, I, "bf16", 8, W)
+    x0 = torch.zeros(8, d, dtype=torch.bfloat16, device="cuda")
+    y0, c0 = L0.run(x0, dev(np.array([0, 0, 0])), 2, eps=eps)
+    assert torch.count_nonzero(y0).item() == 0
+    assert torch.count_nonzero(c0).item() == 0
+
+
+@pytest.mark.parametrize("policy", [0, 1])
+def test_detect_and_repack_largest_batch(S, policy):
+    """1024 sequences (the largest batch one repack launch plans), with empty
+    windows, empty prefixes and windows too short for any candidate; hybrid
+    routing (all varlen here) and naive padding (all static)."""
+    import torch
+    rng = np.random.default_rng(2024)
+    B, I, d = 1024, 257, 64
+    pre = rng.integers(0, 9, size=B)
+    win = rng.integers(0, 40, size=B)
+    win[:6] = [0, 0, 1, 2, 3, 4]
+    pre[6:9] = 0
+    lens = pre + win
+    cu = np.concatenate([[0], np.cumsum(lens)])
+    T = int(cu[-1])
+    counts = rng.integers(0, 60, size=T)
+    for b in range(B):
+        if win[b] > 4 and b % 3:
+            j = int(cu[b] + pre[b] + rng.integers(0, win[b]))
+            counts[j:cu[b + 1]] += 100
+    counts = np.minimum(counts, I).astype(np.int32)
+    bnd, keep = _i32(B), _i32(B)
+    log("detect + repack, B=%d, %d rows, policy %d" % (B, T, policy))
+    S.seer_step0_detect(dev(counts), dev(cu), dev(pre), dev(win), B, I, S.seer_snr_params(3, 100, 3, 5, 3),
+                        bnd, keep)
+    torch.cuda.synchronize()
+    eb, ek = detect_batch(counts, cu, pre, win, I, Fraction(3, 100), Fraction(3, 5), 3)
+    np.testing.assert_array_equal(host(bnd), eb)
+    np.testing.assert_array_equal(host(keep), ek)
+    src = rng.standard_normal((T, d)).astype(np.float32)
+    s1 = dev(src, "bf16")
+    cap = int(np.sum(pre)) + B * (int(win.max()) + 8) + 256
+    d1 = torch.full((cap, d), -7.0, dtype=torch.bfloat16, device="cuda")
+    cu_dst, used = _i32(B + 1), _i32(B)
+    route = torch.empty(B, 3, dtype=torch.int32, device="cuda")
+    ctrl = torch.zeros(16, dtype=torch.int32, device="cuda")
+    desc = S.seer_repack_desc(policy, 1, 5, 1, d * 2, cap, 0, 0)
+    S.seer_batch_repack(desc, [s1], [d1], dev(cu), dev(pre), dev(win), keep, B, cu_dst, used, route, ctrl)
+    torch.cuda.synchronize()
+    rt = route_batch(ek, win, policy, Fraction(1, 5))
+    rh = host(route)
+    np.testing.assert_array_equal(rh[:, 0], rt.path)
+    np.testing.assert_array_equal(rh[:, 1], rt.group)
+    np.testing.assert_array_equal(rh[:, 2], rt.alloc)
+    exp, cu_e, used_e, cap_e = repack_rows(host(s1), cu, pre, ek, rt.alloc, 1)
+    np.testing.assert_array_equal(host(cu_dst), cu_e)
+    np.testing.assert_array_equal(host(used), used_e)
+    got = host(d1)
+    np.testing.assert_array_equal(got[:cap_e], exp)
+    assert np.all(got[cap_e:] == -7.0)
+    assert host(ctrl)[7] == 0 and host(ctrl)[0] == cu_e[-1]
