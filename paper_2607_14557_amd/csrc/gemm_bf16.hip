@@ -39,15 +39,17 @@ constexpr int ROW_BYTES = BK * 2;                   // 128 bytes per tile row
 
 __device__ __forceinline__ int swz(int r) { return (r & 7) ^ ((r >> 3) & 1); }
 
-// Block id -> (tile_m, tile_n).  Consecutive workgroup ids are spread round
-// robin over the 8 XCDs; re-number so that each XCD walks a contiguous range
-// of logical tiles, then raster those in groups of GROUP_M tile rows so the
-// blocks resident on one XCD share A row-tiles and B column-tiles in its L2.
-__device__ __forceinline__ void tile_of(int bid, int nblk, int tiles_m, int tiles_n,
-                                        int& tm, int& tn) {
+// Workgroup ids are dealt round robin over the 8 XCDs.  xcd_remap turns block
+// id bid in [0, nblk) into a logical tile id such that each XCD walks a
+// contiguous range of logical tiles; raster lays those out in groups of
+// GROUP_M tile rows, so the blocks resident on one XCD share A row-tiles and
+// B column-tiles in its L2.
+__device__ __forceinline__ int xcd_remap(int bid, int nblk) {
   const int per = nblk >> 3;
-  int lid = bid;
-  if (bid < (per << 3)) lid = (bid & 7) * per + (bid >> 3);
+  return bid < (per << 3) ? (bid & 7) * per + (bid >> 3) : bid;
+}
+
+__device__ __forceinline__ void raster(int lid, int tiles_m, int tiles_n, int& tm, int& tn) {
   const int gsz = GROUP_M * tiles_n;
   const int g = lid / gsz;
   const int first_m = g * GROUP_M;
@@ -61,60 +63,65 @@ __device__ __forceinline__ void tile_of(int bid, int nblk, int tiles_m, int tile
 }  // namespace
 
 // Instruction order inside one K slice (masks: 0x008 MFMA, 0x020 VMEM,
-// 0x100 LDS read, 0x200 LDS write).  Per slice: the next slice's 8 fragment
-// reads, a quarter of the next-next tile's global loads (4) and the LDS
-// writes of the next tile (4; 8 in slice 2, none in slice 3), spread between
-// the 16 MFMAs.
+// 0x100 LDS read, 0x200 LDS write).  Per slice: the next slice's fragment
+// reads, a quarter of the next-next tile's global loads and the LDS writes of
+// the next tile (none in the last slice, twice as many in slice 2), spread
+// between the 4 NJ MFMAs.
+template <int BN>
 __device__ __forceinline__ void seer_slice_schedule(int ks) {
-#pragma unroll
-  for (int g = 0; g < 4; ++g) {
-    __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
-    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-  }
-#pragma unroll
-  for (int g = 0; g < 4; ++g) {
-    __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
-    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-  }
-  if (ks < 2) {
+  if constexpr (BN == 256) {        // 8 reads, 4 loads, 4/8/0 writes, 16 MFMAs
 #pragma unroll
     for (int g = 0; g < 4; ++g) {
-      __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
     }
-    __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
-  } else if (ks == 2) {
 #pragma unroll
-    for (int g = 0; g < 8; ++g) {
-      __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);
+    for (int g = 0; g < 4; ++g) {
+      __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
     }
-  } else {
-    __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
+    if (ks < 2) {
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      }
+      __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
+    } else if (ks == 2) {
+#pragma unroll
+      for (int g = 0; g < 8; ++g) {
+        __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      }
+    } else {
+      __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
+    }
+  } else {                          // 6 reads, 3 loads, 3/6/0 writes, 8 MFMAs
+#pragma unroll
+    for (int g = 0; g < 3; ++g) {
+      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    }
+#pragma unroll
+    for (int g = 0; g < 3; ++g) {
+      __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+      if (ks < 2) __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);
+      if (ks == 2) __builtin_amdgcn_sched_group_barrier(0x200, 2, 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
   }
 }
 
-template <int EPI>
-__global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmParams p) {
-  constexpr int BN = 256;
+// One BMxBN output tile over the whole K range.  BN = 256 is the main tile
+// (waves of 128x128); BN = 128 (waves of 128x64) serves the halves of the
+// tiles of a partly filled last round.
+template <int EPI, int BN>
+__device__ __forceinline__ void gemm_tile(const GemmParams& p, uint8_t* smem, int M, int m0, int n0) {
   constexpr int NJ = BN / 64;                       // 32-column MFMA tiles per wave
   constexpr int NB = BN / 32;                       // B chunks per thread per K tile
   constexpr int BP = NB / 4;                        // ... per slice
   constexpr int STAGE_BYTES = (BM + BN) * ROW_BYTES;
-  __shared__ __attribute__((aligned(1024))) uint8_t smem[2 * STAGE_BYTES];
-
-  // Tile geometry follows the real row count read on the device, so that the
-  // blocks carrying work are spread over every XCD; surplus blocks of the
-  // upper-bound grid exit at once.
-  const int M = rows_from(p.m_ptr, p.m_ub);
-  const int tiles_m = (M + BM - 1) / BM;
-  const int tiles_n = p.N / BN;
-  const int ntiles = tiles_m * tiles_n;
-  if ((int)blockIdx.x >= ntiles) return;
-  int tm, tn;
-  tile_of(blockIdx.x, ntiles, tiles_m, tiles_n, tm, tn);
-  const int m0 = tm * BM;
-  const int n0 = tn * BN;
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -226,7 +233,7 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmParams p) {
         SEER_LSTORE(RA, RB, ((T) + 1) & 1, 2);                                      \
         SEER_LSTORE(RA, RB, ((T) + 1) & 1, 3);                                      \
       }                                                                             \
-      seer_slice_schedule(ks);                                                  \
+      seer_slice_schedule<BN>(ks);                                                \
       __builtin_amdgcn_sched_barrier(0);                                            \
       if (ks == 2) __syncthreads();                                                 \
     }                                                                               \
@@ -359,10 +366,42 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmParams p) {
   }
 }
 
+// Units of work: the 256x256 tiles, except that when the tiles leave a last
+// round of r < n_units/2 tiles on the n_units workgroups that run at once,
+// each of those r tiles becomes two 256x128 halves (disjoint outputs, no
+// reduction), so the last round keeps twice as many CUs busy.  Tile geometry
+// follows the real row count read on the device; surplus blocks of the
+// upper-bound grid exit at once.
+template <int EPI>
+__global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmParams p) {
+  __shared__ __attribute__((aligned(1024))) uint8_t smem[2 * (BM + 256) * ROW_BYTES];
+  const int M = rows_from(p.m_ptr, p.m_ub);
+  const int tiles_m = (M + BM - 1) / BM;
+  const int tiles_n = p.N / 256;
+  const int ntiles = tiles_m * tiles_n;
+  int full = ntiles;
+  if (p.n_units > 0) {
+    const int rem = ntiles % p.n_units;
+    if (2 * rem <= p.n_units) full = ntiles - rem;
+  }
+  const int u = blockIdx.x;
+  if (u >= full + 2 * (ntiles - full)) return;
+  int tm, tn;
+  if (u < full) {
+    raster(xcd_remap(u, full), tiles_m, tiles_n, tm, tn);
+    gemm_tile<EPI, 256>(p, smem, M, tm * BM, tn * 256);
+  } else {
+    const int v = u - full;
+    raster(full + (v >> 1), tiles_m, tiles_n, tm, tn);
+    gemm_tile<EPI, 128>(p, smem, M, tm * BM, tn * 256 + (v & 1) * 128);
+  }
+}
+
 int launch_gemm_bf16(int epi, const GemmParams& p, hipStream_t s) {
   const int tiles_m = (p.m_ub + BM - 1) / BM;
   const int tiles_n = p.N / 256;
-  dim3 grid(tiles_m * tiles_n), block(NT);
+  // the split last round adds at most n_units / 2 units
+  dim3 grid(tiles_m * tiles_n + (p.n_units > 0 ? p.n_units / 2 : 0)), block(NT);
   switch (epi) {
     case EPI_SCALE: hipLaunchKernelGGL(gemm_bf16_kernel<EPI_SCALE>, grid, block, 0, s, p); break;
     case EPI_RESID: hipLaunchKernelGGL(gemm_bf16_kernel<EPI_RESID>, grid, block, 0, s, p); break;

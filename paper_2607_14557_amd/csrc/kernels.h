@@ -35,6 +35,10 @@ struct GemmParams {
   // bf16 SCALE only: output columns >= f16_col0 are stored as fp16 (the V
   // third of the QKV projection); 0 means none
   int f16_col0;
+  // bf16 only: workgroups that run at once (one per CU).  When the 256x256
+  // tiles leave a last round of r <= n_units / 2 tiles, those r tiles run as
+  // 2 r halves of 256x128.  0 disables the split.
+  int n_units;
 };
 
 // bf16 operands; requires N % 256 == 0, K % 128 == 0, 16-byte aligned rows.

@@ -164,6 +164,13 @@ static int layer_forward_impl(const seer_dims* dims, const void* w_packed, const
   float* inv1 = reinterpret_cast<float*>(ws + L.inv1);
   float* inv2 = reinterpret_cast<float*>(ws + L.inv2);
   float* h1f = reinterpret_cast<float*>(ws + L.h1f);
+  int n_units = 0;                      // CUs: sizes the split of a partly filled last GEMM round
+  if (bf16) {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&n_units, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+      return hip_fail("device query");
+  }
   const int* m_ptr = cu_seqlens + batch;
   const seer::PackedLayout P = seer::packed_layout(d, I, bf16);
   const size_t es = bf16 ? 2 : 4;
@@ -179,6 +186,7 @@ static int layer_forward_impl(const seer_dims* dims, const void* w_packed, const
   if (mark(1) != hipSuccess) return hip_fail("event record");
   {
     seer::GemmParams g{};
+    g.n_units = n_units;
     g.A = x_in; g.B = wb + P.qkv * es; g.C = qkv; g.rs = inv1;
     g.m_ptr = m_ptr; g.m_ub = R; g.N = 3 * d; g.K = d;
     g.lda = d; g.ldb = d; g.ldc = 3 * d;
@@ -199,6 +207,7 @@ static int layer_forward_impl(const seer_dims* dims, const void* w_packed, const
   if (mark(3) != hipSuccess) return hip_fail("event record");
   {
     seer::GemmParams g{};
+    g.n_units = n_units;
     g.A = o; g.B = wb + P.o * es; g.C = h1; g.R = x_in; g.C2 = h1f;
     g.m_ptr = m_ptr; g.m_ub = R; g.N = d; g.K = d;
     g.lda = d; g.ldb = d; g.ldc = d; g.ldr = d;
@@ -212,6 +221,7 @@ static int layer_forward_impl(const seer_dims* dims, const void* w_packed, const
   {
     if (act_count && seer::launch_zero_i32(act_count, R, stream)) return hip_fail("zero launch");
     seer::GemmParams g{};
+    g.n_units = n_units;
     g.A = h1; g.C = act; g.rs = inv2; g.cnt = act_count; g.eps = act_eps;
     g.m_ptr = m_ptr; g.m_ub = R; g.K = d; g.lda = d; g.ldb = d; g.ldc = I;
     if (bf16) {
@@ -230,6 +240,7 @@ static int layer_forward_impl(const seer_dims* dims, const void* w_packed, const
   if (mark(6) != hipSuccess) return hip_fail("event record");
   {
     seer::GemmParams g{};
+    g.n_units = n_units;
     g.A = act; g.B = wb + P.dn * es; g.C = x_out; g.R = h1; g.R32 = h1f;
     g.m_ptr = m_ptr; g.m_ub = R; g.N = d; g.K = I;
     g.lda = I; g.ldb = I; g.ldc = d; g.ldr = d;
