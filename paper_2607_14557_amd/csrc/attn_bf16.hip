@@ -12,11 +12,9 @@
 // that each lane owns one query column: the online-softmax statistics are
 // per-lane values and the probabilities already sit in the B-operand layout
 // of the next product O^T = V^T P^T -- no shuffle of P through LDS.  V arrives
-// in fp16 (the QKV projection stores it so) and is transposed while it is
-// written to LDS, with keys permuted inside each group of 16 so that every
-// lane's eight keys are one 16-byte read; sixteen lanes fill one V^T row and
-// the two rows a lane pair writes at once have opposite parity, so the
-// transposing writes are free of bank conflicts.  The P V product runs in
+// in fp16 (the QKV projection stores it so) and is staged row-major like K;
+// its A-operand fragments (8 keys of one dim per lane) come from pairs of LDS
+// transpose reads (ds_read_b64_tr_b16).  The P V product runs in
 // fp16: the probabilities keep three more mantissa bits than bf16 would give.
 // The running maximum is moved only when a tile raises it by more than 2^8
 // (log2 units), so the O rescale is rare and P stays <= 256, exact in fp16.
@@ -33,25 +31,18 @@ constexpr int QT = 128;   // queries per workgroup
 constexpr int KT = 64;    // keys per LDS tile
 constexpr int DH = 128;   // head dim
 constexpr int NT = 256;
-constexpr int K_ROW = DH * 2;   // 256 bytes per key row of K
-constexpr int V_ROW = KT * 2;   // 128 bytes per dim row of V^T
+constexpr int K_ROW = DH * 2;   // 256 bytes per key row of K and of V
 
-__device__ __forceinline__ int swz8(int r) { return (r & 7) ^ ((r >> 3) & 1); }
-
-// Position of key k (0..63) inside a V^T row: within each 16-key group the
-// quads are stored in the order {0, 2, 1, 3}.
-__device__ __forceinline__ int vpos(int k) {
-  const int q = (k >> 2) & 3;
-  const int pq = ((q & 1) << 1) | (q >> 1);
-  return (k & ~15) | (pq << 2) | (k & 3);
-}
+typedef short v4i16_t __attribute__((ext_vector_type(4)));
+typedef short v8i16_t __attribute__((ext_vector_type(8)));
+typedef __attribute__((address_space(3))) v4i16_t lds_v4i16_t;
 
 }  // namespace
 
 __global__ __launch_bounds__(NT, 2) void attn_bf16_kernel(AttnParams p) {
   // two K/V buffers: tile t+1 is written into one while tile t is read from the other
   __shared__ __attribute__((aligned(16))) uint8_t k_lds[2][KT * K_ROW];
-  __shared__ __attribute__((aligned(16))) uint8_t v_lds[2][DH * V_ROW];
+  __shared__ __attribute__((aligned(16))) uint8_t v_lds[2][KT * K_ROW];
 
   // ---- which (sequence, query tile) this block owns -------------------------
   int b = -1, t = 0;
@@ -107,17 +98,15 @@ __global__ __launch_bounds__(NT, 2) void attn_bf16_kernel(AttnParams p) {
   const float c = p.scale * 1.4426950408889634f;
 
   // ---- K/V tile staging -------------------------------------------------------
-  // K: thread moves 16-byte chunks id = tid + 256 i: key id/16, dim chunk id%16.
-  // V (fp16): thread moves keys 4 kq .. +3 (kq = tid%16) of dim chunk vc = tid/16
-  // and writes them transposed, one dim row per 8-byte write.
-  const int kq = tid & 15;
-  const int vc = tid >> 4;
-  uint32_t k_off[4], v_off[4];
+  // Thread moves 16-byte chunks id = tid + 256 i of K and of V (fp16): key
+  // id/16, dim chunk id%16.  Both stay row-major in LDS; K's chunks are XOR-
+  // swizzled by key%16, V's by 4 (key%4) -- V fragments are read with the LDS
+  // transpose read, whose 8-byte accesses then hit distinct banks.
+  uint32_t k_off[4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const int id = tid + NT * i;
     k_off[i] = (uint32_t)(id >> 4) * ld + (uint32_t)(p.d + h * DH + (id & 15) * 8);
-    v_off[i] = (uint32_t)(4 * kq + i) * ld + (uint32_t)(2 * p.d + h * DH + vc * 8);
   }
   u32x4_t kreg[4], vreg[4];
   auto load_tile = [&](int kbase) {
@@ -126,7 +115,7 @@ __global__ __launch_bounds__(NT, 2) void attn_bf16_kernel(AttnParams p) {
 #pragma unroll
       for (int i = 0; i < 4; ++i) kreg[i] = *reinterpret_cast<const u32x4_t*>(tb + k_off[i]);
 #pragma unroll
-      for (int i = 0; i < 4; ++i) vreg[i] = *reinterpret_cast<const u32x4_t*>(tb + v_off[i]);
+      for (int i = 0; i < 4; ++i) vreg[i] = *reinterpret_cast<const u32x4_t*>(tb + k_off[i] + p.d);
     } else {
       // last tile: keys at or past `used` re-read key used-1 (masked below)
 #pragma unroll
@@ -134,21 +123,12 @@ __global__ __launch_bounds__(NT, 2) void attn_bf16_kernel(AttnParams p) {
         const int id = tid + NT * i;
         int key = kbase + (id >> 4);
         key = key < used ? key : used - 1;
-        kreg[i] = *reinterpret_cast<const u32x4_t*>(seq + (uint32_t)key * ld + (p.d + h * DH + (id & 15) * 8));
-      }
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        int key = kbase + 4 * kq + i;
-        key = key < used ? key : used - 1;
-        vreg[i] = *reinterpret_cast<const u32x4_t*>(seq + (uint32_t)key * ld + (2 * p.d + h * DH + vc * 8));
+        const uint16_t* row = seq + (uint32_t)key * ld + (p.d + h * DH + (id & 15) * 8);
+        kreg[i] = *reinterpret_cast<const u32x4_t*>(row);
+        vreg[i] = *reinterpret_cast<const u32x4_t*>(row + p.d);
       }
     }
   };
-  // Lanes with an odd dim chunk walk their eight dims in the order e ^ 1, so the
-  // two V^T rows written by one instruction have opposite parity.
-  const int vflip = vc & 1;
-  const uint32_t vsel = vflip ? 0x07060302u : 0x05040100u;   // high or low fp16 of each word
-  const int vp = vpos(4 * kq);
   auto store_tile = [&](int buf) {
     uint8_t* kl = k_lds[buf];
     uint8_t* vl = v_lds[buf];
@@ -156,20 +136,8 @@ __global__ __launch_bounds__(NT, 2) void attn_bf16_kernel(AttnParams p) {
     for (int i = 0; i < 4; ++i) {
       const int id = tid + NT * i;
       const int key = id >> 4;
-      const int ch = (id & 15) ^ (key & 15);
-      *reinterpret_cast<u32x4_t*>(kl + key * K_ROW + ch * 16) = kreg[i];
-    }
-    // vreg[i] word w holds dims 2w (low half) and 2w+1 (high half) of key 4 kq + i
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const int w = j >> 1;
-      const uint32_t sel = (j & 1) ? (vsel ^ 0x02020202u) : vsel;
-      uint2 v;
-      v.x = __builtin_amdgcn_perm(vreg[1][w], vreg[0][w], sel);
-      v.y = __builtin_amdgcn_perm(vreg[3][w], vreg[2][w], sel);
-      const int dim = vc * 8 + (j ^ vflip);
-      const int ch = (vp >> 3) ^ swz8(dim);
-      *reinterpret_cast<uint2*>(vl + dim * V_ROW + ch * 16 + (vp & 7) * 2) = v;
+      *reinterpret_cast<u32x4_t*>(kl + key * K_ROW + (((id & 15) ^ (key & 15)) << 4)) = kreg[i];
+      *reinterpret_cast<u32x4_t*>(vl + key * K_ROW + (((id & 15) ^ (4 * (key & 3))) << 4)) = vreg[i];
     }
   };
 
@@ -276,11 +244,24 @@ __global__ __launch_bounds__(NT, 2) void attn_bf16_kernel(AttnParams p) {
         pk[3] = pack_h2(s[i][hf * 8 + 6], s[i][hf * 8 + 7]);
         pf[sl] = __builtin_bit_cast(f16x8_t, pk);
       }
+      // A operand of step n (16-key slice sl = n/4, 32-dim tile dt = n%4): lane
+      // l needs 8 keys of dim 32 dt + l%32, in the order the P fragment holds
+      // them (keys 16 hf + 4 kh + 0..3, then + 8).  In each group of 16 lanes
+      // the transpose read hands lane j element j%4 of lanes 4e + j/4, e < 4;
+      // so lane i of the group points at key K0 + i/4, dims C + 4 (i%4) .. +3,
+      // and lane j receives keys K0 .. K0+3 of dim C + j.
+      const int il = lane & 15;
+      const int vkey = 4 * (lane >> 5) + (il >> 2);           // + 32 i + 16 hf (+ 8)
+      const int vc8 = 4 * ((lane >> 4) & 1) + (il & 3);        // + 8 dt, 8-byte chunk
+      const uint8_t* vrow = vl + vkey * K_ROW;
       auto vread = [&](int n) {
         const int sl = n >> 2, dt = n & 3;
-        const int dim = dt * 32 + fr;
-        const int ch = (2 * sl + fhalf) ^ swz8(dim);
-        return __builtin_bit_cast(f16x8_t, *reinterpret_cast<const u32x4_t*>(vl + dim * V_ROW + ch * 16));
+        const int key0 = 32 * (sl >> 1) + 16 * (sl & 1);
+        const int c8 = (8 * dt + vc8) ^ (8 * (vkey & 3));
+        const uint8_t* a = vrow + key0 * K_ROW + (c8 << 3);
+        const v4i16_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16_t*)a);
+        const v4i16_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16_t*)(a + 8 * K_ROW));
+        return __builtin_bit_cast(f16x8_t, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
       };
       f16x8_t vf[3];
       __builtin_amdgcn_sched_barrier(0);
@@ -291,7 +272,7 @@ __global__ __launch_bounds__(NT, 2) void attn_bf16_kernel(AttnParams p) {
       for (int n = 0; n < 16; ++n) {
         if (n + 2 < 16) vf[(n + 2) % 3] = vread(n + 2);
         o[n & 3] = __builtin_amdgcn_mfma_f32_32x32x16_f16(vf[n % 3], pf[n >> 2], o[n & 3], 0, 0, 0);
-        if (n + 2 < 16) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        if (n + 2 < 16) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
       }
       __builtin_amdgcn_sched_barrier(0);
