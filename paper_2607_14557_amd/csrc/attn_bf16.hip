@@ -20,6 +20,8 @@
 // (log2 units), so the O rescale is rare and P stays <= 256, exact in fp16.
 #include <math.h>
 
+#include <type_traits>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -154,10 +156,14 @@ __global__ __launch_bounds__(NT, 2) void attn_bf16_kernel(AttnParams p) {
   __builtin_amdgcn_s_waitcnt(0x0f70);       // vmcnt(0), other counters unconstrained
   __builtin_amdgcn_sched_barrier(0);
   __syncthreads();
-  for (int kt = 0; kt < n_kv; ++kt) {
+  // One tile: scores, online softmax, P V.  BUF is the LDS buffer holding the
+  // tile (compile-time, so every fragment address is a loop-invariant base
+  // plus an immediate); the next tile goes to the other buffer.
+  auto tile_step = [&](int kt, auto buf_tag) {
+    constexpr int BUF = decltype(buf_tag)::value;
     const int kbase = kt * KT;
-    const uint8_t* kl = k_lds[kt & 1];
-    const uint8_t* vl = v_lds[kt & 1];
+    const uint8_t* kl = k_lds[BUF];
+    const uint8_t* vl = v_lds[BUF];
     if (kt + 1 < n_kv) load_tile(kbase + KT);
 
     // S^T for 64 keys: two 32-key MFMA row tiles, walked over the 8 dim
@@ -277,10 +283,14 @@ __global__ __launch_bounds__(NT, 2) void attn_bf16_kernel(AttnParams p) {
       }
       __builtin_amdgcn_sched_barrier(0);
     }
-    // Buffer (kt+1)&1 was last read in iteration kt-1, which every wave left
-    // through the barrier below; one barrier then publishes tile kt+1.
-    if (kt + 1 < n_kv) store_tile((kt + 1) & 1);
+    // Buffer BUF^1 was last read in tile kt-1, which every wave left through
+    // the barrier below; one barrier then publishes tile kt+1.
+    if (kt + 1 < n_kv) store_tile(BUF ^ 1);
     __syncthreads();
+  };
+  for (int kt = 0; kt < n_kv; kt += 2) {
+    tile_step(kt, std::integral_constant<int, 0>{});
+    if (kt + 1 < n_kv) tile_step(kt + 1, std::integral_constant<int, 1>{});
   }
 
   // ---- normalise and store ----------------------------------------------------
