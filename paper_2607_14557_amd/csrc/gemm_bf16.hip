@@ -34,7 +34,7 @@ namespace {
 
 constexpr int BM = 256, BK = 64;
 constexpr int NT = 256;
-constexpr int GROUP_M = 8;
+constexpr int GROUP_M = 4;
 constexpr int ROW_BYTES = BK * 2;                   // 128 bytes per tile row
 
 __device__ __forceinline__ int swz(int r) { return (r & 7) ^ ((r >> 3) & 1); }
