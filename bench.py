@@ -128,11 +128,119 @@ def cpu_baseline(w, layers, batch, seconds):
                       % (nseq, w.batch, dt)}
 
 
+def bench_stack(args, w):
+    """A 32-layer stack: one job = step 0 (layers up to the detection layer on
+    the full window with the count, the SNR scan, routing + compaction, the
+    remaining layers on the compacted batch) plus the truncated denoising steps
+    (every layer on the compacted batch).  Prints one JSON line."""
+    import numpy as np
+    import torch
+    from paper_2607_14557_amd import seer as S
+    from paper_2607_14557_amd.runner import SeerStack, dims_for
+    from workloads.generate import layer_weights_torch, make_stack_batch
+
+    sh = w.shape
+    d, I, B, L = sh.d_model, sh.d_ff, w.batch, w.n_layers
+    dev = torch.device("cuda:0")
+    log("generating stack workload %s (%d layers)" % (w.name, L))
+    t0 = time.perf_counter()
+    batch = make_stack_batch(w, dev)
+    T = w.rows_full
+    granule = 256
+    cap = ((T + granule - 1) // granule) * granule + granule
+    dims = dims_for(d, sh.n_heads, sh.head_dim, I, "bf16", w.rms_eps)
+    st = SeerStack(dims, L, cap)
+    for l in range(L):
+        Wl = layer_weights_torch(w, l, dev)
+        st.set_layer(l, Wl)
+        del Wl
+    x = torch.from_numpy(batch.x).to(torch.bfloat16).to(dev)
+    i32 = lambda a: torch.from_numpy(np.asarray(a, np.int32)).to(dev)
+    cu, off, wl = i32(batch.cu_seqlens), i32(batch.win_off), i32(batch.win_len)
+    log("  inputs and %d prepacked layers ready in %.1f s" % (L, time.perf_counter() - t0))
+    sp = torch.cuda.current_stream().cuda_stream
+    hip = Hip()
+    n_trunc = w.trunc_steps
+
+    def job():
+        r = st.step0(x, cu, off, wl, B, T, w.l_det, w.act_eps, granule=granule, trunc_capacity=cap, stream=sp)
+        for _ in range(n_trunc):
+            st.forward(r.x_trunc, r.cu_trunc, r.seqused, B, cap, stream=sp)
+        return r
+
+    log("warmup %d job(s)" % args.warmup)
+    r = None
+    for _ in range(args.warmup):
+        r = job()
+    torch.cuda.synchronize()
+    log("timing %d job(s) of 1 + %d denoising steps" % (args.steps, n_trunc))
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        r = job()
+    torch.cuda.synchronize()
+    ms_job = (time.perf_counter() - t0) * 1e3 / args.steps
+    keep = r.keep_len.cpu().numpy()
+    if not np.array_equal(r.boundary.cpu().numpy(), batch.planted):
+        log("WARNING: detected boundaries differ from the planted ones")
+    rows_t = int(r.seqused.cpu().numpy().sum())
+
+    def timed(fn, reps=3):
+        e0, e1 = hip.event(), hip.event()
+        fn()
+        hip.record(e0, sp)
+        for _ in range(reps):
+            fn()
+        hip.record(e1, sp)
+        torch.cuda.synchronize()
+        return hip.ms(e0, e1) / reps
+
+    log("timing one truncated and one untruncated %d-layer step" % L)
+    t_trunc = timed(lambda: st.forward(r.x_trunc, r.cu_trunc, r.seqused, B, cap, stream=sp))
+    t_full = timed(lambda: st.forward(x, cu, None, B, T, stream=sp), reps=1)
+    # the dominant kernel: gate/up GEMM of a truncated step, timed inside one layer
+    ev = [hip.event() for _ in range(8)]
+    y = torch.empty(cap, d, dtype=torch.bfloat16, device=dev)
+    for _ in range(2):
+        S.seer_layer_forward_varlen_timed(dims, st.packed[0], r.x_trunc, y, cap, r.cu_trunc, r.seqused, B,
+                                          0.0, None, st.workspace, ev, stream=sp)
+    torch.cuda.synchronize()
+    gu_ms = hip.ms(ev[5], ev[6])
+    flop = rows_t * 2 * 2 * I * d
+    achieved = flop / (gu_ms * 1e-3) / 1e12
+    n_den = 1 + n_trunc
+    value = int(keep.sum()) * n_den / (ms_job * 1e-3)
+    out = {
+        "metric": "effective gen tokens/sec over step 0 + %d truncated denoising steps (%d-layer stack)"
+                  % (n_trunc, L),
+        "value": round(value, 1), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms_job, 3), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic (seeded; random-init LLaDA-8B-shaped %d-layer stack, planted EOS suffixes)" % L,
+        "config": {"workload": w.name, "batch": B, "visual_prefix": w.n_visual, "prompt": w.n_prompt,
+                   "window": w.window, "layers": L, "detection_layer": w.l_det,
+                   "denoising_steps_per_job": n_den, "sum_keep_len": int(keep.sum()), "rows_full": T,
+                   "rows_trunc": rows_t, "d_model": d, "heads": sh.n_heads, "head_dim": sh.head_dim,
+                   "d_ff": I},
+        "roofline": {"bound": "mfma", "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS,
+                     "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                     "kernel": "gemm_bf16_kernel<EPI_SWIGLU> (truncated-step gate/up GEMM, layer 0)",
+                     "flop_per_launch": flop, "launch_ms": round(gu_ms, 4)},
+        "trunc_step_ms": round(t_trunc, 3), "full_step_ms": round(t_full, 3),
+        "speedup_trunc_vs_full": round(t_full / t_trunc, 3),
+        "job_speedup_vs_untruncated": round(n_den * t_full / ms_job, 3),
+        "cpu_baseline": None,
+        "cpu_baseline_note": "one oracle step of a 32-layer stack takes hours; the default workload's line "
+                             "carries the CPU baseline",
+    }
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--steps", type=int, default=None,
+                    help="timed steps (default 20; 1 for the 32-layer stacks, where a step is a whole job)")
+    ap.add_argument("--warmup", type=int, default=None, help="untimed steps (default 5; 1 for the stacks)")
     ap.add_argument("--workload", default="llada_b16_ragged")
     ap.add_argument("--policy", default="hybrid", choices=["hybrid", "naive_pad", "varlen_only"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -161,8 +269,14 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     S.load_library()
     w = WORKLOADS[args.workload]
-    if w.n_layers != 1 or w.dtype != "bf16":
-        raise SystemExit("bench.py times single-layer bf16 workloads")
+    if args.steps is None:
+        args.steps = 20 if w.n_layers == 1 else 1
+    if args.warmup is None:
+        args.warmup = 5 if w.n_layers == 1 else 1
+    if w.dtype != "bf16":
+        raise SystemExit("bench.py times bf16 workloads")
+    if w.n_layers > 1:
+        return bench_stack(args, w)
     sh = w.shape
     d, I = sh.d_model, sh.d_ff
     policy = {"hybrid": S.SEER_ROUTE_HYBRID, "naive_pad": S.SEER_ROUTE_NAIVE_PAD,
