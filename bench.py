@@ -47,8 +47,8 @@ PEAK_HBM_GBS = 8000.0
 # was taken on: when their hash differs the figure is reported as null.
 TRAFFIC_SOURCES = ("paper_2607_14557_amd/csrc/gemm_bf16.hip", "paper_2607_14557_amd/csrc/kernels.h",
                    "paper_2607_14557_amd/csrc/common.h")
-TRAFFIC = {"sources_sha256": "0f8d5322bcd8f7a72135d64ee8de6f9372e1ed280e2a5d60b6221ebf78145772",
-           "rows": 14280, "fetch_bytes": 4218665363, "write_bytes": 350979994}
+TRAFFIC = {"sources_sha256": "e6e8db780e90d1b2283f1551123c260ab33448c94328189b1f3aefbb95a4f733",
+           "rows": 14280, "fetch_bytes": 4223313473, "write_bytes": 350945792}
 
 
 def sources_sha256():
