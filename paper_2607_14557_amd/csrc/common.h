@@ -15,6 +15,7 @@ typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4_t;
 // (not HIP's struct uint4): arrays of it stay in registers after unrolling,
 // where struct copies become private-memory memcpys.
 typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x2_t __attribute__((ext_vector_type(2)));
 
 typedef __attribute__((address_space(3))) void lds_void_t;
 typedef __attribute__((address_space(3))) uint8_t lds_u8_t;

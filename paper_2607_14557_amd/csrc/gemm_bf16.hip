@@ -270,12 +270,14 @@ __device__ __forceinline__ void gemm_tile(const GemmParams& p, uint8_t* smem, in
   constexpr bool kGlu = (EPI == EPI_SWIGLU || EPI == EPI_SWIGLU_COUNT);
   constexpr bool kRes = (EPI == EPI_RESID || EPI == EPI_RESID_DUAL || EPI == EPI_RESID_R32);
   const int cq = 4 * fhalf;
-  // Residual operands of one 32-row block: 4 NJ quads per lane, all fetched
-  // before the block is added and stored.  Issued inside the store loop they
-  // would wait out one load latency per quad (the compiler cannot move a load
-  // of R past a store to C that might alias it).
+  // Everything the epilogue reads besides the accumulators is requested up
+  // front: the row scales of the four 32-row blocks, and the residual quads
+  // (4 NJ per lane and block) of all four blocks, or, for fp32 residuals, of
+  // two blocks ahead.  Fetched block by block between the stores, each block
+  // would wait out a full memory latency behind the previous block's stores.
   using RQ = typename std::conditional<EPI == EPI_RESID_R32, f32x4_t, uint2>::type;
-  RQ rq[4 * NJ];
+  constexpr int RDEPTH = EPI == EPI_RESID_R32 ? 2 : 4;
+  RQ rq[RDEPTH][4 * NJ];
   // Per row one base pointer; the quads of a lane sit at constant offsets
   // (32 j + 8 q elements) from it.
   const int col0 = n0 + wn * (BN / 2) + cq;
@@ -292,17 +294,85 @@ __device__ __forceinline__ void gemm_tile(const GemmParams& p, uint8_t* smem, in
       for (int jq = 0; jq < 4 * NJ; ++jq) dst[jq] = *reinterpret_cast<const uint2*>(rb + 8 * jq);
     }
   };
+  float rsv[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    int row = m0 + wm * 128 + i * 32 + fr;
+    row = row < M ? row : M - 1;
+    rsv[i] = (EPI == EPI_SCALE || kGlu) ? p.rs[row] : 1.0f;
+  }
+  if constexpr (kRes) {
+#pragma unroll
+    for (int i = 0; i < RDEPTH; ++i) fetch(i, rq[i]);
+  }
+  // V columns of the QKV projection are stored as fp16 (block-uniform)
+  const bool to_f16 = EPI == EPI_SCALE && p.f16_col0 > 0 && n0 >= p.f16_col0;
+
+  // Stores: lanes l and l+32 hold the two 4-column halves of each 8-column
+  // group of a row.  One v_permlane32_swap per packed register gives lane l
+  // columns 8q..8q+7 and lane l+32 columns 8q+8..8q+15 of quads (q, q+1), so
+  // every lane writes 16 contiguous bytes: half the store instructions of
+  // 8-byte stores, which bound the epilogue.
+  auto store_pair = [&](uint16_t* base, uint2 a, uint2 b) {
+    const u32x2_t sx = __builtin_amdgcn_permlane32_swap(a.x, b.x, false, false);
+    const u32x2_t sy = __builtin_amdgcn_permlane32_swap(a.y, b.y, false, false);
+    *reinterpret_cast<u32x4_t*>(base) = u32x4_t{sx[0], sy[0], sx[1], sy[1]};
+  };
+
+  // One 32-row block of the non-GLU epilogues, straight-line for one output
+  // type (F16 is the type of the whole block).
+  auto store_block = [&](auto f16_tag, int i, const RQ* rr) {
+    constexpr bool F16 = decltype(f16_tag)::value;
+    const int row = m0 + wm * 128 + i * 32 + fr;
+    if (row >= M) return;
+    const float sc = rsv[i];
+    uint16_t* cb = C + (size_t)row * p.ldc + col0;
+    uint16_t* cw = C + (size_t)row * p.ldc + n0 + wn * (BN / 2) + 8 * fhalf;
+    float* c2b = EPI == EPI_RESID_DUAL ? static_cast<float*>(p.C2) + (size_t)row * p.ldc + col0 : nullptr;
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+      uint2 pk[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int cc = 32 * j + 8 * q;
+        float v[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[e] = acc[i][j][4 * q + e];
+        if constexpr (EPI == EPI_SCALE) {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) v[e] *= sc;
+        } else if constexpr (EPI == EPI_RESID || EPI == EPI_RESID_DUAL) {
+          const uint2 rv = rr[4 * j + q];
+          v[0] += __uint_as_float(rv.x << 16);
+          v[1] += __uint_as_float(rv.x & 0xffff0000u);
+          v[2] += __uint_as_float(rv.y << 16);
+          v[3] += __uint_as_float(rv.y & 0xffff0000u);
+        } else if constexpr (EPI == EPI_RESID_R32) {
+          const f32x4_t r32 = rr[4 * j + q];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) v[e] += r32[e];
+        }
+        pk[q].x = F16 ? pack_h2(v[0], v[1]) : pack_bf2(v[0], v[1]);
+        pk[q].y = F16 ? pack_h2(v[2], v[3]) : pack_bf2(v[2], v[3]);
+        if constexpr (EPI == EPI_RESID_DUAL)
+          *reinterpret_cast<f32x4_t*>(c2b + cc) = f32x4_t{v[0], v[1], v[2], v[3]};
+      }
+      store_pair(cw + 32 * j, pk[0], pk[1]);
+      store_pair(cw + 32 * j + 16, pk[2], pk[3]);
+    }
+  };
+
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const int row = m0 + wm * 128 + i * 32 + fr;
     const bool ok = row < M;
-    if constexpr (kRes) fetch(i, rq);
     if constexpr (kGlu) {
-      const float sc = ok ? p.rs[row] : 0.0f;
+      const float sc = rsv[i];
       int nz = 0;
 #pragma unroll
       for (int h = 0; h < NJ / 2; ++h) {
         const int col = (n0 + wn * (BN / 2)) / 2 + 32 * h + cq;
+        uint2 pk[4];
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
           float a[4];
@@ -313,54 +383,33 @@ __device__ __forceinline__ void gemm_tile(const GemmParams& p, uint8_t* smem, in
             // difference and equality gives +0 (no compare, no SGPR hazard)
             if constexpr (EPI == EPI_SWIGLU_COUNT) nz += __float_as_uint(fabsf(a[e]) - p.eps) >> 31;
           }
-          if (ok) {
-            uint2 pk;
-            pk.x = pack_bf2(a[0], a[1]);
-            pk.y = pack_bf2(a[2], a[3]);
-            *reinterpret_cast<uint2*>(C + (size_t)row * p.ldc + col + 8 * q) = pk;
-          }
+          pk[q].x = pack_bf2(a[0], a[1]);
+          pk[q].y = pack_bf2(a[2], a[3]);
+        }
+        // the swaps are wave-wide: every lane takes part, rows past M store nothing
+        uint16_t* cw = C + (size_t)row * p.ldc + col - cq + 8 * fhalf;
+        const u32x2_t s0x = __builtin_amdgcn_permlane32_swap(pk[0].x, pk[1].x, false, false);
+        const u32x2_t s0y = __builtin_amdgcn_permlane32_swap(pk[0].y, pk[1].y, false, false);
+        const u32x2_t s1x = __builtin_amdgcn_permlane32_swap(pk[2].x, pk[3].x, false, false);
+        const u32x2_t s1y = __builtin_amdgcn_permlane32_swap(pk[2].y, pk[3].y, false, false);
+        if (ok) {
+          *reinterpret_cast<u32x4_t*>(cw) = u32x4_t{s0x[0], s0y[0], s0x[1], s0y[1]};
+          *reinterpret_cast<u32x4_t*>(cw + 16) = u32x4_t{s1x[0], s1y[0], s1x[1], s1y[1]};
         }
       }
       if constexpr (EPI == EPI_SWIGLU_COUNT) {
         nz += __shfl_xor(nz, 32, kWave);
         if (ok && fhalf == 0) atomicAdd(p.cnt + row, nz);
       }
-    } else if (ok) {
-      float sc = 1.0f;
-      if constexpr (EPI == EPI_SCALE) sc = p.rs[row];
-      const bool to_f16 = EPI == EPI_SCALE && p.f16_col0 > 0 && n0 >= p.f16_col0;   // block-uniform
-      const RQ* rr = rq;
-      uint16_t* cb = C + (size_t)row * p.ldc + col0;
-      float* c2b = EPI == EPI_RESID_DUAL ? static_cast<float*>(p.C2) + (size_t)row * p.ldc + col0 : nullptr;
-#pragma unroll
-      for (int j = 0; j < NJ; ++j) {
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const int cc = 32 * j + 8 * q;
-          float v[4];
-#pragma unroll
-          for (int e = 0; e < 4; ++e) v[e] = acc[i][j][4 * q + e];
-          if constexpr (EPI == EPI_SCALE) {
-#pragma unroll
-            for (int e = 0; e < 4; ++e) v[e] *= sc;
-          } else if constexpr (EPI == EPI_RESID || EPI == EPI_RESID_DUAL) {
-            const uint2 rv = rr[4 * j + q];
-            v[0] += __uint_as_float(rv.x << 16);
-            v[1] += __uint_as_float(rv.x & 0xffff0000u);
-            v[2] += __uint_as_float(rv.y << 16);
-            v[3] += __uint_as_float(rv.y & 0xffff0000u);
-          } else {
-            const f32x4_t r32 = rr[4 * j + q];
-#pragma unroll
-            for (int e = 0; e < 4; ++e) v[e] += r32[e];
-          }
-          uint2 pk;
-          pk.x = to_f16 ? pack_h2(v[0], v[1]) : pack_bf2(v[0], v[1]);
-          pk.y = to_f16 ? pack_h2(v[2], v[3]) : pack_bf2(v[2], v[3]);
-          *reinterpret_cast<uint2*>(cb + cc) = pk;
-          if constexpr (EPI == EPI_RESID_DUAL)
-            *reinterpret_cast<f32x4_t*>(c2b + cc) = f32x4_t{v[0], v[1], v[2], v[3]};
-        }
+    } else {
+      const RQ* rr = rq[i % RDEPTH];
+      if (EPI == EPI_SCALE && to_f16)
+        store_block(std::true_type{}, i, rr);
+      else
+        store_block(std::false_type{}, i, rr);
+      // fp32 residuals: the block two ahead goes into the buffer just used
+      if constexpr (EPI == EPI_RESID_R32) {
+        if (i + RDEPTH < 4) fetch(i + RDEPTH, rq[i % RDEPTH]);
       }
     }
   }
