@@ -113,9 +113,11 @@ size_t seer_layer_workspace_bytes(const seer_dims* dims, int32_t max_rows);
  *   offsets[3] act  [max_rows, d_ff]        silu(gate) * up
  *   offsets[4] fp32 [max_rows]              1/rms of x
  *   offsets[5] fp32 [max_rows]              1/rms of h1 (as the MLP reads it)
- *   offsets[6] fp32 [max_rows, d_model]     h1 unrounded, used for the final
- *                                           residual add (bf16 layers; fp32
- *                                           layers: equal to offsets[2])
+ *   offsets[6] bf16 [max_rows, d_model]     low part of h1, bf16(h1 - bf16(h1)):
+ *                                           the final residual add uses
+ *                                           offsets[2] + offsets[6], h1 to
+ *                                           ~2^-17 (bf16 layers; fp32 layers:
+ *                                           equal to offsets[2])
  *   offsets[7] total workspace bytes
  * Rows [0, cu_seqlens[batch]) of the last call are valid.  Meant for
  * inspection and teacher-forced checks.  Errors: EINVAL, EUNSUPPORTED. */
@@ -132,7 +134,7 @@ int seer_layer_workspace_offsets(const seer_dims* dims, int32_t max_rows, size_t
  * Precision (bf16 layers): operands bf16, accumulation fp32; q, k, v, o, h1
  * and act are rounded to bf16 where they feed a matrix product; the
  * probabilities of the attention-weighted sum are kept in fp16; the residual
- * h1 enters the final add unrounded (fp32).
+ * h1 enters the final add as a bf16 high/low pair (exact to ~2^-17).
  * x_in, x_out: [total_rows_ub, d_model] rows (may not alias).  Only rows
  * [0, cu_seqlens[batch]) are read and written.
  * seqused: optional [batch]; when given, rows at index >= seqused[b] inside

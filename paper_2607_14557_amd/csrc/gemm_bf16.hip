@@ -16,8 +16,9 @@
 //   SCALE   C = bf16(acc * rowscale[r])         folded RMSNorm before QKV;
 //           column tiles from f16_col0 on (V) are stored as fp16 instead
 //   RESID   C = bf16(R[r,c] + acc)              residual add
-//   RESID_DUAL  as RESID, plus an fp32 copy     residual after O (h1 kept in fp32)
-//   RESID_R32   C = bf16(R32[r,c] + acc)        residual after down, fp32 h1
+//   RESID_SPLIT v = R[r,c] + acc: C = bf16(v) and residual after O: h1 as a bf16
+//               C2 = bf16(v - C)                high/low pair, exact to ~2^-17
+//   RESID_PAIR  C = bf16(R + R2 + acc)          residual after down from that pair
 //   SWIGLU  act = silu(acc_g * s) * (acc_u * s) gate/up with folded RMSNorm;
 //           the packed weight interleaves 32 gate rows with 32 up rows, so a
 //           wave holds matching gate and up columns in its registers
@@ -263,35 +264,39 @@ __device__ __forceinline__ void gemm_tile(const GemmParams& p, uint8_t* smem, in
   // (i, j) accumulates the transposed 32x32 block: register r holds output
   // row m0 + 128 wm + 32 i + lane%32 and column n0 + (BN/2) wn + 32 j + 8 (r/4) +
   // 4 (lane/32) + r%4.  Each lane owns one row and four consecutive columns
-  // per register quad, written straight from registers as one 8-byte bf16
-  // store (16 contiguous bytes per row over a lane pair).  For SWIGLU the
-  // gate/up tiles (j = 2h, 2h+1) sit in the same lane and register; the
-  // near-zero count is a per-lane tally of its row, folded over the lane pair.
+  // per register quad; lanes l and l+32 hold the two halves of each 8-column
+  // group.  Stores and residual loads move 16 bytes (8 columns) per lane, and
+  // one v_permlane32_swap per register pair deals them between the two
+  // layouts.  For SWIGLU the gate/up tiles (j = 2h, 2h+1) sit in the same lane
+  // and register; the near-zero count is a per-lane tally of its row, folded
+  // over the lane pair.
   constexpr bool kGlu = (EPI == EPI_SWIGLU || EPI == EPI_SWIGLU_COUNT);
-  constexpr bool kRes = (EPI == EPI_RESID || EPI == EPI_RESID_DUAL || EPI == EPI_RESID_R32);
+  constexpr bool kRes = (EPI == EPI_RESID || EPI == EPI_RESID_SPLIT || EPI == EPI_RESID_PAIR);
+  constexpr bool kPair = EPI == EPI_RESID_PAIR;
   const int cq = 4 * fhalf;
-  // Everything the epilogue reads besides the accumulators is requested up
-  // front: the row scales of the four 32-row blocks, and the residual quads
-  // (4 NJ per lane and block) of all four blocks, or, for fp32 residuals, of
-  // two blocks ahead.  Fetched block by block between the stores, each block
-  // would wait out a full memory latency behind the previous block's stores.
-  using RQ = typename std::conditional<EPI == EPI_RESID_R32, f32x4_t, uint2>::type;
-  constexpr int RDEPTH = EPI == EPI_RESID_R32 ? 2 : 4;
-  RQ rq[RDEPTH][4 * NJ];
-  // Per row one base pointer; the quads of a lane sit at constant offsets
-  // (32 j + 8 q elements) from it.
+  // Everything the epilogue reads besides the accumulators is requested ahead
+  // of its use: the row scales of the four 32-row blocks, and the residual
+  // columns of all four blocks (of two blocks ahead for a high/low pair).
+  // Fetched block by block between the stores, each block would wait out a
+  // full memory latency behind the previous block's stores.  Residual word jt
+  // of a block holds columns 16 jt + 8 (lane/32) .. +7 of the lane's row.
+  constexpr int NRQ = (kPair ? 2 : 1) * 2 * NJ;
+  constexpr int RDEPTH = kPair ? 2 : 4;
+  u32x4_t rq[RDEPTH][NRQ];
   const int col0 = n0 + wn * (BN / 2) + cq;
-  auto fetch = [&](int i, RQ* dst) {
+  const int colw = n0 + wn * (BN / 2) + 8 * fhalf;
+  auto fetch = [&](int i, u32x4_t* dst) {
     int row = m0 + wm * 128 + i * 32 + fr;
     row = row < M ? row : M - 1;             // rows past M are never stored
-    if constexpr (EPI == EPI_RESID_R32) {
-      const float* rb = p.R32 + (size_t)row * p.ldr + col0;
+    if constexpr (kRes) {
+      const uint16_t* rb = R + (size_t)row * p.ldr + colw;
 #pragma unroll
-      for (int jq = 0; jq < 4 * NJ; ++jq) dst[jq] = *reinterpret_cast<const f32x4_t*>(rb + 8 * jq);
-    } else if constexpr (kRes) {
-      const uint16_t* rb = R + (size_t)row * p.ldr + col0;
+      for (int jt = 0; jt < 2 * NJ; ++jt) dst[jt] = *reinterpret_cast<const u32x4_t*>(rb + 16 * jt);
+    }
+    if constexpr (kPair) {
+      const uint16_t* rb = static_cast<const uint16_t*>(p.R2) + (size_t)row * p.ldr + colw;
 #pragma unroll
-      for (int jq = 0; jq < 4 * NJ; ++jq) dst[jq] = *reinterpret_cast<const uint2*>(rb + 8 * jq);
+      for (int jt = 0; jt < 2 * NJ; ++jt) dst[2 * NJ + jt] = *reinterpret_cast<const u32x4_t*>(rb + 16 * jt);
     }
   };
   float rsv[4];
@@ -318,47 +323,66 @@ __device__ __forceinline__ void gemm_tile(const GemmParams& p, uint8_t* smem, in
     const u32x2_t sy = __builtin_amdgcn_permlane32_swap(a.y, b.y, false, false);
     *reinterpret_cast<u32x4_t*>(base) = u32x4_t{sx[0], sy[0], sx[1], sy[1]};
   };
+  // the inverse: a 16-byte residual word back to the quads (q, q+1)
+  auto split_pair = [&](u32x4_t w, uint2& a, uint2& b) {
+    const u32x2_t sx = __builtin_amdgcn_permlane32_swap(w[0], w[2], false, false);
+    const u32x2_t sy = __builtin_amdgcn_permlane32_swap(w[1], w[3], false, false);
+    a.x = sx[0]; a.y = sy[0];
+    b.x = sx[1]; b.y = sy[1];
+  };
+  auto add_bf4 = [](float* v, uint2 r) {
+    v[0] += __uint_as_float(r.x << 16);
+    v[1] += __uint_as_float(r.x & 0xffff0000u);
+    v[2] += __uint_as_float(r.y << 16);
+    v[3] += __uint_as_float(r.y & 0xffff0000u);
+  };
 
   // One 32-row block of the non-GLU epilogues, straight-line for one output
   // type (F16 is the type of the whole block).
-  auto store_block = [&](auto f16_tag, int i, const RQ* rr) {
+  auto store_block = [&](auto f16_tag, int i, const u32x4_t* rr) {
     constexpr bool F16 = decltype(f16_tag)::value;
     const int row = m0 + wm * 128 + i * 32 + fr;
     if (row >= M) return;
     const float sc = rsv[i];
-    uint16_t* cb = C + (size_t)row * p.ldc + col0;
-    uint16_t* cw = C + (size_t)row * p.ldc + n0 + wn * (BN / 2) + 8 * fhalf;
-    float* c2b = EPI == EPI_RESID_DUAL ? static_cast<float*>(p.C2) + (size_t)row * p.ldc + col0 : nullptr;
+    uint16_t* cw = C + (size_t)row * p.ldc + colw;
+    uint16_t* cw2 = EPI == EPI_RESID_SPLIT ? static_cast<uint16_t*>(p.C2) + (size_t)row * p.ldc + colw : nullptr;
 #pragma unroll
     for (int j = 0; j < NJ; ++j) {
-      uint2 pk[4];
+      uint2 rv[4], rv2[4];
+      if constexpr (kRes) {
+        split_pair(rr[2 * j], rv[0], rv[1]);
+        split_pair(rr[2 * j + 1], rv[2], rv[3]);
+      }
+      if constexpr (kPair) {
+        split_pair(rr[2 * NJ + 2 * j], rv2[0], rv2[1]);
+        split_pair(rr[2 * NJ + 2 * j + 1], rv2[2], rv2[3]);
+      }
+      uint2 pk[4], lo[4];
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        const int cc = 32 * j + 8 * q;
         float v[4];
 #pragma unroll
         for (int e = 0; e < 4; ++e) v[e] = acc[i][j][4 * q + e];
         if constexpr (EPI == EPI_SCALE) {
 #pragma unroll
           for (int e = 0; e < 4; ++e) v[e] *= sc;
-        } else if constexpr (EPI == EPI_RESID || EPI == EPI_RESID_DUAL) {
-          const uint2 rv = rr[4 * j + q];
-          v[0] += __uint_as_float(rv.x << 16);
-          v[1] += __uint_as_float(rv.x & 0xffff0000u);
-          v[2] += __uint_as_float(rv.y << 16);
-          v[3] += __uint_as_float(rv.y & 0xffff0000u);
-        } else if constexpr (EPI == EPI_RESID_R32) {
-          const f32x4_t r32 = rr[4 * j + q];
-#pragma unroll
-          for (int e = 0; e < 4; ++e) v[e] += r32[e];
         }
+        if constexpr (kRes) add_bf4(v, rv[q]);
+        if constexpr (kPair) add_bf4(v, rv2[q]);
         pk[q].x = F16 ? pack_h2(v[0], v[1]) : pack_bf2(v[0], v[1]);
         pk[q].y = F16 ? pack_h2(v[2], v[3]) : pack_bf2(v[2], v[3]);
-        if constexpr (EPI == EPI_RESID_DUAL)
-          *reinterpret_cast<f32x4_t*>(c2b + cc) = f32x4_t{v[0], v[1], v[2], v[3]};
+        if constexpr (EPI == EPI_RESID_SPLIT) {
+          // v - bf16(v) is exact in fp32; its bf16 rounding leaves ~2^-17 of v
+          lo[q].x = pack_bf2(v[0] - __uint_as_float(pk[q].x << 16), v[1] - __uint_as_float(pk[q].x & 0xffff0000u));
+          lo[q].y = pack_bf2(v[2] - __uint_as_float(pk[q].y << 16), v[3] - __uint_as_float(pk[q].y & 0xffff0000u));
+        }
       }
       store_pair(cw + 32 * j, pk[0], pk[1]);
       store_pair(cw + 32 * j + 16, pk[2], pk[3]);
+      if constexpr (EPI == EPI_RESID_SPLIT) {
+        store_pair(cw2 + 32 * j, lo[0], lo[1]);
+        store_pair(cw2 + 32 * j + 16, lo[2], lo[3]);
+      }
     }
   };
 
@@ -402,13 +426,13 @@ __device__ __forceinline__ void gemm_tile(const GemmParams& p, uint8_t* smem, in
         if (ok && fhalf == 0) atomicAdd(p.cnt + row, nz);
       }
     } else {
-      const RQ* rr = rq[i % RDEPTH];
+      const u32x4_t* rr = rq[i % RDEPTH];
       if (EPI == EPI_SCALE && to_f16)
         store_block(std::true_type{}, i, rr);
       else
         store_block(std::false_type{}, i, rr);
-      // fp32 residuals: the block two ahead goes into the buffer just used
-      if constexpr (EPI == EPI_RESID_R32) {
+      // high/low residuals: the block two ahead goes into the buffer just used
+      if constexpr (kPair) {
         if (i + RDEPTH < 4) fetch(i + RDEPTH, rq[i % RDEPTH]);
       }
     }
@@ -457,10 +481,10 @@ int launch_gemm_bf16(int epi, const GemmParams& p, hipStream_t s) {
     case EPI_SWIGLU: hipLaunchKernelGGL(gemm_bf16_kernel<EPI_SWIGLU>, grid, block, 0, s, p); break;
     case EPI_SWIGLU_COUNT:
       hipLaunchKernelGGL(gemm_bf16_kernel<EPI_SWIGLU_COUNT>, grid, block, 0, s, p); break;
-    case EPI_RESID_DUAL:
-      hipLaunchKernelGGL(gemm_bf16_kernel<EPI_RESID_DUAL>, grid, block, 0, s, p); break;
-    case EPI_RESID_R32:
-      hipLaunchKernelGGL(gemm_bf16_kernel<EPI_RESID_R32>, grid, block, 0, s, p); break;
+    case EPI_RESID_SPLIT:
+      hipLaunchKernelGGL(gemm_bf16_kernel<EPI_RESID_SPLIT>, grid, block, 0, s, p); break;
+    case EPI_RESID_PAIR:
+      hipLaunchKernelGGL(gemm_bf16_kernel<EPI_RESID_PAIR>, grid, block, 0, s, p); break;
     default: return -1;
   }
   return hipGetLastError() == hipSuccess ? 0 : -1;

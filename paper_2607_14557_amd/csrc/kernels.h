@@ -7,10 +7,11 @@
 namespace seer {
 
 // SCALE: C = acc * rs[r]; RESID: C = R + acc; SWIGLU(_COUNT): gate/up pairs;
-// RESID_DUAL: C = bf16(R + acc) and C2 = fp32(R + acc); RESID_R32: C = bf16(R32 + acc).
+// RESID_SPLIT: v = R + acc, C = bf16(v), C2 = bf16(v - C) (bf16 only);
+// RESID_PAIR: C = bf16(R + R2 + acc) (bf16 only).
 enum Epilogue {
   EPI_SCALE = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_SWIGLU_COUNT = 3,
-  EPI_RESID_DUAL = 4, EPI_RESID_R32 = 5
+  EPI_RESID_SPLIT = 4, EPI_RESID_PAIR = 5
 };
 
 // C[M,N] = A[M,K] * B[N,K]^T with a fused epilogue.  M is read on the device
@@ -20,8 +21,8 @@ struct GemmParams {
   const void* B;
   void* C;
   const void* R;      // residual rows (RESID*), same element type as C
-  void* C2;           // fp32 copy of the output (RESID_DUAL)
-  const float* R32;   // fp32 residual rows (RESID_R32), leading dimension ldr
+  void* C2;           // low part of the output, same layout as C (RESID_SPLIT)
+  const void* R2;     // low part of the residual, same layout as R (RESID_PAIR)
   const float* rs;    // per-row scale (SCALE, SWIGLU*)
   int* cnt;           // per-row near-zero count (SWIGLU_COUNT)
   float eps;

@@ -61,7 +61,7 @@ int check_dims(const seer_dims* d) {
 }
 
 struct WsLayout {
-  size_t qkv, o, h1, act, inv1, inv2, h1f, total;
+  size_t qkv, o, h1, act, inv1, inv2, h1lo, total;
 };
 
 WsLayout ws_layout(const seer_dims* d, int rows) {
@@ -75,9 +75,10 @@ WsLayout ws_layout(const seer_dims* d, int rows) {
   L.act = off; off = up256(off + R * d->d_ff * es);
   L.inv1 = off; off = up256(off + R * 4);
   L.inv2 = off; off = up256(off + R * 4);
-  // bf16 layers keep an fp32 copy of h1 for the final residual add
-  L.h1f = d->dtype == SEER_DTYPE_BF16 ? off : L.h1;
-  if (d->dtype == SEER_DTYPE_BF16) off = up256(off + R * d->d_model * 4);
+  // bf16 layers keep the low part of h1, bf16(h1 - bf16(h1)), for the final
+  // residual add
+  L.h1lo = d->dtype == SEER_DTYPE_BF16 ? off : L.h1;
+  if (d->dtype == SEER_DTYPE_BF16) off = up256(off + R * d->d_model * 2);
   L.total = off;
   return L;
 }
@@ -130,7 +131,7 @@ int seer_layer_workspace_offsets(const seer_dims* dims, int32_t max_rows, size_t
   const WsLayout L = ws_layout(dims, max_rows);
   offsets[0] = L.qkv; offsets[1] = L.o; offsets[2] = L.h1;
   offsets[3] = L.act; offsets[4] = L.inv1; offsets[5] = L.inv2;
-  offsets[6] = L.h1f; offsets[7] = L.total;
+  offsets[6] = L.h1lo; offsets[7] = L.total;
   return ok();
 }
 
@@ -163,7 +164,7 @@ static int layer_forward_impl(const seer_dims* dims, const void* w_packed, const
   void* act = ws + L.act;
   float* inv1 = reinterpret_cast<float*>(ws + L.inv1);
   float* inv2 = reinterpret_cast<float*>(ws + L.inv2);
-  float* h1f = reinterpret_cast<float*>(ws + L.h1f);
+  void* h1lo = ws + L.h1lo;
   int n_units = 0;                      // CUs: sizes the split of a partly filled last GEMM round
   if (bf16) {
     int dev = 0;
@@ -208,10 +209,10 @@ static int layer_forward_impl(const seer_dims* dims, const void* w_packed, const
   {
     seer::GemmParams g{};
     g.n_units = n_units;
-    g.A = o; g.B = wb + P.o * es; g.C = h1; g.R = x_in; g.C2 = h1f;
+    g.A = o; g.B = wb + P.o * es; g.C = h1; g.R = x_in; g.C2 = h1lo;
     g.m_ptr = m_ptr; g.m_ub = R; g.N = d; g.K = d;
     g.lda = d; g.ldb = d; g.ldc = d; g.ldr = d;
-    if (gemm(bf16 ? seer::EPI_RESID_DUAL : seer::EPI_RESID, g, stream)) return hip_fail("o gemm launch");
+    if (gemm(bf16 ? seer::EPI_RESID_SPLIT : seer::EPI_RESID, g, stream)) return hip_fail("o gemm launch");
   }
   // 5. RMSNorm statistics before the MLP
   if (mark(4) != hipSuccess) return hip_fail("event record");
@@ -241,10 +242,10 @@ static int layer_forward_impl(const seer_dims* dims, const void* w_packed, const
   {
     seer::GemmParams g{};
     g.n_units = n_units;
-    g.A = act; g.B = wb + P.dn * es; g.C = x_out; g.R = h1; g.R32 = h1f;
+    g.A = act; g.B = wb + P.dn * es; g.C = x_out; g.R = h1; g.R2 = h1lo;
     g.m_ptr = m_ptr; g.m_ub = R; g.N = d; g.K = I;
     g.lda = I; g.ldb = I; g.ldc = d; g.ldr = d;
-    if (gemm(bf16 ? seer::EPI_RESID_R32 : seer::EPI_RESID, g, stream)) return hip_fail("down gemm launch");
+    if (gemm(bf16 ? seer::EPI_RESID_PAIR : seer::EPI_RESID, g, stream)) return hip_fail("down gemm launch");
   }
   if (mark(7) != hipSuccess) return hip_fail("event record");
   return ok();

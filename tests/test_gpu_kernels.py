@@ -203,7 +203,11 @@ class _Layer:
         if name.startswith("inv"):
             return view_ws_f32(self.ws, self.off[idx], rows)
         if name == "h1f":
-            return view_ws(self.ws, self.off[idx], rows, cols, "f32")
+            # h1 as the final residual add reads it: bf16 high part + bf16 low part
+            if self.dtype == "f32":
+                return view_ws(self.ws, self.off[idx], rows, cols, "f32")
+            return (view_ws(self.ws, self.off[2], rows, cols, "bf16").float() +
+                    view_ws(self.ws, self.off[idx], rows, cols, "bf16").float())
         t = view_ws(self.ws, self.off[idx], rows, cols, self.dtype)
         if name == "qkv" and self.dtype == "bf16":
             # bf16 layers store the v third in fp16 (the type of the P V product)
@@ -261,7 +265,7 @@ def test_layer_vs_oracle_ragged(S, dtype):
         # the fp32 activations are stored unrounded: the kernel's count must be
         # exactly the count of its own activations
         np.testing.assert_array_equal(host(cnt)[:T], near_zero_count(act, eps))
-    # the final residual add uses the unrounded h1
+    # the final residual add uses h1 to ~2^-17 (bf16 high + low part)
     h1f = host(L.inter("h1f", T, d))
     assert rel_err(h1f, x[:T] + o @ W["wo"].T) <= (1e-5 if dtype == "bf16" else tol)
     e_dn = rel_err(y[:T], h1f + act @ W["wd"].T)
