@@ -47,8 +47,8 @@ PEAK_HBM_GBS = 8000.0
 # was taken on: when their hash differs the figure is reported as null.
 TRAFFIC_SOURCES = ("paper_2607_14557_amd/csrc/gemm_bf16.hip", "paper_2607_14557_amd/csrc/kernels.h",
                    "paper_2607_14557_amd/csrc/common.h")
-TRAFFIC = {"sources_sha256": "e6e8db780e90d1b2283f1551123c260ab33448c94328189b1f3aefbb95a4f733",
-           "rows": 14280, "fetch_bytes": 4223313473, "write_bytes": 350945792}
+TRAFFIC = {"sources_sha256": "c610919eb9a6bcea160da85aa97936db7fa8b0bf2ae9237e8d7c33bd26a216d6",
+           "rows": 14280, "fetch_bytes": 4223505272, "write_bytes": 350945600}
 
 
 def sources_sha256():
