@@ -13,6 +13,8 @@ Modules (each function cites the passage of the paper it follows):
   route     -- static micro-buckets, padding waste ratio, three-tier routing
                and the compaction layout (Sec. 3.4-3.5)
   pipeline  -- step 0 detection, one-shot truncation, truncated steps
+  kvcache   -- truncated steps on the window rows with the prefix's keys and
+               values cached (Appendix D, KV-cache compatibility)
 
 Parity status: every function here is pinned by CPU tests against values
 fixed by the mathematics (brute force, closed forms, invariants, planted
@@ -25,3 +27,4 @@ from .detect import detect_boundary, detect_batch
 from .route import (bucket_set, bucket_of, padding_waste_ratio, coarse_class,
                     route_batch, repack_rows, RouteResult)
 from .pipeline import run_pipeline, PipelineResult
+from .kvcache import prefix_kv, layer_forward_cached_rows, layer_forward_cached
