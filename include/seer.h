@@ -15,6 +15,8 @@
  *                              optional fused near-zero activation count
  *   seer_step0_detect          the SNR boundary criterion per sequence
  *   seer_batch_repack          padding-waste-aware routing plus compaction
+ *   seer_kv_export,            truncated steps on the window rows with the
+ *   seer_layer_forward_cached  prefix keys/values cached (Appendix D)
  *
  * Conventions shared by every call:
  *   - Buffers are owned by the caller.  Pointers are device pointers unless a
@@ -169,6 +171,44 @@ int seer_layer_forward_varlen_timed(const seer_dims* dims, const void* w_packed,
                                     void* workspace, size_t workspace_bytes,
                                     hipStream_t stream, hipEvent_t events[8]);
 
+/* Truncated step with the prefix's keys and values cached (the KV-cache
+ * combination of Appendix D, compatibility with KV caching): the layer of
+ * seer_layer_forward_varlen on rows that hold only the kept generation
+ * window of each sequence, every row attending to the cached keys of its
+ * sequence's prefix followed by the sequence's own keys.
+ * x_in, x_out, total_rows_ub, cu_seqlens, seqused, batch, workspace: as in
+ * seer_layer_forward_varlen, for the window rows (seqused[b] = real window
+ * rows; padding rows are no keys and receive no attention output).
+ * kv_cache: [kv_rows, 2 d_model] rows of K | V as seer_kv_export writes
+ * them (bf16 layers: K bf16, V fp16; fp32 layers: fp32), 16-byte aligned;
+ * sequence b's prefix is rows [cu_kv[b], cu_kv[b+1]) (cu_kv: [batch+1],
+ * device, non-decreasing); kv_rows_ub >= cu_kv[batch] bounds it.
+ * Given the cache of a full step over the same inputs, the outputs equal
+ * that step's window rows.  No near-zero count (only step 0 counts).
+ * Errors: as seer_layer_forward_varlen; EINVAL (kv_cache or cu_kv NULL,
+ * kv_rows_ub < 0, misaligned cache), EUNSUPPORTED (kv_rows_ub * 2 d_model
+ * >= 2^32). */
+int seer_layer_forward_cached(const seer_dims* dims, const void* w_packed,
+                              const void* x_in, void* x_out, int32_t total_rows_ub,
+                              const int32_t* cu_seqlens, const int32_t* seqused,
+                              int32_t batch, const void* kv_cache, const int32_t* cu_kv,
+                              int32_t kv_rows_ub, void* workspace, size_t workspace_bytes,
+                              hipStream_t stream);
+
+/* Cache the prefix keys and values of the last layer call made on
+ * `workspace` (with the same total_rows_ub): for sequence b, the K | V
+ * columns of its first cu_kv[b+1] - cu_kv[b] rows (rows [cu_seqlens[b], ...)
+ * of that call) go to kv_dst rows [cu_kv[b], cu_kv[b+1]) ([kv_rows, 2 d_model],
+ * element types as in the call's qkv region).  kv_rows_ub >= cu_kv[batch]
+ * sizes the launch.  Cache rows of a prefix longer than its sequence are left
+ * untouched.  Errors: EINVAL (null pointers, batch < 1, total_rows_ub < 1,
+ * kv_rows_ub < 0, misaligned workspace or kv_dst), EUNSUPPORTED (dims),
+ * EWORKSPACE. */
+int seer_kv_export(const seer_dims* dims, const void* workspace, size_t workspace_bytes,
+                   int32_t total_rows_ub, const int32_t* cu_seqlens, int32_t batch,
+                   const int32_t* cu_kv, int32_t kv_rows_ub, void* kv_dst,
+                   hipStream_t stream);
+
 /* SNR criterion parameters as exact rationals: tau_jump = tau_num/tau_den,
  * gamma = gamma_num/gamma_den; lookahead = size of the window W_i.
  * The paper's defaults are {3, 100, 3, 5, 3}. */
@@ -216,8 +256,12 @@ typedef struct seer_repack_desc {
   int32_t row_bytes;         /* bytes per row, a positive multiple of 16 */
   int32_t dst_capacity_rows; /* rows available in every dst buffer */
   int32_t max_batch_hint;    /* unused, 0 */
-  int32_t reserved;
+  int32_t flags;             /* SEER_REPACK_* bits, 0 for the default layout */
 } seer_repack_desc;
+
+/* seer_repack_desc.flags: copy only the kept window rows of each sequence
+ * (no prefix rows), the input layout of seer_layer_forward_cached. */
+#define SEER_REPACK_WINDOW_ONLY 1
 
 /* Control word written by seer_batch_repack: the routed shape of the batch,
  * so a host can pick the launch configuration of the next steps without
@@ -249,6 +293,9 @@ typedef struct seer_route_ctrl {
  * rows [cu_dst[b], ...) and the rest of its allocation is zero-filled;
  * cu_dst[b+1] = cu_dst[b] + win_off[b] + alloc_b; seqused[b] =
  * win_off[b] + keep_len[b]; rows [cu_dst[batch], capacity) are zero-filled.
+ * With SEER_REPACK_WINDOW_ONLY in desc->flags the prefix rows are left out:
+ * rows [win_off[b], win_off[b] + keep_len[b]) of sequence b are copied,
+ * cu_dst[b+1] = cu_dst[b] + alloc_b and seqused[b] = keep_len[b].
  * Order of sequences is preserved.  ctrl_dev (device) and ctrl_host
  * (host-pinned, hipHostMalloc'ed) are optional.  If the routed capacity
  * exceeds desc->dst_capacity_rows, nothing is copied, cu_dst is all zero and

@@ -31,23 +31,28 @@ def prefix_kv(x_seq, W, rms_eps, n_prefix):
     return a @ _w(W, "wk").T, a @ _w(W, "wv").T
 
 
-def layer_forward_cached_rows(x_win, used, k_pre, v_pre, W, n_heads, rms_eps, want_act=False):
+def layer_forward_cached_rows(x_win, used, k_pre, v_pre, W, n_heads, rms_eps, want_act=False,
+                              rows=None):
     """The layer on the window rows of one sequence with cached prefix keys.
 
     x_win: [Sw, d] window rows; rows [0, used) are real.  k_pre, v_pre:
     [P, d] cached keys/values of the prefix.  Every real row attends to the
-    P prefix keys followed by the `used` window keys.  Returns dict y [Sw, d]
-    (and act, h1 when want_act)."""
+    P prefix keys followed by the `used` window keys.  ``rows``: the window
+    rows whose outputs are wanted (default all).  Returns dict y
+    [len(rows), d] (and act, h1 when want_act)."""
     x = np.asarray(x_win, np.float64)
+    rows = np.arange(x.shape[0]) if rows is None else np.asarray(rows, np.int64)
     g1, g2 = _w(W, "g1"), _w(W, "g2")
-    a = rms_norm(x, g1, rms_eps)
-    q = a @ _w(W, "wq").T
-    k = np.concatenate([np.asarray(k_pre, np.float64), a[:used] @ _w(W, "wk").T], axis=0)
-    v = np.concatenate([np.asarray(v_pre, np.float64), a[:used] @ _w(W, "wv").T], axis=0)
-    o = np.zeros_like(x)
-    if used > 0 and k.shape[0] > 0:
-        o[:used] = attention_seq(q[:used], k, v, n_heads)
-    h1 = x + o @ _w(W, "wo").T
+    a_keys = rms_norm(x[:used], g1, rms_eps)
+    k = np.concatenate([np.asarray(k_pre, np.float64), a_keys @ _w(W, "wk").T], axis=0)
+    v = np.concatenate([np.asarray(v_pre, np.float64), a_keys @ _w(W, "wv").T], axis=0)
+    xr = x[rows]
+    q = rms_norm(xr, g1, rms_eps) @ _w(W, "wq").T
+    o = np.zeros_like(xr)
+    real = rows < used
+    if np.any(real) and k.shape[0] > 0:
+        o[real] = attention_seq(q[real], k, v, n_heads)
+    h1 = xr + o @ _w(W, "wo").T
     b = rms_norm(h1, g2, rms_eps)
     act = silu(b @ _w(W, "wg").T) * (b @ _w(W, "wu").T)
     y = h1 + act @ _w(W, "wd").T

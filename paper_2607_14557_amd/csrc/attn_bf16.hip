@@ -4,7 +4,9 @@
 // causal mask (the denoising step sees the whole window, Sec. 3.1; logits
 // q.k / sqrt(head_dim) and a softmax over the sequence, Sec. 3.6).  Keys at
 // positions >= seqused[b] are masked and those query rows get a zero output
-// (the static-bucket padding of Sec. 3.5).
+// (the static-bucket padding of Sec. 3.5).  With a prefix cache (KV-cache
+// compatibility, Appendix D) the keys are the cached prefix rows followed by
+// the sequence's own rows.
 //
 // Design: one workgroup = (sequence, 128-query tile, head); four waves of 32
 // queries.  K and V tiles of 64 keys are staged in LDS, double-buffered, and
@@ -68,6 +70,14 @@ __global__ __launch_bounds__(NT, 2) void attn_bf16_kernel(AttnParams p) {
   if (t * QT >= len) return;
   int used = p.used ? p.used[b] : len;
   used = used < 0 ? 0 : (used > len ? len : used);
+  // keys: the cached prefix rows (if any), then the sequence's own used rows
+  int P = 0, kv0 = 0;
+  if (p.cu_kv) {
+    kv0 = p.cu_kv[b];
+    P = p.cu_kv[b + 1] - kv0;
+    P = P < 0 ? 0 : P;
+  }
+  const int nk = P + used;
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -111,9 +121,24 @@ __global__ __launch_bounds__(NT, 2) void attn_bf16_kernel(AttnParams p) {
     k_off[i] = (uint32_t)(id >> 4) * ld + (uint32_t)(p.d + h * DH + (id & 15) * 8);
   }
   u32x4_t kreg[4], vreg[4];
+  // cache rows are 2 d elements; K and V sit d elements apart in both layouts
+  const uint16_t* kvp = p.cu_kv ? static_cast<const uint16_t*>(p.kv) + (size_t)kv0 * 2 * p.d : nullptr;
   auto load_tile = [&](int kbase) {
     const uint16_t* tb = seq + (size_t)kbase * ld;
-    if (kbase + KT <= used) {
+    if (P > 0) {
+      // keys below P come from the cache; keys at or past nk re-read key nk-1 (masked below)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int id = tid + NT * i;
+        int key = kbase + (id >> 4);
+        key = key < nk ? key : nk - 1;
+        const uint16_t* row = key < P
+            ? kvp + (uint32_t)key * (2u * (uint32_t)p.d) + (h * DH + (id & 15) * 8)
+            : seq + (uint32_t)(key - P) * ld + (p.d + h * DH + (id & 15) * 8);
+        kreg[i] = *reinterpret_cast<const u32x4_t*>(row);
+        vreg[i] = *reinterpret_cast<const u32x4_t*>(row + p.d);
+      }
+    } else if (kbase + KT <= used) {
 #pragma unroll
       for (int i = 0; i < 4; ++i) kreg[i] = *reinterpret_cast<const u32x4_t*>(tb + k_off[i]);
 #pragma unroll
@@ -143,7 +168,7 @@ __global__ __launch_bounds__(NT, 2) void attn_bf16_kernel(AttnParams p) {
     }
   };
 
-  const int n_kv = (used + KT - 1) / KT;
+  const int n_kv = (nk + KT - 1) / KT;
   if (n_kv > 0) {
     load_tile(0);
     store_tile(0);
@@ -196,14 +221,14 @@ __global__ __launch_bounds__(NT, 2) void attn_bf16_kernel(AttnParams p) {
       }
       __builtin_amdgcn_sched_barrier(0);
     }
-    // keys at or past `used` only occur in the last tile
-    if (kbase + KT > used) {
+    // keys at or past nk only occur in the last tile
+    if (kbase + KT > nk) {
 #pragma unroll
       for (int i = 0; i < 2; ++i)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           const int key = kbase + i * 32 + (r >> 2) * 8 + fhalf * 4 + (r & 3);
-          if (key >= used) s[i][r] = -INFINITY;
+          if (key >= nk) s[i][r] = -INFINITY;
         }
     }
     float mt = s[0][0];
@@ -313,8 +338,9 @@ __global__ __launch_bounds__(NT, 2) void attn_bf16_kernel(AttnParams p) {
 
 int launch_attn_bf16(const AttnParams& p, hipStream_t s) {
   if (p.head_dim != DH) return -1;
-  // element offsets inside the qkv rows are 32-bit
+  // element offsets inside the qkv rows (and the cache rows of one sequence) are 32-bit
   if ((uint64_t)p.rows_ub * 3u * (uint64_t)p.d >= (1ull << 32)) return -1;
+  if (p.cu_kv && !p.kv) return -1;
   dim3 grid((p.rows_ub + QT - 1) / QT + p.B, p.n_heads), block(NT);
   hipLaunchKernelGGL(attn_bf16_kernel, grid, block, 0, s, p);
   return hipGetLastError() == hipSuccess ? 0 : -1;

@@ -154,17 +154,29 @@ __global__ __launch_bounds__(AQ) void attn_f32_kernel(AttnParams p) {
     q[e] = e < p.head_dim ? qkv[(size_t)(s0 + q_src) * ld + h * p.head_dim + e] * p.scale : 0.0f;
     o[e] = 0.0f;
   }
+  // keys: the cached prefix rows (if any), then the sequence's own used rows
+  int P = 0, kv0 = 0;
+  if (p.cu_kv) {
+    kv0 = p.cu_kv[b];
+    P = p.cu_kv[b + 1] - kv0;
+    P = P < 0 ? 0 : P;
+  }
+  const int n_keys = P + used;
+  const float* kvc = static_cast<const float*>(p.kv);
   float m = -INFINITY, l = 0.0f;
-  for (int k0 = 0; k0 < used; k0 += AK) {
+  for (int k0 = 0; k0 < n_keys; k0 += AK) {
     for (int e = threadIdx.x; e < AK * DH; e += AQ) {
       const int kk = e / DH, c = e % DH;
       const int key = k0 + kk;
-      const bool ok = key < used && c < p.head_dim;
-      ks[kk][c] = ok ? qkv[(size_t)(s0 + key) * ld + p.d + h * p.head_dim + c] : 0.0f;
-      vs[kk][c] = ok ? qkv[(size_t)(s0 + key) * ld + 2 * p.d + h * p.head_dim + c] : 0.0f;
+      const bool ok = key < n_keys && c < p.head_dim;
+      const float* kr = !ok ? nullptr
+          : key < P ? kvc + (size_t)(kv0 + key) * 2 * p.d + h * p.head_dim + c
+                    : qkv + (size_t)(s0 + key - P) * ld + p.d + h * p.head_dim + c;
+      ks[kk][c] = ok ? kr[0] : 0.0f;
+      vs[kk][c] = ok ? kr[p.d] : 0.0f;
     }
     __syncthreads();
-    const int nk = min(AK, used - k0);
+    const int nk = min(AK, n_keys - k0);
     for (int kk = 0; kk < nk; ++kk) {
       float sc = 0.0f;
 #pragma unroll
@@ -187,6 +199,7 @@ __global__ __launch_bounds__(AQ) void attn_f32_kernel(AttnParams p) {
 }
 
 int launch_attn_f32(const AttnParams& p, hipStream_t s) {
+  if (p.cu_kv && !p.kv) return -1;
   dim3 grid((p.rows_ub + AQ - 1) / AQ + p.B, p.n_heads), block(AQ);
   if (p.head_dim <= 64) {
     hipLaunchKernelGGL(attn_f32_kernel<64>, grid, block, 0, s, p);

@@ -64,6 +64,11 @@ struct AttnParams {
   int head_dim;
   int rows_ub;           // bound on cu[B] (sizes the grid)
   float scale;           // 1/sqrt(head_dim)
+  // optional cached prefix keys/values: sequence b's queries also attend to
+  // cache rows [cu_kv[b], cu_kv[b+1]) of kv ([rows, 2d]: K | V, the element
+  // types of the K and V thirds of qkv), ahead of its own keys; null: none
+  const void* kv;
+  const int* cu_kv;
 };
 
 int launch_attn_bf16(const AttnParams& p, hipStream_t s);
@@ -107,8 +112,23 @@ struct RepackParams {
   int* route;
   int* ctrl_dev;    // seer_route_ctrl as int[16]
   int* ctrl_host;
+  bool window_only; // copy only the kept window rows (no prefix rows)
 };
 int launch_repack(const RepackParams& p, hipStream_t s);
+
+// K | V columns of the prefix rows of each sequence, from the qkv rows of a
+// layer call (row stride 3 d elements) into a cache ([rows, 2 d]).
+struct KvExportParams {
+  const uint8_t* qkv;
+  const int* cu;        // [B+1] rows of the layer call
+  const int* cu_kv;     // [B+1] cache rows; sequence b's prefix has cu_kv[b+1] - cu_kv[b] rows
+  uint8_t* dst;
+  int B;
+  int d;
+  int es;               // bytes per element
+  int rows_ub;          // rows of the qkv region
+};
+int launch_kv_export(const KvExportParams& p, int kv_rows_ub, hipStream_t s);
 
 struct PrepackParams {
   const void* wq; const void* wk; const void* wv; const void* wo;

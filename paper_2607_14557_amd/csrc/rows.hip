@@ -162,10 +162,14 @@ __global__ __launch_bounds__(256) void repack_kernel(RepackParams p) {
   __syncthreads();
   for (int b = tid; b < B; b += 256) {
     const int keep = clamp_keep(p, b);
-    int used = p.win_off[b] + keep;
-    const int len = p.cu_src[b + 1] - p.cu_src[b];
-    s_used[b] = used < len ? used : len;   // copies stay inside the source sequence
-    s_src[b] = p.cu_src[b];
+    // rows of sequence b that are copied: its prefix and kept window, or with
+    // window_only the kept window alone
+    const int pre = p.window_only ? 0 : p.win_off[b];
+    const int skip = p.window_only ? p.win_off[b] : 0;
+    int used = pre + keep;
+    const int len = p.cu_src[b + 1] - p.cu_src[b] - skip;
+    s_used[b] = used < len ? (used > 0 ? used : 0) : (len > 0 ? len : 0);   // copies stay inside the source sequence
+    s_src[b] = p.cu_src[b] + skip;
     atomicMax(&s_nmax, p.win_len[b]);
     atomicMax(&s_kmax, keep);
     const int k = coarse_class(keep);
@@ -206,12 +210,12 @@ __global__ __launch_bounds__(256) void repack_kernel(RepackParams p) {
     s_alloc[b] = alloc;
   }
   __syncthreads();
-  // exclusive prefix sum of (win_off + alloc): 4 consecutive entries per thread
+  // exclusive prefix sum of (prefix rows + alloc): 4 consecutive entries per thread
   {
     int local = 0;
     for (int e = 0; e < 4; ++e) {
       const int b = tid * 4 + e;
-      if (b < B) local += p.win_off[b] + s_alloc[b];
+      if (b < B) local += (p.window_only ? 0 : p.win_off[b]) + s_alloc[b];
     }
     s_part[tid] = local;
     __syncthreads();
@@ -230,7 +234,7 @@ __global__ __launch_bounds__(256) void repack_kernel(RepackParams p) {
     int run = s_part[tid];
     for (int e = 0; e < 4; ++e) {
       const int b = tid * 4 + e;
-      if (b < B) { s_cu[b] = run; run += p.win_off[b] + s_alloc[b]; }
+      if (b < B) { s_cu[b] = run; run += (p.window_only ? 0 : p.win_off[b]) + s_alloc[b]; }
     }
     if (tid == 0) s_cu[B] = s_total;
     __syncthreads();
@@ -299,6 +303,35 @@ __global__ __launch_bounds__(256) void repack_kernel(RepackParams p) {
       }
     }
   }
+}
+
+// One workgroup per cache row r: its sequence b (last b with cu_kv[b] <= r),
+// source row cu[b] + (r - cu_kv[b]) of the layer call, K | V columns
+// [d, 3d) moved as 16-byte chunks.  A prefix longer than its sequence, or a
+// source row past the qkv region, leaves the cache row untouched.
+__global__ __launch_bounds__(256) void kv_export_kernel(KvExportParams p) {
+  const int r = blockIdx.x;
+  if (r >= p.cu_kv[p.B]) return;
+  int lo = 0, hi = p.B - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (p.cu_kv[mid] <= r) lo = mid; else hi = mid - 1;
+  }
+  const int j = r - p.cu_kv[lo];
+  const int s0 = p.cu[lo];
+  if (j >= p.cu[lo + 1] - s0) return;
+  const int src = s0 + j;
+  if (src < 0 || src >= p.rows_ub) return;
+  const size_t rb = (size_t)2 * p.d * p.es;
+  const uint4* sp = reinterpret_cast<const uint4*>(p.qkv + (size_t)src * 3 * p.d * p.es + (size_t)p.d * p.es);
+  uint4* dp = reinterpret_cast<uint4*>(p.dst + (size_t)r * rb);
+  for (int c = threadIdx.x; c < (int)(rb >> 4); c += 256) dp[c] = sp[c];
+}
+
+int launch_kv_export(const KvExportParams& p, int kv_rows_ub, hipStream_t s) {
+  if (kv_rows_ub < 1) return 0;
+  hipLaunchKernelGGL(kv_export_kernel, dim3(kv_rows_ub), dim3(256), 0, s, p);
+  return hipGetLastError() == hipSuccess ? 0 : -1;
 }
 
 int launch_repack(const RepackParams& p, hipStream_t s) {

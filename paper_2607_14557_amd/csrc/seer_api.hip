@@ -139,7 +139,8 @@ static int layer_forward_impl(const seer_dims* dims, const void* w_packed, const
                               void* x_out, int32_t total_rows_ub, const int32_t* cu_seqlens,
                               const int32_t* seqused, int32_t batch, float act_eps,
                               int32_t* act_count, void* workspace, size_t workspace_bytes,
-                              hipStream_t stream, hipEvent_t* ev) {
+                              hipStream_t stream, hipEvent_t* ev, const void* kv_cache = nullptr,
+                              const int32_t* cu_kv = nullptr) {
   int rc = check_dims(dims);
   if (rc) return rc;
   if (!w_packed || !x_in || !x_out || !cu_seqlens || !workspace)
@@ -201,6 +202,7 @@ static int layer_forward_impl(const seer_dims* dims, const void* w_packed, const
     a.qkv = qkv; a.out = o; a.cu = cu_seqlens; a.used = seqused; a.B = batch;
     a.d = d; a.n_heads = dims->n_heads; a.head_dim = dims->head_dim; a.rows_ub = R;
     a.scale = 1.0f / sqrtf((float)dims->head_dim);
+    a.kv = kv_cache; a.cu_kv = cu_kv;
     if ((bf16 ? seer::launch_attn_bf16(a, stream) : seer::launch_attn_f32(a, stream)))
       return hip_fail("attention launch");
   }
@@ -272,6 +274,44 @@ int seer_layer_forward_varlen_timed(const seer_dims* dims, const void* w_packed,
                             act_eps, act_count, workspace, workspace_bytes, stream, events);
 }
 
+int seer_layer_forward_cached(const seer_dims* dims, const void* w_packed, const void* x_in,
+                              void* x_out, int32_t total_rows_ub, const int32_t* cu_seqlens,
+                              const int32_t* seqused, int32_t batch, const void* kv_cache,
+                              const int32_t* cu_kv, int32_t kv_rows_ub, void* workspace,
+                              size_t workspace_bytes, hipStream_t stream) {
+  int rc = check_dims(dims);
+  if (rc) return rc;
+  if (!kv_cache || !cu_kv) return fail(SEER_EINVAL, "kv_cache/cu_kv is NULL");
+  if (kv_rows_ub < 0) return fail(SEER_EINVAL, "kv_rows_ub must be >= 0");
+  if (!aligned(kv_cache, 16)) return fail(SEER_EINVAL, "kv_cache must be 16-byte aligned");
+  if ((size_t)kv_rows_ub * 2 * (size_t)dims->d_model >= ((size_t)1 << 32))
+    return fail(SEER_EUNSUPPORTED, "kv_rows_ub %d is too large: cache element offsets must fit 32 bits", kv_rows_ub);
+  return layer_forward_impl(dims, w_packed, x_in, x_out, total_rows_ub, cu_seqlens, seqused, batch, 0.0f,
+                            nullptr, workspace, workspace_bytes, stream, nullptr, kv_cache, cu_kv);
+}
+
+int seer_kv_export(const seer_dims* dims, const void* workspace, size_t workspace_bytes,
+                   int32_t total_rows_ub, const int32_t* cu_seqlens, int32_t batch,
+                   const int32_t* cu_kv, int32_t kv_rows_ub, void* kv_dst, hipStream_t stream) {
+  int rc = check_dims(dims);
+  if (rc) return rc;
+  if (!workspace || !cu_seqlens || !cu_kv || !kv_dst) return fail(SEER_EINVAL, "a required pointer is NULL");
+  if (batch < 1) return fail(SEER_EINVAL, "batch must be >= 1 (got %d)", batch);
+  if (total_rows_ub < 1) return fail(SEER_EINVAL, "total_rows_ub must be >= 1 (got %d)", total_rows_ub);
+  if (kv_rows_ub < 0) return fail(SEER_EINVAL, "kv_rows_ub must be >= 0");
+  if (!aligned(workspace, 256) || !aligned(kv_dst, 16)) return fail(SEER_EINVAL, "misaligned workspace or kv_dst");
+  const WsLayout L = ws_layout(dims, total_rows_ub);
+  if (workspace_bytes < L.total)
+    return fail(SEER_EWORKSPACE, "workspace holds %zu bytes, need %zu", workspace_bytes, L.total);
+  seer::KvExportParams p{};
+  p.qkv = static_cast<const uint8_t*>(workspace) + L.qkv;
+  p.cu = cu_seqlens; p.cu_kv = cu_kv; p.dst = static_cast<uint8_t*>(kv_dst);
+  p.B = batch; p.d = dims->d_model; p.es = dims->dtype == SEER_DTYPE_BF16 ? 2 : 4;
+  p.rows_ub = total_rows_ub;
+  if (seer::launch_kv_export(p, kv_rows_ub, stream)) return hip_fail("kv export launch");
+  return ok();
+}
+
 int seer_step0_detect(const int32_t* act_count, const int32_t* cu_seqlens, const int32_t* win_off,
                       const int32_t* win_len, int32_t batch, int32_t d_ff,
                       const seer_snr_params* params, int32_t* boundary, int32_t* keep_len,
@@ -327,6 +367,7 @@ int seer_batch_repack(const seer_repack_desc* desc, const void* const* src, void
   p.granule = desc->granule; p.row_bytes = desc->row_bytes;
   p.dst_capacity_rows = desc->dst_capacity_rows;
   p.cu_dst = cu_dst; p.seqused = seqused; p.route = route;
+  p.window_only = (desc->flags & SEER_REPACK_WINDOW_ONLY) != 0;
   p.ctrl_dev = reinterpret_cast<int*>(ctrl_dev);
   p.ctrl_host = reinterpret_cast<int*>(ctrl_host);
   if (seer::launch_repack(p, stream)) return hip_fail("repack launch");

@@ -7,7 +7,8 @@ the method's order (Sec. 3.2-3.5): layers 0..l_det on the full window with
 the count at l_det, boundary detection, route + compaction of the in-flight
 residual and of the step-input embeddings in one launch, then the remaining
 layers on the compacted batch.  Later denoising steps run every layer on the
-compacted batch.
+compacted batch, or, with the prefix keys/values cached (Appendix D), on the
+kept window rows alone.
 """
 from dataclasses import dataclass
 from typing import List, Optional
@@ -81,6 +82,61 @@ class SeerStack:
             out[:rows_ub].copy_(cur[:rows_ub])
             cur = out
         return cur
+
+    # ---- truncated steps with the prefix keys/values cached (Appendix D) ----
+    def alloc_kv_caches(self, kv_rows):
+        """One [kv_rows, 2 d] cache per layer (K | V, the qkv element types)."""
+        return [torch.empty(max(int(kv_rows), 1), 2 * self.dims.d_model, dtype=self.dtype,
+                            device=self.device) for _ in range(self.n_layers)]
+
+    def forward_export(self, x, cu, seqused, batch, rows_ub, caches, cu_kv, kv_rows_ub, out=None,
+                       stream=None):
+        """A full truncated step over [prefix; kept window] rows that also
+        caches, per layer, the K | V of each sequence's first cu_kv[b+1] - cu_kv[b]
+        rows."""
+        cur = x
+        for l in range(self.n_layers):
+            nxt = self.buf[l % 2] if cur is not self.buf[l % 2] else self.buf[(l + 1) % 2]
+            self.layer(l, cur, nxt, cu, seqused, batch, rows_ub, stream=stream)
+            S.seer_kv_export(self.dims, self.workspace, rows_ub, cu, batch, cu_kv, kv_rows_ub, caches[l],
+                             workspace_bytes=self.ws_bytes, stream=stream)
+            cur = nxt
+        if out is not None and cur is not out:
+            out[:rows_ub].copy_(cur[:rows_ub])
+            cur = out
+        return cur
+
+    def forward_cached(self, x_w, cu_w, used_w, batch, rows_ub, caches, cu_kv, kv_rows_ub, out=None,
+                       stream=None):
+        """A truncated step on the kept window rows only, every layer reading
+        its cached prefix keys/values."""
+        cur = x_w
+        for l in range(self.n_layers):
+            nxt = self.buf[l % 2] if cur is not self.buf[l % 2] else self.buf[(l + 1) % 2]
+            S.seer_layer_forward_cached(self.dims, self.packed[l], cur, nxt, rows_ub, cu_w, used_w, batch,
+                                        caches[l], cu_kv, kv_rows_ub, self.workspace, self.ws_bytes,
+                                        stream=stream)
+            cur = nxt
+        if out is not None and cur is not out:
+            out[:rows_ub].copy_(cur[:rows_ub])
+            cur = out
+        return cur
+
+    def window_rows(self, src, cu_src, win_off, win_len, keep, batch, capacity, policy=S.SEER_ROUTE_HYBRID,
+                    tau_pad=(1, 5), granule=256, stream=None):
+        """The kept window rows of each sequence of `src`, routed and compacted
+        (no prefix rows): returns (rows, cu, seqused, route)."""
+        dev = self.device
+        dst = torch.empty(capacity, self.dims.d_model, dtype=self.dtype, device=dev)
+        cu = torch.empty(batch + 1, dtype=torch.int32, device=dev)
+        used = torch.empty(batch, dtype=torch.int32, device=dev)
+        route = torch.empty(batch, 3, dtype=torch.int32, device=dev)
+        desc = S.seer_repack_desc(policy, tau_pad[0], tau_pad[1], granule,
+                                  self.dims.d_model * (2 if self.dtype == torch.bfloat16 else 4),
+                                  capacity, 0, S.SEER_REPACK_WINDOW_ONLY)
+        S.seer_batch_repack(desc, [src], [dst], cu_src, win_off, win_len, keep, batch, cu, used, route,
+                            stream=stream)
+        return dst, cu, used, route
 
     def step0(self, x_full, cu_full, win_off, win_len, batch, rows_full, l_det, act_eps,
               snr=(3, 100, 3, 5, 3), policy=S.SEER_ROUTE_HYBRID, tau_pad=(1, 5), granule=256,

@@ -16,11 +16,12 @@ SEER_OK, SEER_EINVAL, SEER_EUNSUPPORTED, SEER_EWORKSPACE, SEER_EHIP = 0, -1, -2,
 SEER_DTYPE_BF16, SEER_DTYPE_F32 = 1, 2
 SEER_ROUTE_HYBRID, SEER_ROUTE_NAIVE_PAD, SEER_ROUTE_VARLEN_ONLY = 0, 1, 2
 SEER_PATH_STATIC, SEER_PATH_VARLEN, SEER_PATH_EAGER = 0, 1, 2
+SEER_REPACK_WINDOW_ONLY = 1
 
 EXPORTED = ("seer_prepacked_bytes", "seer_prepack_weights", "seer_layer_workspace_bytes",
             "seer_layer_workspace_offsets", "seer_layer_forward_varlen",
             "seer_layer_forward_varlen_timed", "seer_step0_detect", "seer_batch_repack",
-            "seer_last_error", "seer_abi_version")
+            "seer_layer_forward_cached", "seer_kv_export", "seer_last_error", "seer_abi_version")
 
 
 class SeerError(RuntimeError):
@@ -49,7 +50,7 @@ class seer_repack_desc(ctypes.Structure):
     _fields_ = [("policy", ctypes.c_int32), ("tau_pad_num", ctypes.c_int32),
                 ("tau_pad_den", ctypes.c_int32), ("granule", ctypes.c_int32),
                 ("row_bytes", ctypes.c_int32), ("dst_capacity_rows", ctypes.c_int32),
-                ("max_batch_hint", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+                ("max_batch_hint", ctypes.c_int32), ("flags", ctypes.c_int32)]
 
 
 class seer_route_ctrl(ctypes.Structure):
@@ -98,6 +99,11 @@ def load_library():
     L.seer_batch_repack.argtypes = [ctypes.POINTER(seer_repack_desc), ctypes.POINTER(_P),
                                     ctypes.POINTER(_P), _I, _P, _P, _P, _P, _I, _P, _P, _P, _P, _P, _P]
     L.seer_batch_repack.restype = ctypes.c_int
+    L.seer_layer_forward_cached.argtypes = [ctypes.POINTER(seer_dims), _P, _P, _P, _I, _P, _P, _I,
+                                            _P, _P, _I, _P, ctypes.c_size_t, _P]
+    L.seer_layer_forward_cached.restype = ctypes.c_int
+    L.seer_kv_export.argtypes = [ctypes.POINTER(seer_dims), _P, ctypes.c_size_t, _I, _P, _I, _P, _I, _P, _P]
+    L.seer_kv_export.restype = ctypes.c_int
     L.seer_last_error.argtypes = []
     L.seer_last_error.restype = ctypes.c_char_p
     L.seer_abi_version.argtypes = []
@@ -180,6 +186,23 @@ def seer_layer_forward_varlen_timed(dims, w_packed, x_in, x_out, total_rows_ub, 
         ctypes.byref(dims), _ptr(w_packed), _ptr(x_in), _ptr(x_out), int(total_rows_ub),
         _ptr(cu_seqlens), _ptr(seqused), int(batch), float(act_eps), _ptr(act_count),
         _ptr(workspace), nbytes, _stream(stream), ev))
+
+
+def seer_layer_forward_cached(dims, w_packed, x_in, x_out, total_rows_ub, cu_seqlens, seqused, batch,
+                              kv_cache, cu_kv, kv_rows_ub, workspace, workspace_bytes=None, stream=None):
+    nbytes = workspace_bytes if workspace_bytes is not None else workspace.numel() * workspace.element_size()
+    _check(load_library().seer_layer_forward_cached(
+        ctypes.byref(dims), _ptr(w_packed), _ptr(x_in), _ptr(x_out), int(total_rows_ub),
+        _ptr(cu_seqlens), _ptr(seqused), int(batch), _ptr(kv_cache), _ptr(cu_kv), int(kv_rows_ub),
+        _ptr(workspace), nbytes, _stream(stream)))
+
+
+def seer_kv_export(dims, workspace, total_rows_ub, cu_seqlens, batch, cu_kv, kv_rows_ub, kv_dst,
+                   workspace_bytes=None, stream=None):
+    nbytes = workspace_bytes if workspace_bytes is not None else workspace.numel() * workspace.element_size()
+    _check(load_library().seer_kv_export(
+        ctypes.byref(dims), _ptr(workspace), nbytes, int(total_rows_ub), _ptr(cu_seqlens), int(batch),
+        _ptr(cu_kv), int(kv_rows_ub), _ptr(kv_dst), _stream(stream)))
 
 
 def seer_step0_detect(act_count, cu_seqlens, win_off, win_len, batch, d_ff, params, boundary,

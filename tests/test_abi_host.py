@@ -120,14 +120,14 @@ def test_repack_argument_errors(S):
                                    FAKE, FAKE, None, None, 0)
 
     ok = dict(policy=0, tau_pad_num=1, tau_pad_den=5, granule=256, row_bytes=8192,
-              dst_capacity_rows=100, max_batch_hint=0, reserved=0)
+              dst_capacity_rows=100, max_batch_hint=0, flags=0)
 
     def desc(**kw):
         a = dict(ok)
         a.update(kw)
         return S.seer_repack_desc(*[a[k] for k in ("policy", "tau_pad_num", "tau_pad_den", "granule",
                                                    "row_bytes", "dst_capacity_rows", "max_batch_hint",
-                                                   "reserved")])
+                                                   "flags")])
 
     assert call(desc(policy=3)) == S.SEER_EINVAL
     assert call(desc(tau_pad_den=0)) == S.SEER_EINVAL
@@ -139,3 +139,39 @@ def test_repack_argument_errors(S):
     assert call(desc(), n=5) == S.SEER_EINVAL
     assert call(desc(), dst=FAKE) == S.SEER_EINVAL              # src aliases dst
     assert call(desc(), src=FAKE + 8) == S.SEER_EINVAL          # misaligned
+
+
+def test_cached_forward_argument_errors(S):
+    L = S.load_library()
+    d = dims(S)
+
+    def call(kv=FAKE, cu_kv=FAKE, kv_rows=1000, ws_bytes=1 << 40, w=FAKE):
+        return L.seer_layer_forward_cached(ctypes.byref(d), w, FAKE, FAKE + 4096, 100, FAKE, None, 1,
+                                           kv, cu_kv, kv_rows, FAKE, ws_bytes, 0)
+
+    assert call(kv=None) == S.SEER_EINVAL
+    assert call(cu_kv=None) == S.SEER_EINVAL
+    assert call(kv_rows=-1) == S.SEER_EINVAL
+    assert call(kv=FAKE + 8) == S.SEER_EINVAL                    # misaligned cache
+    assert call(kv_rows=1 << 20) == S.SEER_EUNSUPPORTED          # 2^20 * 8192 elements >= 2^32
+    assert call(ws_bytes=1024) == S.SEER_EWORKSPACE
+    assert call(w=None) == S.SEER_EINVAL
+
+
+def test_kv_export_argument_errors(S):
+    L = S.load_library()
+    d = dims(S)
+
+    def call(ws=FAKE, ws_bytes=1 << 40, rows=100, cu=FAKE, batch=1, cu_kv=FAKE, kv_rows=10, dst=FAKE):
+        return L.seer_kv_export(ctypes.byref(d), ws, ws_bytes, rows, cu, batch, cu_kv, kv_rows, dst, 0)
+
+    assert call(ws=None) == S.SEER_EINVAL
+    assert call(cu=None) == S.SEER_EINVAL
+    assert call(cu_kv=None) == S.SEER_EINVAL
+    assert call(dst=None) == S.SEER_EINVAL
+    assert call(batch=0) == S.SEER_EINVAL
+    assert call(rows=0) == S.SEER_EINVAL
+    assert call(kv_rows=-1) == S.SEER_EINVAL
+    assert call(dst=FAKE + 4) == S.SEER_EINVAL                    # misaligned destination
+    assert call(ws_bytes=1024) == S.SEER_EWORKSPACE
+    assert call(ws=FAKE + 16) == S.SEER_EINVAL                    # misaligned workspace

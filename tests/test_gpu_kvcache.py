@@ -1,0 +1,158 @@
+"""GPU parity of truncated steps with the prefix keys/values cached
+(KV-cache compatibility, Appendix D), through the C ABI.
+
+Per workload (planted boundaries, keep = b + 1): the full truncated step runs
+over [prefix; kept window] rows and caches every layer's prefix K | V; the
+cached step then runs on the kept window rows alone.
+  * window-only compaction (SEER_REPACK_WINDOW_ONLY): rows, offsets, seqused
+    and routes bit-exact against the oracle router;
+  * K | V export: bit-exact against the K | V columns of the full step's qkv
+    rows (the layer call's own workspace);
+  * the cached step against the full step's window rows: the same inputs, so
+    equal up to rounding (the attention's lazy rescale is decided per wave, and
+    the window rows are grouped into waves differently in the two layouts);
+  * teacher-forced against oracle.layer_forward_cached_rows fed with the GPU's
+    layer input and cache, on sampled sequences, layers and rows.
+"""
+import numpy as np
+import pytest
+
+import oracle
+from gpu_util import dev, host, log, rel_err, upload_weights, view_ws
+from oracle.route import route_batch
+from workloads import WORKLOADS
+from workloads.generate import make_workload
+
+pytestmark = pytest.mark.gpu
+
+TOL = {"bf16": 2e-2, "f32": 1e-4}
+SAME = {"bf16": 1e-2, "f32": 1e-5}   # cached vs full step, both on the GPU
+
+
+@pytest.fixture(scope="module")
+def S():
+    from paper_2607_14557_amd import seer
+    seer.load_library()
+    return seer
+
+
+def _kv_host(cache, d, dtype):
+    """[rows, 2d] cache -> (K, V) float64; bf16 layers keep V in fp16."""
+    import torch
+    if dtype == "bf16":
+        k = cache[:, :d].float()
+        v = cache[:, d:].contiguous().view(torch.float16).float()
+        return k.cpu().numpy().astype(np.float64), v.cpu().numpy().astype(np.float64)
+    return host(cache[:, :d]), host(cache[:, d:])
+
+
+def _bits(t):
+    import torch
+    return t.contiguous().view(torch.int16 if t.element_size() == 2 else torch.int32)
+
+
+@pytest.mark.parametrize("name", ["tiny_f32", "small_bf16_ragged", "small_bf16_stack", "llada_b16_ragged"])
+def test_cached_truncated_step(S, name):
+    import torch
+    from paper_2607_14557_amd.runner import SeerStack, dims_for
+    w = WORKLOADS[name]
+    sh = w.shape
+    d, H, B, L = sh.d_model, sh.n_heads, w.batch, w.n_layers
+    log("kv cache %s: inputs" % name)
+    layers, batch = make_workload(w)
+    keep = np.minimum(batch.planted + 1, batch.win_len).astype(np.int64)
+    P = np.asarray(batch.win_off, np.int64)
+    T = w.rows_full
+    granule = 256
+    cap = ((T + granule - 1) // granule) * granule + granule
+    st = SeerStack(dims_for(d, H, sh.head_dim, sh.d_ff, w.dtype, w.rms_eps), L, cap)
+    for l in range(L):
+        st.set_layer(l, upload_weights(layers[l], w.dtype))
+    x = dev(batch.x, w.dtype)
+    cu, off, wl, kp = dev(batch.cu_seqlens), dev(batch.win_off), dev(batch.win_len), dev(keep)
+    row_bytes = d * (2 if w.dtype == "bf16" else 4)
+
+    # full truncated layout [prefix; kept window] and the window-only layout
+    x_t = torch.empty(cap, d, dtype=st.dtype, device="cuda")
+    cu_t = torch.empty(B + 1, dtype=torch.int32, device="cuda")
+    used_t = torch.empty(B, dtype=torch.int32, device="cuda")
+    route_t = torch.empty(B, 3, dtype=torch.int32, device="cuda")
+    desc = S.seer_repack_desc(S.SEER_ROUTE_HYBRID, 1, 5, granule, row_bytes, cap, 0, 0)
+    S.seer_batch_repack(desc, [x], [x_t], cu, off, wl, kp, B, cu_t, used_t, route_t)
+    x_w, cu_w, used_w, route_w = st.window_rows(x, cu, off, wl, kp, B, cap, granule=granule)
+    torch.cuda.synchronize()
+
+    # -- window-only compaction against the oracle router
+    rt = route_batch(keep, batch.win_len)
+    cu_w_h, used_w_h = host(cu_w), host(used_w)
+    np.testing.assert_array_equal(cu_w_h, np.concatenate([[0], np.cumsum(rt.alloc)]))
+    np.testing.assert_array_equal(used_w_h, keep)
+    np.testing.assert_array_equal(host(route_w), np.stack([rt.path, rt.group, rt.alloc], 1))
+    xw_h = host(x_w)
+    for b in range(B):
+        s0 = int(batch.cu_seqlens[b]) + int(P[b])
+        np.testing.assert_array_equal(xw_h[cu_w_h[b]:cu_w_h[b] + keep[b]], host(x[s0:s0 + keep[b]]))
+        assert not np.any(xw_h[cu_w_h[b] + keep[b]:cu_w_h[b + 1]])
+    tot_w = int(cu_w_h[-1])
+    assert not np.any(xw_h[tot_w:((tot_w + granule - 1) // granule) * granule])
+
+    # -- full truncated step, caching each layer's prefix K | V
+    cu_kv_h = np.concatenate([[0], np.cumsum(P)]).astype(np.int64)
+    kv_rows = int(cu_kv_h[-1])
+    cu_kv = dev(cu_kv_h)
+    caches = st.alloc_kv_caches(kv_rows)
+    cu_t_h = host(cu_t)
+    off_ws = S.seer_layer_workspace_offsets(st.dims, cap)
+    log("kv cache %s: full step (%d rows) + export" % (name, int(cu_t_h[-1])))
+    cur = x_t
+    for l in range(L):
+        nxt = torch.empty_like(x_t)
+        st.layer(l, cur, nxt, cu_t, used_t, B, cap)
+        S.seer_kv_export(st.dims, st.workspace, cap, cu_t, B, cu_kv, kv_rows, caches[l])
+        torch.cuda.synchronize()
+        qkv = view_ws(st.workspace, off_ws[0], cap, 3 * d, w.dtype)
+        for b in range(B):
+            src = qkv[cu_t_h[b]:cu_t_h[b] + P[b], d:]
+            assert torch.equal(_bits(caches[l][cu_kv_h[b]:cu_kv_h[b + 1]]), _bits(src)), (l, b)
+        cur = nxt
+    y_full = cur
+
+    # -- cached step on the window rows, keeping every layer's input
+    log("kv cache %s: cached step (%d rows)" % (name, tot_w))
+    ins = []
+    cur = x_w
+    for l in range(L):
+        ins.append(cur)
+        nxt = torch.empty_like(x_w)
+        S.seer_layer_forward_cached(st.dims, st.packed[l], cur, nxt, cap, cu_w, used_w, B, caches[l], cu_kv,
+                                    kv_rows, st.workspace)
+        cur = nxt
+    ins.append(cur)
+    torch.cuda.synchronize()
+
+    # -- against the full step's window rows
+    yf, yc = host(y_full), host(cur)
+    worst = 0.0
+    for b in range(B):
+        a = yf[cu_t_h[b] + P[b]:cu_t_h[b] + P[b] + keep[b]]
+        c = yc[cu_w_h[b]:cu_w_h[b] + keep[b]]
+        worst = max(worst, rel_err(c, a))
+    log("  cached vs full step, window rows: max rel diff %.3e" % worst)
+    assert worst <= SAME[w.dtype]
+
+    # -- teacher-forced against the oracle on sampled sequences / layers / rows
+    rng = np.random.default_rng(17)
+    seqs = sorted({0, B - 1})
+    for l in sorted({0, L - 1}):
+        W = {k: np.asarray(v, np.float64) for k, v in layers[l].items()}
+        kc, vc = _kv_host(caches[l], d, w.dtype)
+        for b in seqs:
+            r0, n = int(cu_w_h[b]), int(cu_w_h[b + 1] - cu_w_h[b])
+            rows = np.array(sorted({0, int(keep[b]) - 1, n - 1} | set(int(i) for i in rng.integers(0, n, 3))))
+            ref = oracle.layer_forward_cached_rows(host(ins[l][r0:r0 + n]), int(keep[b]),
+                                                   kc[cu_kv_h[b]:cu_kv_h[b + 1]], vc[cu_kv_h[b]:cu_kv_h[b + 1]],
+                                                   W, H, w.rms_eps, rows=rows)["y"]
+            e = rel_err(host(ins[l + 1][r0:r0 + n])[rows], ref)
+            log("  layer %d seq %d: rel err %.3e over %d rows" % (l, b, e, len(rows)))
+            assert e <= TOL[w.dtype]
+        del W

@@ -104,3 +104,14 @@ def test_packed_two_layer_stack():
         xw = layer_forward_cached(xw, cu, caches[l], W, H, EPS, seqused=used)
     for b in range(3):
         np.testing.assert_allclose(xw[cu[b]:cu[b] + used[b]], cur[b][P[b]:P[b] + used[b]], rtol=0, atol=1e-11)
+
+
+def test_selected_rows_match_all_rows():
+    rng = np.random.default_rng(8)
+    W = rand_layer(rng, 16, 20)
+    x = rng.standard_normal((10, 16))
+    k_pre, v_pre = prefix_kv(rng.standard_normal((4, 16)), W, EPS, 4)
+    full = layer_forward_cached_rows(x, 7, k_pre, v_pre, W, 2, EPS)["y"]
+    rows = np.array([0, 3, 6, 7, 9])
+    part = layer_forward_cached_rows(x, 7, k_pre, v_pre, W, 2, EPS, rows=rows)["y"]
+    np.testing.assert_allclose(part, full[rows], rtol=0, atol=1e-13)
