@@ -162,10 +162,31 @@ def bench_stack(args, w):
     hip = Hip()
     n_trunc = w.trunc_steps
 
+    kv = None
+    if args.kv_cache:
+        # prefix keys/values of every layer, cached by the first truncated step
+        P = np.asarray(batch.win_off, np.int64)
+        kv_rows = int(P.sum())
+        cu_kv = i32(np.concatenate([[0], np.cumsum(P)]))
+        caches = st.alloc_kv_caches(kv_rows)
+        kv = (caches, cu_kv, kv_rows)
+        log("  prefix K/V caches: %d rows x %d layers (%.1f GB)" % (kv_rows, L, kv_rows * 2 * d * 2 * L / 1e9))
+
     def job():
         r = st.step0(x, cu, off, wl, B, T, w.l_det, w.act_eps, granule=granule, trunc_capacity=cap, stream=sp)
-        for _ in range(n_trunc):
-            st.forward(r.x_trunc, r.cu_trunc, r.seqused, B, cap, stream=sp)
+        if kv is None:
+            for _ in range(n_trunc):
+                st.forward(r.x_trunc, r.cu_trunc, r.seqused, B, cap, stream=sp)
+            return r
+        caches, cu_kv, kv_rows = kv
+        # the kept window rows alone, and their routed capacity (one host read per job)
+        x_w, cu_w, used_w, _ = st.window_rows(x, cu, off, wl, r.keep_len, B, cap, granule=granule, stream=sp)
+        rows_w = int(cu_w[B].item())
+        rows_w = ((rows_w + granule - 1) // granule) * granule
+        st.forward_export(r.x_trunc, r.cu_trunc, r.seqused, B, cap, caches, cu_kv, kv_rows, stream=sp)
+        for _ in range(n_trunc - 1):
+            st.forward_cached(x_w, cu_w, used_w, B, max(rows_w, 1), caches, cu_kv, kv_rows, stream=sp)
+        r.cached = (x_w, cu_w, used_w, rows_w)
         return r
 
     log("warmup %d job(s)" % args.warmup)
@@ -197,6 +218,11 @@ def bench_stack(args, w):
     log("timing one truncated and one untruncated %d-layer step" % L)
     t_trunc = timed(lambda: st.forward(r.x_trunc, r.cu_trunc, r.seqused, B, cap, stream=sp))
     t_full = timed(lambda: st.forward(x, cu, None, B, T, stream=sp), reps=1)
+    t_cached = None
+    if kv is not None:
+        x_w, cu_w, used_w, rows_w = r.cached
+        t_cached = timed(lambda: st.forward_cached(x_w, cu_w, used_w, B, max(rows_w, 1), kv[0], kv[1], kv[2],
+                                                   stream=sp))
     # the dominant kernel: gate/up GEMM of a truncated step, timed inside one layer
     ev = [hip.event() for _ in range(8)]
     y = torch.empty(cap, d, dtype=torch.bfloat16, device=dev)
@@ -210,8 +236,8 @@ def bench_stack(args, w):
     n_den = 1 + n_trunc
     value = int(keep.sum()) * n_den / (ms_job * 1e-3)
     out = {
-        "metric": "effective gen tokens/sec over step 0 + %d truncated denoising steps (%d-layer stack)"
-                  % (n_trunc, L),
+        "metric": "effective gen tokens/sec over step 0 + %d truncated denoising steps (%d-layer stack%s)"
+                  % (n_trunc, L, ", prefix K/V cached after the first truncated step" if kv else ""),
         "value": round(value, 1), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(ms_job, 3), "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
@@ -228,6 +254,8 @@ def bench_stack(args, w):
         "trunc_step_ms": round(t_trunc, 3), "full_step_ms": round(t_full, 3),
         "speedup_trunc_vs_full": round(t_full / t_trunc, 3),
         "job_speedup_vs_untruncated": round(n_den * t_full / ms_job, 3),
+        "cached_step_ms": None if t_cached is None else round(t_cached, 3),
+        "speedup_cached_vs_trunc": None if t_cached is None else round(t_trunc / t_cached, 3),
         "cpu_baseline": None,
         "cpu_baseline_note": "one oracle step of a 32-layer stack takes hours; the default workload's line "
                              "carries the CPU baseline",
@@ -249,8 +277,12 @@ def main():
                     help="after timing, run a 1 GiB fill and a 1 GiB read+write streaming kernel "
                          "(the known-size dispatches that scale the HBM byte counters)")
     ap.add_argument("--no-untruncated", action="store_true",
-                    help="skip the separate untruncated-step timing (it launches the gate/up GEMM "
-                         "kernel at the full-window size, which a per-kernel profile would mix in)")
+                    help="skip the separate untruncated-step and cached-prefix-step timings (they "
+                         "launch the gate/up GEMM kernel at other sizes, which a per-kernel profile "
+                         "would mix in)")
+    ap.add_argument("--kv-cache", action="store_true",
+                    help="32-layer stacks: after step 0, one full truncated step caches every layer's "
+                         "prefix keys/values and the remaining steps run on the kept window rows")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -385,10 +417,46 @@ def main():
         torch.cuda.synchronize()
         return hip.ms(e0, e1) / reps
 
-    # untruncated denoising step (same layer over the full window, no count) for the speedup
-    t_full = None
+    def time_cached():
+        """A truncated step on the kept window rows alone, the prefix keys and
+        values cached from a full truncated step (Appendix D, KV caching)."""
+        log("timing the cached-prefix truncated step")
+        x_w = torch.zeros(cap, d, dtype=torch.bfloat16, device=dev)
+        y_w = torch.zeros(cap, d, dtype=torch.bfloat16, device=dev)
+        cu_w = torch.empty(w.batch + 1, dtype=torch.int32, device=dev)
+        used_w = torch.empty(w.batch, dtype=torch.int32, device=dev)
+        route_w = torch.empty(w.batch, 3, dtype=torch.int32, device=dev)
+        ctrl_w = torch.zeros(16, dtype=torch.int32, device=dev)
+        desc_w = S.seer_repack_desc(policy, 1, 5, granule, d * 2, cap, 0, S.SEER_REPACK_WINDOW_ONLY)
+        S.seer_batch_repack(desc_w, [x_full], [x_w], cu_full, win_off, win_len, keep, w.batch, cu_w,
+                            used_w, route_w, ctrl_w, None, stream=sp)
+        P = np.asarray(batch.win_off, np.int64)
+        kv_rows = int(P.sum())
+        cu_kv = i32(np.concatenate([[0], np.cumsum(P)]))
+        kv = torch.empty(kv_rows, 2 * d, dtype=torch.bfloat16, device=dev)
+        S.seer_layer_forward_varlen(dims, packed, x_t, y_t, cap, cu_t, used, w.batch, 0.0, None, ws, stream=sp)
+        S.seer_kv_export(dims, ws, cap, cu_t, w.batch, cu_kv, kv_rows, kv, stream=sp)
+        torch.cuda.synchronize()
+        rows_w = int(ctrl_w[1].item())          # routed capacity of the window rows
+        for _ in range(3):
+            S.seer_layer_forward_cached(dims, packed, x_w, y_w, rows_w, cu_w, used_w, w.batch, kv, cu_kv,
+                                        kv_rows, ws, stream=sp)
+        e0, e1 = hip.event(), hip.event()
+        reps = max(10, args.steps)
+        hip.record(e0, sp)
+        for _ in range(reps):
+            S.seer_layer_forward_cached(dims, packed, x_w, y_w, rows_w, cu_w, used_w, w.batch, kv, cu_kv,
+                                        kv_rows, ws, stream=sp)
+        hip.record(e1, sp)
+        torch.cuda.synchronize()
+        return hip.ms(e0, e1) / reps, int(ctrl_w[0].item())
+
+    # untruncated denoising step (same layer over the full window, no count) for the speedup,
+    # and the cached-prefix variant of the truncated step
+    t_full = t_cached = rows_cached = None
     if not args.no_untruncated:
         t_full = time_untruncated()
+        t_cached, rows_cached = time_cached()
 
     gemm_flop_row = {"qkv": 2 * 3 * d * d, "o": 2 * d * d, "gateup": 2 * 2 * I * d, "down": 2 * I * d}
     seqlens_full = np.diff(batch.cu_seqlens).astype(np.int64)
@@ -439,6 +507,11 @@ def main():
         "speedup_trunc_vs_full": None if t_full is None else round(t_full / t_trunc, 3),
         "trunc_step_tokens_per_s": round(sum_keep / (t_trunc * 1e-3), 1),
         "full_step_tokens_per_s": None if t_full is None else round(sum_keep / (t_full * 1e-3), 1),
+        "cached_step_ms": None if t_cached is None else round(t_cached, 4),
+        "cached_step_tokens_per_s": None if t_cached is None else round(sum_keep / (t_cached * 1e-3), 1),
+        "speedup_cached_vs_trunc": None if t_cached is None else round(t_trunc / t_cached, 3),
+        "speedup_cached_vs_full": None if t_cached is None or t_full is None else round(t_full / t_cached, 3),
+        "rows_cached_executed": rows_cached,
         "step0_layer_ms": round(t_full_layer, 4),
         "detect_repack_ms": round(t_mid, 4),
         "trunc_gemm_mfma_util": round(tflops(gemm_flop_t, gemm_ms_t) / PEAK_BF16_TFLOPS, 4),
