@@ -156,3 +156,51 @@ def test_cached_truncated_step(S, name):
             log("  layer %d seq %d: rel err %.3e over %d rows" % (l, b, e, len(rows)))
             assert e <= TOL[w.dtype]
         del W
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_cached_step_degenerate_shapes(S, dtype):
+    """An empty prefix, a one-row kept window, a prefix that straddles key
+    tiles, and a sequence with no window rows at all (its prefix cached, no
+    queries): the cached layer against the oracle, teacher-forced, and
+    against the full layer's window rows."""
+    import torch
+    from paper_2607_14557_amd.runner import SeerStack, dims_for
+    from test_oracle_layer import rand_layer
+    rng = np.random.default_rng(23)
+    d, H, dh, I = (512, 4, 128, 1024) if dtype == "bf16" else (256, 4, 64, 688)
+    W = rand_layer(rng, d, I, std=0.02)
+    W["g1"] = np.ones(d)
+    W["g2"] = np.ones(d)
+    P = np.array([0, 5, 130, 64, 10])
+    keep = np.array([1, 7, 70, 3, 0])
+    B = len(P)
+    seqs = [rng.standard_normal((P[b] + keep[b], d)) for b in range(B)]
+    x_t = np.concatenate(seqs)
+    cu_t = np.concatenate([[0], np.cumsum(P + keep)])
+    x_w = np.concatenate([s[P[b]:] for b, s in enumerate(seqs)])
+    cu_w = np.concatenate([[0], np.cumsum(keep)])
+    cu_kv = np.concatenate([[0], np.cumsum(P)])
+    rows = int(cu_t[-1])
+    st = SeerStack(dims_for(d, H, dh, I, dtype), 1, rows)
+    st.set_layer(0, upload_weights(W, dtype))
+    xt_d, xw_d = dev(x_t, dtype), dev(x_w, dtype)
+    yt = torch.zeros_like(xt_d)
+    yw = torch.zeros_like(xw_d)
+    caches = st.alloc_kv_caches(int(cu_kv[-1]))
+    st.layer(0, xt_d, yt, dev(cu_t), None, B, rows)
+    S.seer_kv_export(st.dims, st.workspace, rows, dev(cu_t), B, dev(cu_kv), int(cu_kv[-1]), caches[0])
+    S.seer_layer_forward_cached(st.dims, st.packed[0], xw_d, yw, int(cu_w[-1]), dev(cu_w), None, B, caches[0],
+                                dev(cu_kv), int(cu_kv[-1]), st.workspace)
+    torch.cuda.synchronize()
+    kc, vc = _kv_host(caches[0], d, dtype)
+    ytf, ywf = host(yt), host(yw)
+    for b in range(B):
+        got = ywf[cu_w[b]:cu_w[b + 1]]
+        e_same = rel_err(got, ytf[cu_t[b] + P[b]:cu_t[b + 1]])
+        ref = oracle.layer_forward_cached_rows(host(xw_d[cu_w[b]:cu_w[b + 1]]), int(keep[b]),
+                                               kc[cu_kv[b]:cu_kv[b + 1]], vc[cu_kv[b]:cu_kv[b + 1]],
+                                               W, H, 1e-5)["y"]
+        e = rel_err(got, ref)
+        log("  %s seq %d (prefix %d, keep %d): vs full %.2e, vs oracle %.2e" % (dtype, b, P[b], keep[b], e_same, e))
+        assert e_same <= SAME[dtype] and e <= TOL[dtype]
