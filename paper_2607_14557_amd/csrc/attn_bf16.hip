@@ -45,8 +45,12 @@ typedef __attribute__((address_space(3))) v4i16_t lds_v4i16_t;
 
 __global__ __launch_bounds__(NT, 2) void attn_bf16_kernel(AttnParams p) {
   // two K/V buffers: tile t+1 is written into one while tile t is read from the other
-  __shared__ __attribute__((aligned(16))) uint8_t k_lds[2][KT * K_ROW];
-  __shared__ __attribute__((aligned(16))) uint8_t v_lds[2][KT * K_ROW];
+  // two K/V buffers, each its own array so that the compiler sees reads of one
+  // as independent of the direct-to-LDS loads filling the other
+  __shared__ __attribute__((aligned(1024))) uint8_t k_lds0[KT * K_ROW];
+  __shared__ __attribute__((aligned(1024))) uint8_t k_lds1[KT * K_ROW];
+  __shared__ __attribute__((aligned(1024))) uint8_t v_lds0[KT * K_ROW];
+  __shared__ __attribute__((aligned(1024))) uint8_t v_lds1[KT * K_ROW];
 
   // ---- which (sequence, query tile) this block owns -------------------------
   int b = -1, t = 0;
@@ -110,69 +114,49 @@ __global__ __launch_bounds__(NT, 2) void attn_bf16_kernel(AttnParams p) {
   const float c = p.scale * 1.4426950408889634f;
 
   // ---- K/V tile staging -------------------------------------------------------
-  // Thread moves 16-byte chunks id = tid + 256 i of K and of V (fp16): key
-  // id/16, dim chunk id%16.  Both stay row-major in LDS; K's chunks are XOR-
-  // swizzled by key%16, V's by 4 (key%4) -- V fragments are read with the LDS
-  // transpose read, whose 8-byte accesses then hit distinct banks.
-  uint32_t k_off[4];
+  // Direct-to-LDS buffer loads: one load moves 64 x 16 bytes into 1 KiB of
+  // consecutive LDS, i.e. 4 key rows of 256 bytes.  Load q of wave w fills tile
+  // rows 16 w + 4 q + lane/16 at LDS position lane%16, so the lane fetches the
+  // 16-byte dim chunk that the swizzle puts there: (lane%16) ^ (row%16) for K,
+  // (lane%16) ^ 4 (row%4) for V (V fragments are read with the LDS transpose
+  // read, whose 8-byte accesses then hit distinct banks).  Keys below P come
+  // from the prefix cache, keys at or past nk re-read key nk-1 (masked below).
+  // Offsets are bytes from the sequence's first qkv row and the sequence's
+  // first cache row (< 4 GiB, checked by the host).
+  const int wv = __builtin_amdgcn_readfirstlane(wave);
+  const __amdgpu_buffer_rsrc_t rs_q = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(seq), 0, -1, 0x00020000);
+  const __amdgpu_buffer_rsrc_t rs_c = __builtin_amdgcn_make_buffer_rsrc(
+      p.cu_kv ? const_cast<uint16_t*>(static_cast<const uint16_t*>(p.kv) + (size_t)kv0 * 2 * p.d)
+              : const_cast<uint16_t*>(seq), 0, -1, 0x00020000);
+  const uint32_t q_row_bytes = 3u * (uint32_t)p.d * 2u, c_row_bytes = 4u * (uint32_t)p.d;
+  const uint32_t k_col = (uint32_t)(p.d + h * DH) * 2u, c_col = (uint32_t)(h * DH) * 2u, v_step = (uint32_t)p.d * 2u;
+  auto dma_tile = [&](int kbase, auto buf_tag) {
+    constexpr int B_ = decltype(buf_tag)::value;
+    uint8_t* kb = B_ ? k_lds1 : k_lds0;
+    uint8_t* vb = B_ ? v_lds1 : v_lds0;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int id = tid + NT * i;
-    k_off[i] = (uint32_t)(id >> 4) * ld + (uint32_t)(p.d + h * DH + (id & 15) * 8);
-  }
-  u32x4_t kreg[4], vreg[4];
-  // cache rows are 2 d elements; K and V sit d elements apart in both layouts
-  const uint16_t* kvp = p.cu_kv ? static_cast<const uint16_t*>(p.kv) + (size_t)kv0 * 2 * p.d : nullptr;
-  auto load_tile = [&](int kbase) {
-    const uint16_t* tb = seq + (size_t)kbase * ld;
-    if (P > 0) {
-      // keys below P come from the cache; keys at or past nk re-read key nk-1 (masked below)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int id = tid + NT * i;
-        int key = kbase + (id >> 4);
-        key = key < nk ? key : nk - 1;
-        const uint16_t* row = key < P
-            ? kvp + (uint32_t)key * (2u * (uint32_t)p.d) + (h * DH + (id & 15) * 8)
-            : seq + (uint32_t)(key - P) * ld + (p.d + h * DH + (id & 15) * 8);
-        kreg[i] = *reinterpret_cast<const u32x4_t*>(row);
-        vreg[i] = *reinterpret_cast<const u32x4_t*>(row + p.d);
+    for (int q = 0; q < 4; ++q) {
+      const int r = 16 * wv + 4 * q + (lane >> 4);
+      int key = kbase + r;
+      key = key < nk ? key : nk - 1;
+      const uint32_t ck = (uint32_t)(((lane & 15) ^ (r & 15)) << 4);
+      const uint32_t cv = (uint32_t)(((lane & 15) ^ (4 * (r & 3))) << 4);
+      lds_void_t* kd = (lds_void_t*)(kb + (16 * wv + 4 * q) * K_ROW);
+      lds_void_t* vd = (lds_void_t*)(vb + (16 * wv + 4 * q) * K_ROW);
+      if (key < P) {
+        const uint32_t ro = (uint32_t)key * c_row_bytes + c_col;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rs_c, kd, 16, ro + ck, 0, 0, 0);
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rs_c, vd, 16, ro + v_step + cv, 0, 0, 0);
+      } else {
+        const uint32_t ro = (uint32_t)(key - P) * q_row_bytes + k_col;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rs_q, kd, 16, ro + ck, 0, 0, 0);
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rs_q, vd, 16, ro + v_step + cv, 0, 0, 0);
       }
-    } else if (kbase + KT <= used) {
-#pragma unroll
-      for (int i = 0; i < 4; ++i) kreg[i] = *reinterpret_cast<const u32x4_t*>(tb + k_off[i]);
-#pragma unroll
-      for (int i = 0; i < 4; ++i) vreg[i] = *reinterpret_cast<const u32x4_t*>(tb + k_off[i] + p.d);
-    } else {
-      // last tile: keys at or past `used` re-read key used-1 (masked below)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int id = tid + NT * i;
-        int key = kbase + (id >> 4);
-        key = key < used ? key : used - 1;
-        const uint16_t* row = seq + (uint32_t)key * ld + (p.d + h * DH + (id & 15) * 8);
-        kreg[i] = *reinterpret_cast<const u32x4_t*>(row);
-        vreg[i] = *reinterpret_cast<const u32x4_t*>(row + p.d);
-      }
-    }
-  };
-  auto store_tile = [&](int buf) {
-    uint8_t* kl = k_lds[buf];
-    uint8_t* vl = v_lds[buf];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int id = tid + NT * i;
-      const int key = id >> 4;
-      *reinterpret_cast<u32x4_t*>(kl + key * K_ROW + (((id & 15) ^ (key & 15)) << 4)) = kreg[i];
-      *reinterpret_cast<u32x4_t*>(vl + key * K_ROW + (((id & 15) ^ (4 * (key & 3))) << 4)) = vreg[i];
     }
   };
 
   const int n_kv = (nk + KT - 1) / KT;
-  if (n_kv > 0) {
-    load_tile(0);
-    store_tile(0);
-  }
+  if (n_kv > 0) dma_tile(0, std::integral_constant<int, 0>{});
   // Drain every global load issued so far (Q and tile 0) before the loop.  The
   // wait-count insertion merges the loop entry with the back edge; with Q
   // possibly in flight at entry it would make the first score MFMAs of every
@@ -187,9 +171,9 @@ __global__ __launch_bounds__(NT, 2) void attn_bf16_kernel(AttnParams p) {
   auto tile_step = [&](int kt, auto buf_tag) {
     constexpr int BUF = decltype(buf_tag)::value;
     const int kbase = kt * KT;
-    const uint8_t* kl = k_lds[BUF];
-    const uint8_t* vl = v_lds[BUF];
-    if (kt + 1 < n_kv) load_tile(kbase + KT);
+    const uint8_t* kl = BUF ? k_lds1 : k_lds0;
+    const uint8_t* vl = BUF ? v_lds1 : v_lds0;
+    if (kt + 1 < n_kv) dma_tile(kbase + KT, std::integral_constant<int, BUF ^ 1>{});
 
     // S^T for 64 keys: two 32-key MFMA row tiles, walked over the 8 dim
     // slices with the next slice's two K fragments read one step ahead.
@@ -309,8 +293,9 @@ __global__ __launch_bounds__(NT, 2) void attn_bf16_kernel(AttnParams p) {
       __builtin_amdgcn_sched_barrier(0);
     }
     // Buffer BUF^1 was last read in tile kt-1, which every wave left through
-    // the barrier below; one barrier then publishes tile kt+1.
-    if (kt + 1 < n_kv) store_tile(BUF ^ 1);
+    // the barrier below; this wave's loads of tile kt+1 have landed once
+    // vmcnt is zero, and one barrier then publishes the whole tile.
+    __builtin_amdgcn_s_waitcnt(0x0f70);
     __syncthreads();
   };
   for (int kt = 0; kt < n_kv; kt += 2) {
@@ -338,8 +323,8 @@ __global__ __launch_bounds__(NT, 2) void attn_bf16_kernel(AttnParams p) {
 
 int launch_attn_bf16(const AttnParams& p, hipStream_t s) {
   if (p.head_dim != DH) return -1;
-  // element offsets inside the qkv rows (and the cache rows of one sequence) are 32-bit
-  if ((uint64_t)p.rows_ub * 3u * (uint64_t)p.d >= (1ull << 32)) return -1;
+  // byte offsets inside the qkv rows and the cache rows are 32-bit
+  if ((uint64_t)p.rows_ub * 3u * (uint64_t)p.d * 2u >= (1ull << 32)) return -1;
   if (p.cu_kv && !p.kv) return -1;
   dim3 grid((p.rows_ub + QT - 1) / QT + p.B, p.n_heads), block(NT);
   hipLaunchKernelGGL(attn_bf16_kernel, grid, block, 0, s, p);
