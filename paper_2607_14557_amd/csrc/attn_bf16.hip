@@ -81,7 +81,11 @@ __global__ __launch_bounds__(NT, 2) void attn_bf16_kernel(AttnParams p) {
     P = p.cu_kv[b + 1] - kv0;
     P = P < 0 ? 0 : P;
   }
-  const int nk = P + used;
+  // Key positions: cache rows at [0, P), own rows at [P4, P4 + used) with P4 =
+  // P rounded up to a multiple of 4, so that the 4 rows of one staging load
+  // come from one source; the (at most 3) positions [P, P4) are masked.
+  const int P4 = (P + 3) & ~3;
+  const int nk = used > 0 ? P4 + used : P;
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -119,8 +123,10 @@ __global__ __launch_bounds__(NT, 2) void attn_bf16_kernel(AttnParams p) {
   // rows 16 w + 4 q + lane/16 at LDS position lane%16, so the lane fetches the
   // 16-byte dim chunk that the swizzle puts there: (lane%16) ^ (row%16) for K,
   // (lane%16) ^ 4 (row%4) for V (V fragments are read with the LDS transpose
-  // read, whose 8-byte accesses then hit distinct banks).  Keys below P come
-  // from the prefix cache, keys at or past nk re-read key nk-1 (masked below).
+  // read, whose 8-byte accesses then hit distinct banks).  The 4 positions of
+  // one load are all cache rows (below P4) or all own rows, so the descriptor
+  // and row stride are chosen per wave; gap positions re-read cache row P-1,
+  // positions at or past nk re-read the last key (all masked below).
   // Offsets are bytes from the sequence's first qkv row and the sequence's
   // first cache row (< 4 GiB, checked by the host).
   const int wv = __builtin_amdgcn_readfirstlane(wave);
@@ -143,15 +149,12 @@ __global__ __launch_bounds__(NT, 2) void attn_bf16_kernel(AttnParams p) {
       const uint32_t cv = (uint32_t)(((lane & 15) ^ (4 * (r & 3))) << 4);
       lds_void_t* kd = (lds_void_t*)(kb + (16 * wv + 4 * q) * K_ROW);
       lds_void_t* vd = (lds_void_t*)(vb + (16 * wv + 4 * q) * K_ROW);
-      if (key < P) {
-        const uint32_t ro = (uint32_t)key * c_row_bytes + c_col;
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(rs_c, kd, 16, ro + ck, 0, 0, 0);
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(rs_c, vd, 16, ro + v_step + cv, 0, 0, 0);
-      } else {
-        const uint32_t ro = (uint32_t)(key - P) * q_row_bytes + k_col;
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(rs_q, kd, 16, ro + ck, 0, 0, 0);
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(rs_q, vd, 16, ro + v_step + cv, 0, 0, 0);
-      }
+      const bool cache = kbase + 16 * wv + 4 * q < P4 || used == 0;
+      const int row = cache ? (key < P ? key : P - 1) : key - P4;
+      const uint32_t ro = (uint32_t)row * (cache ? c_row_bytes : q_row_bytes) + (cache ? c_col : k_col);
+      const __amdgpu_buffer_rsrc_t rs = cache ? rs_c : rs_q;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, kd, 16, ro + ck, 0, 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, vd, 16, ro + v_step + cv, 0, 0, 0);
     }
   };
 
@@ -205,14 +208,15 @@ __global__ __launch_bounds__(NT, 2) void attn_bf16_kernel(AttnParams p) {
       }
       __builtin_amdgcn_sched_barrier(0);
     }
-    // keys at or past nk only occur in the last tile
-    if (kbase + KT > nk) {
+    // positions at or past nk only occur in the last tile, gap positions in
+    // the tile holding P
+    if (kbase + KT > nk || (P < P4 && kbase < P4 && kbase + KT > P)) {
 #pragma unroll
       for (int i = 0; i < 2; ++i)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           const int key = kbase + i * 32 + (r >> 2) * 8 + fhalf * 4 + (r & 3);
-          if (key >= nk) s[i][r] = -INFINITY;
+          if (key >= nk || (key >= P && key < P4)) s[i][r] = -INFINITY;
         }
     }
     float mt = s[0][0];

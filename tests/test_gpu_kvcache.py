@@ -26,7 +26,11 @@ from workloads.generate import make_workload
 pytestmark = pytest.mark.gpu
 
 TOL = {"bf16": 2e-2, "f32": 1e-4}
-SAME = {"bf16": 1e-2, "f32": 1e-5}   # cached vs full step, both on the GPU
+# cached vs full step, both on the GPU.  The cached step places the window's
+# own keys after the prefix rounded up to a multiple of 4, so its key tiles
+# (and the softmax rescale points) differ from the full step's and bf16 results
+# differ by a few ulps; each side is also held to TOL against the oracle.
+SAME = {"bf16": 2e-2, "f32": 1e-5}
 
 
 @pytest.fixture(scope="module")
