@@ -136,7 +136,7 @@ def bench_stack(args, w):
     import numpy as np
     import torch
     from paper_2607_14557_amd import seer as S
-    from paper_2607_14557_amd.runner import SeerStack, dims_for
+    from paper_2607_14557_amd.runner import SeerStack, StepGraphs, dims_for, pinned_ctrl, poll_ctrl
     from workloads.generate import layer_weights_torch, make_stack_batch
 
     sh = w.shape
@@ -158,9 +158,15 @@ def bench_stack(args, w):
     i32 = lambda a: torch.from_numpy(np.asarray(a, np.int32)).to(dev)
     cu, off, wl = i32(batch.cu_seqlens), i32(batch.win_off), i32(batch.win_len)
     log("  inputs and %d prepacked layers ready in %.1f s" % (L, time.perf_counter() - t0))
+    if args.graph:
+        # recorded steps need a created stream; everything runs on it
+        gs = torch.cuda.Stream()
+        torch.cuda.set_stream(gs)
+        ctrl_t, ctrl_w = pinned_ctrl(), pinned_ctrl()
     sp = torch.cuda.current_stream().cuda_stream
     hip = Hip()
     n_trunc = w.trunc_steps
+    graphs = {}
 
     kv = None
     if args.kv_cache:
@@ -173,6 +179,8 @@ def bench_stack(args, w):
         log("  prefix K/V caches: %d rows x %d layers (%.1f GB)" % (kv_rows, L, kv_rows * 2 * d * 2 * L / 1e9))
 
     def job():
+        if args.graph:
+            return job_graph()
         r = st.step0(x, cu, off, wl, B, T, w.l_det, w.act_eps, granule=granule, trunc_capacity=cap, stream=sp)
         if kv is None:
             for _ in range(n_trunc):
@@ -187,6 +195,35 @@ def bench_stack(args, w):
         for _ in range(n_trunc - 1):
             st.forward_cached(x_w, cu_w, used_w, B, max(rows_w, 1), caches, cu_kv, kv_rows, stream=sp)
         r.cached = (x_w, cu_w, used_w, rows_w)
+        return r
+
+    def job_graph():
+        # step 0 eager; the host polls the pinned control word of each repack
+        # (no stream sync) and replays the truncated steps recorded for the
+        # routed capacity's 1-D graph shape
+        r = st.step0(x, cu, off, wl, B, T, w.l_det, w.act_eps, granule=granule, trunc_capacity=cap,
+                     ctrl_host=ctrl_t, stream=sp)
+        if kv is None:
+            if "trunc" not in graphs:
+                graphs["trunc"] = StepGraphs(
+                    lambda rows: st.forward(r.x_trunc, r.cu_trunc, r.seqused, B, rows, stream=sp), gs, cap,
+                    granule)
+            for _ in range(n_trunc):
+                graphs["trunc"].run(r.routed["capacity_rows"])
+            return r
+        caches, cu_kv, kv_rows = kv
+        x_w, cu_w, used_w, _ = st.window_rows(x, cu, off, wl, r.keep_len, B, cap, granule=granule,
+                                              ctrl_host=ctrl_w, stream=sp)
+        st.forward_export(r.x_trunc, r.cu_trunc, r.seqused, B, r.rows_ub, caches, cu_kv, kv_rows, stream=sp)
+        routed_w = poll_ctrl(ctrl_w)
+        rows_w = routed_w["capacity_rows"]
+        if "cached" not in graphs:
+            graphs["cached"] = StepGraphs(
+                lambda rows: st.forward_cached(x_w, cu_w, used_w, B, rows, caches, cu_kv, kv_rows, stream=sp),
+                gs, cap, granule)
+        for _ in range(n_trunc - 1):
+            graphs["cached"].run(rows_w)
+        r.cached = (x_w, cu_w, used_w, max(rows_w, 1))
         return r
 
     log("warmup %d job(s)" % args.warmup)
@@ -223,6 +260,13 @@ def bench_stack(args, w):
         x_w, cu_w, used_w, rows_w = r.cached
         t_cached = timed(lambda: st.forward_cached(x_w, cu_w, used_w, B, max(rows_w, 1), kv[0], kv[1], kv[2],
                                                    stream=sp))
+    t_graph = {}
+    if args.graph:
+        log("timing one replay of each recorded step")
+        if kv is None:
+            t_graph["trunc"] = timed(lambda: graphs["trunc"].run(r.routed["capacity_rows"]))
+        else:
+            t_graph["cached"] = timed(lambda: graphs["cached"].run(r.cached[3]))
     # the dominant kernel: gate/up GEMM of a truncated step, timed inside one layer
     ev = [hip.event() for _ in range(8)]
     y = torch.empty(cap, d, dtype=torch.bfloat16, device=dev)
@@ -256,6 +300,10 @@ def bench_stack(args, w):
         "job_speedup_vs_untruncated": round(n_den * t_full / ms_job, 3),
         "cached_step_ms": None if t_cached is None else round(t_cached, 3),
         "speedup_cached_vs_trunc": None if t_cached is None else round(t_trunc / t_cached, 3),
+        "graph": bool(args.graph),
+        "trunc_step_ms_graph": round(t_graph["trunc"], 3) if "trunc" in t_graph else None,
+        "cached_step_ms_graph": round(t_graph["cached"], 3) if "cached" in t_graph else None,
+        "graph_shapes": {k: sorted(g.graphs) for k, g in graphs.items()} if args.graph else None,
         "cpu_baseline": None,
         "cpu_baseline_note": "one oracle step of a 32-layer stack takes hours; the default workload's line "
                              "carries the CPU baseline",
@@ -280,6 +328,10 @@ def main():
                     help="skip the separate untruncated-step and cached-prefix-step timings (they "
                          "launch the gate/up GEMM kernel at other sizes, which a per-kernel profile "
                          "would mix in)")
+    ap.add_argument("--graph", action="store_true",
+                    help="32-layer stacks: the host polls the pinned control word of each repack and "
+                         "replays the truncated (or cached) steps from HIP graphs recorded per 1-D graph "
+                         "shape of the routed capacity")
     ap.add_argument("--kv-cache", action="store_true",
                     help="32-layer stacks: after step 0, one full truncated step caches every layer's "
                          "prefix keys/values and the remaining steps run on the kept window rows")
@@ -287,7 +339,7 @@ def main():
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print("bench.py measures one GPU: this build has no multi-GPU path "
+        print("bench.py measures one GPU; there is no multi-GPU path "
               "(requested --gpus %d, WORLD_SIZE %d)" % (args.gpus, world), file=sys.stderr)
         sys.exit(2)
 
@@ -309,6 +361,10 @@ def main():
         raise SystemExit("bench.py times bf16 workloads")
     if w.n_layers > 1:
         return bench_stack(args, w)
+    if args.graph or args.kv_cache:
+        print("--graph and --kv-cache apply to the layer stacks (--workload llada32_video_b4 or "
+              "llada32_multicrop_b8)", file=sys.stderr)
+        sys.exit(2)
     sh = w.shape
     d, I = sh.d_model, sh.d_ff
     policy = {"hybrid": S.SEER_ROUTE_HYBRID, "naive_pad": S.SEER_ROUTE_NAIVE_PAD,

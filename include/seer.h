@@ -17,6 +17,8 @@
  *   seer_batch_repack          padding-waste-aware routing plus compaction
  *   seer_kv_export,            truncated steps on the window rows with the
  *   seer_layer_forward_cached  prefix keys/values cached (Appendix D)
+ *   seer_graph_*               record a launch sequence once, replay it
+ *                              (graph-compatible paths, Sec. 3.5)
  *
  * Conventions shared by every call:
  *   - Buffers are owned by the caller.  Pointers are device pointers unless a
@@ -52,7 +54,7 @@ extern "C" {
 /* ---- status codes ------------------------------------------------------ */
 #define SEER_OK            0
 #define SEER_EINVAL       -1   /* bad argument (null pointer, bad size, ...) */
-#define SEER_EUNSUPPORTED -2   /* shape or dtype this build has no kernel for */
+#define SEER_EUNSUPPORTED -2   /* shape or dtype the library has no kernel for */
 #define SEER_EWORKSPACE   -3   /* workspace or destination buffer too small */
 #define SEER_EHIP         -4   /* a HIP runtime call failed */
 
@@ -307,6 +309,34 @@ int seer_batch_repack(const seer_repack_desc* desc, const void* const* src,
                       const int32_t* keep_len, int32_t batch, int32_t* cu_dst,
                       int32_t* seqused, int32_t* route, seer_route_ctrl* ctrl_dev,
                       seer_route_ctrl* ctrl_host, hipStream_t stream);
+
+/* ---- recorded launch sequences (Sec. 3.5) -------------------------------
+ * The graph-compatible execution paths replay a fixed launch sequence.  Every
+ * kernel here reads its row counts and sequence offsets from device memory
+ * and sizes its grid from the rows_ub the host passes, so one recorded
+ * sequence serves every batch whose routed capacity (seer_route_ctrl.
+ * capacity_rows) is at most the rows_ub it was recorded with: a 1-D graph
+ * shape per capacity.
+ *
+ * seer_graph_begin starts recording the calls issued on `stream` by the
+ * calling host thread (HIP stream capture, thread-local mode); they are not
+ * run.  Only asynchronous seer_* entry points (not the _timed variant) may be
+ * issued on the stream until seer_graph_end, which closes the recording and
+ * instantiates it.  seer_graph_launch runs one replay on `stream`; a replay
+ * reads the current contents of every buffer that the recorded calls named,
+ * so inputs are updated in place between replays.  The buffers must stay
+ * allocated while the graph exists.  seer_graph_destroy frees the graph
+ * (NULL: no-op).  Replays on one stream run in order; a graph must not be
+ * replayed on two streams at once.
+ * Errors: EINVAL (null stream for begin, stream already recording, null
+ * graph), EHIP (the runtime refused the recording, e.g. a recorded call
+ * failed or an unsupported API was used while recording).  After a failed
+ * recorded call, seer_graph_end still ends the recording and returns EHIP. */
+typedef struct seer_graph_* seer_graph_t;
+int seer_graph_begin(hipStream_t stream);
+int seer_graph_end(hipStream_t stream, seer_graph_t* graph);
+int seer_graph_launch(seer_graph_t graph, hipStream_t stream);
+int seer_graph_destroy(seer_graph_t graph);
 
 /* Description of the last error on the calling host thread ("" if none). */
 const char* seer_last_error(void);

@@ -374,4 +374,55 @@ int seer_batch_repack(const seer_repack_desc* desc, const void* const* src, void
   return ok();
 }
 
+// ---- recorded launch sequences (Sec. 3.5, graph-compatible paths) ----------
+
+struct seer_graph_ {
+  hipGraph_t graph;
+  hipGraphExec_t exec;
+};
+
+int seer_graph_begin(hipStream_t stream) {
+  if (stream == nullptr) return fail(SEER_EINVAL, "the default (null) stream cannot be recorded; use a created stream");
+  hipStreamCaptureStatus st = hipStreamCaptureStatusNone;
+  if (hipStreamIsCapturing(stream, &st) != hipSuccess) return hip_fail("hipStreamIsCapturing");
+  if (st != hipStreamCaptureStatusNone) return fail(SEER_EINVAL, "the stream is already being recorded");
+  if (hipStreamBeginCapture(stream, hipStreamCaptureModeThreadLocal) != hipSuccess)
+    return hip_fail("hipStreamBeginCapture");
+  return ok();
+}
+
+int seer_graph_end(hipStream_t stream, seer_graph_t* graph) {
+  if (graph == nullptr) return fail(SEER_EINVAL, "graph is NULL");
+  *graph = nullptr;
+  if (stream == nullptr) return fail(SEER_EINVAL, "stream is NULL");
+  hipGraph_t g = nullptr;
+  if (hipStreamEndCapture(stream, &g) != hipSuccess || g == nullptr) {
+    if (g) hipGraphDestroy(g);
+    return hip_fail("hipStreamEndCapture (a call recorded since seer_graph_begin failed, or the stream "
+                    "was not being recorded)");
+  }
+  hipGraphExec_t exec = nullptr;
+  if (hipGraphInstantiate(&exec, g, nullptr, nullptr, 0) != hipSuccess) {
+    hipGraphDestroy(g);
+    return hip_fail("hipGraphInstantiate");
+  }
+  *graph = new seer_graph_{g, exec};
+  return ok();
+}
+
+int seer_graph_launch(seer_graph_t graph, hipStream_t stream) {
+  if (graph == nullptr) return fail(SEER_EINVAL, "graph is NULL");
+  if (hipGraphLaunch(graph->exec, stream) != hipSuccess) return hip_fail("hipGraphLaunch");
+  return ok();
+}
+
+int seer_graph_destroy(seer_graph_t graph) {
+  if (graph == nullptr) return ok();
+  const bool bad = hipGraphExecDestroy(graph->exec) != hipSuccess;
+  const bool bad2 = hipGraphDestroy(graph->graph) != hipSuccess;
+  delete graph;
+  if (bad || bad2) return hip_fail("hipGraphExecDestroy / hipGraphDestroy");
+  return ok();
+}
+
 }  // extern "C"

@@ -9,9 +9,17 @@ residual and of the step-input embeddings in one launch, then the remaining
 layers on the compacted batch.  Later denoising steps run every layer on the
 compacted batch, or, with the prefix keys/values cached (Appendix D), on the
 kept window rows alone.
+
+Graph-compatible execution (Sec. 3.5): every kernel reads its row counts from
+device memory, so one recorded launch sequence (a HIP graph, recorded through
+the library's seer_graph_* calls) serves any batch whose routed capacity fits
+the rows bound it was recorded with.  The repack kernel writes the routed
+shape to pinned host memory; the host polls that word, without waiting on the
+stream, to pick the recorded sequence for the capacity.
 """
+import time
 from dataclasses import dataclass
-from typing import List, Optional
+from typing import Dict, List, Optional
 
 import torch
 
@@ -27,6 +35,76 @@ def torch_dtype(dtype):
     return torch.bfloat16 if dtype == "bf16" else torch.float32
 
 
+CTRL_FIELDS = ("total_rows", "capacity_rows", "n_static", "n_varlen", "n_eager", "n_groups", "max_alloc",
+               "status", "ready")
+
+
+def pinned_ctrl():
+    """A host-pinned control word (16 int32) for seer_batch_repack."""
+    return torch.zeros(16, dtype=torch.int32, pin_memory=True)
+
+
+def poll_ctrl(ctrl_host, timeout_s=30.0):
+    """Spin on the pinned control word until the repack kernel has written it
+    (its ready field is stored last), without synchronising any stream.
+    Returns the fields as a dict.  The caller clears `ready` (ctrl_host[8] = 0)
+    before enqueuing the repack."""
+    a = ctrl_host.numpy()
+    t_end = time.monotonic() + timeout_s
+    while int(a[8]) != 1:
+        if time.monotonic() > t_end:
+            raise TimeoutError("control word not written within %.0f s" % timeout_s)
+    v = [int(a[i]) for i in range(9)]
+    return dict(zip(CTRL_FIELDS, v))
+
+
+def graph_shape(rows, granule=256):
+    """The 1-D graph shape for a routed capacity: the smallest of granule x
+    {1, 2, 3, 4, 6, 8, 12, 16, ...} (at most 1.5x over) that holds `rows`."""
+    units = max(1, -(-int(rows) // granule))
+    u = 1
+    while u < units:
+        if u >= 2 and u & (u - 1) == 0:
+            u += u // 2            # 2^k -> 1.5 x 2^k
+        elif u % 3 == 0:
+            u = u // 3 * 4         # 1.5 x 2^k -> 2^(k+1)
+        else:
+            u = 2 * u
+    return u * granule
+
+
+class SeerGraph:
+    """A recorded launch sequence; replay() runs it on a stream."""
+
+    def __init__(self, handle):
+        self.handle = handle
+
+    def replay(self, stream=None):
+        S.seer_graph_launch(self.handle, stream=stream)
+
+    def close(self):
+        if self.handle:
+            S.seer_graph_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def record(fn, stream):
+    """Record the seer calls fn() issues on `stream` (a created torch stream;
+    fn must issue nothing else on it) into a SeerGraph."""
+    S.seer_graph_begin(stream)
+    try:
+        fn()
+    finally:
+        handle = S.seer_graph_end(stream)
+    return SeerGraph(handle)
+
+
 @dataclass
 class Step0Result:
     counts: torch.Tensor        # [rows_full] int32 at the detection layer
@@ -38,6 +116,40 @@ class Step0Result:
     ctrl: torch.Tensor          # [16] int32 (device copy of the control word)
     x_trunc: torch.Tensor       # compacted step-input embeddings
     h_trunc: torch.Tensor       # step-0 residual after the last layer (compacted)
+    routed: Optional[dict] = None   # the control word read from pinned memory (if polled)
+    rows_ub: int = 0            # rows bound the layers after the repack ran with
+
+
+class StepGraphs:
+    """Recorded denoising steps, one per 1-D graph shape (Sec. 3.5).
+
+    step_fn(rows_ub) issues one step's seer calls on `stream`, on buffers that
+    stay fixed for the life of this object; run(capacity_rows) replays the
+    recording for graph_shape(capacity_rows) (recorded on first use)."""
+
+    def __init__(self, step_fn, stream, max_rows, granule=256):
+        self.step_fn = step_fn
+        self.stream = stream
+        self.max_rows = int(max_rows)
+        self.granule = granule
+        self.graphs: Dict[int, SeerGraph] = {}
+
+    def shape(self, capacity_rows):
+        return min(graph_shape(capacity_rows, self.granule), self.max_rows)
+
+    def run(self, capacity_rows):
+        rows = self.shape(capacity_rows)
+        g = self.graphs.get(rows)
+        if g is None:
+            g = record(lambda: self.step_fn(rows), self.stream)
+            self.graphs[rows] = g
+        g.replay(self.stream)
+        return rows
+
+    def close(self):
+        for g in self.graphs.values():
+            g.close()
+        self.graphs.clear()
 
 
 class SeerStack:
@@ -58,6 +170,7 @@ class SeerStack:
         self.workspace = torch.empty(self.ws_bytes, dtype=torch.uint8, device=device)
         d = dims.d_model
         self.buf = [torch.zeros(self.max_rows, d, dtype=self.dtype, device=device) for _ in range(2)]
+        self._trunc_bufs = {}
 
     def set_layer(self, l, weights, stream=None):
         if self.packed[l] is None:
@@ -123,19 +236,28 @@ class SeerStack:
         return cur
 
     def window_rows(self, src, cu_src, win_off, win_len, keep, batch, capacity, policy=S.SEER_ROUTE_HYBRID,
-                    tau_pad=(1, 5), granule=256, stream=None):
+                    tau_pad=(1, 5), granule=256, ctrl_host=None, stream=None):
         """The kept window rows of each sequence of `src`, routed and compacted
-        (no prefix rows): returns (rows, cu, seqused, route)."""
+        (no prefix rows): returns (rows, cu, seqused, route).  The buffers are
+        owned by the stack and reused by the next call of the same shape.  With
+        ctrl_host (pinned_ctrl()), the routed shape is also written there for
+        poll_ctrl; its ready field is cleared here before the launch."""
         dev = self.device
-        dst = torch.empty(capacity, self.dims.d_model, dtype=self.dtype, device=dev)
-        cu = torch.empty(batch + 1, dtype=torch.int32, device=dev)
-        used = torch.empty(batch, dtype=torch.int32, device=dev)
-        route = torch.empty(batch, 3, dtype=torch.int32, device=dev)
+        key = ("win", capacity, batch)
+        if key not in self._trunc_bufs:
+            self._trunc_bufs[key] = (
+                torch.empty(capacity, self.dims.d_model, dtype=self.dtype, device=dev),
+                torch.empty(batch + 1, dtype=torch.int32, device=dev),
+                torch.empty(batch, dtype=torch.int32, device=dev),
+                torch.empty(batch, 3, dtype=torch.int32, device=dev))
+        dst, cu, used, route = self._trunc_bufs[key]
         desc = S.seer_repack_desc(policy, tau_pad[0], tau_pad[1], granule,
                                   self.dims.d_model * (2 if self.dtype == torch.bfloat16 else 4),
                                   capacity, 0, S.SEER_REPACK_WINDOW_ONLY)
+        if ctrl_host is not None:
+            ctrl_host[8] = 0
         S.seer_batch_repack(desc, [src], [dst], cu_src, win_off, win_len, keep, batch, cu, used, route,
-                            stream=stream)
+                            ctrl_host=ctrl_host, stream=stream)
         return dst, cu, used, route
 
     def step0(self, x_full, cu_full, win_off, win_len, batch, rows_full, l_det, act_eps,
@@ -149,24 +271,44 @@ class SeerStack:
             self.layer(l, cur, nxt, cu_full, None, batch, rows_full,
                        act_eps=act_eps, act_count=counts if l == l_det else None, stream=stream)
             cur = nxt
-        boundary = torch.empty(batch, dtype=torch.int32, device=dev)
-        keep = torch.empty(batch, dtype=torch.int32, device=dev)
+        cap = trunc_capacity if trunc_capacity is not None else rows_full + granule
+        key = (cap, batch)
+        if key not in self._trunc_bufs:
+            # compacted buffers, reused by every step0 call of this shape so that
+            # recorded truncated steps keep valid addresses
+            d = self.dims.d_model
+            self._trunc_bufs[key] = dict(
+                boundary=torch.empty(batch, dtype=torch.int32, device=dev),
+                keep=torch.empty(batch, dtype=torch.int32, device=dev),
+                x_t=torch.empty(cap, d, dtype=self.dtype, device=dev),
+                h_t=torch.empty(cap, d, dtype=self.dtype, device=dev),
+                cu_t=torch.empty(batch + 1, dtype=torch.int32, device=dev),
+                used=torch.empty(batch, dtype=torch.int32, device=dev),
+                route=torch.empty(batch, 3, dtype=torch.int32, device=dev),
+                ctrl=torch.zeros(16, dtype=torch.int32, device=dev))
+        tb = self._trunc_bufs[key]
+        boundary, keep, x_t, h_t = tb["boundary"], tb["keep"], tb["x_t"], tb["h_t"]
+        cu_t, used, route, ctrl = tb["cu_t"], tb["used"], tb["route"], tb["ctrl"]
         S.seer_step0_detect(counts, cu_full, win_off, win_len, batch, self.dims.d_ff,
                             S.seer_snr_params(*snr), boundary, keep, stream=stream)
-        cap = trunc_capacity if trunc_capacity is not None else rows_full + granule
-        x_t = torch.empty(cap, self.dims.d_model, dtype=self.dtype, device=dev)
-        h_t = torch.empty(cap, self.dims.d_model, dtype=self.dtype, device=dev)
-        cu_t = torch.empty(batch + 1, dtype=torch.int32, device=dev)
-        used = torch.empty(batch, dtype=torch.int32, device=dev)
-        route = torch.empty(batch, 3, dtype=torch.int32, device=dev)
-        ctrl = torch.zeros(16, dtype=torch.int32, device=dev)
         desc = S.seer_repack_desc(policy, tau_pad[0], tau_pad[1], granule,
                                   self.dims.d_model * (2 if self.dtype == torch.bfloat16 else 4),
                                   cap, 0, 0)
+        if ctrl_host is not None:
+            ctrl_host[8] = 0
         S.seer_batch_repack(desc, [x_full, cur], [x_t, h_t], cu_full, win_off, win_len, keep, batch,
                             cu_t, used, route, ctrl, ctrl_host, stream=stream)
+        routed = None
+        rows_ub = cap
+        if ctrl_host is not None:
+            # the routed capacity sizes the remaining launches (no stream sync)
+            routed = poll_ctrl(ctrl_host)
+            if routed["status"] != 0:
+                raise S.SeerError(routed["status"], "compacted batch exceeds the %d-row buffers" % cap)
+            rows_ub = max(1, min(cap, routed["capacity_rows"]))
         if l_det + 1 < self.n_layers:
-            h_t = self.forward(h_t, cu_t, used, batch, cap, layers=range(l_det + 1, self.n_layers),
+            h_t = self.forward(h_t, cu_t, used, batch, rows_ub, layers=range(l_det + 1, self.n_layers),
                                out=h_t, stream=stream)
         return Step0Result(counts=counts, boundary=boundary, keep_len=keep, cu_trunc=cu_t,
-                           seqused=used, route=route, ctrl=ctrl, x_trunc=x_t, h_trunc=h_t)
+                           seqused=used, route=route, ctrl=ctrl, x_trunc=x_t, h_trunc=h_t,
+                           routed=routed, rows_ub=rows_ub)

@@ -21,7 +21,8 @@ SEER_REPACK_WINDOW_ONLY = 1
 EXPORTED = ("seer_prepacked_bytes", "seer_prepack_weights", "seer_layer_workspace_bytes",
             "seer_layer_workspace_offsets", "seer_layer_forward_varlen",
             "seer_layer_forward_varlen_timed", "seer_step0_detect", "seer_batch_repack",
-            "seer_layer_forward_cached", "seer_kv_export", "seer_last_error", "seer_abi_version")
+            "seer_layer_forward_cached", "seer_kv_export", "seer_graph_begin", "seer_graph_end",
+            "seer_graph_launch", "seer_graph_destroy", "seer_last_error", "seer_abi_version")
 
 
 class SeerError(RuntimeError):
@@ -104,6 +105,14 @@ def load_library():
     L.seer_layer_forward_cached.restype = ctypes.c_int
     L.seer_kv_export.argtypes = [ctypes.POINTER(seer_dims), _P, ctypes.c_size_t, _I, _P, _I, _P, _I, _P, _P]
     L.seer_kv_export.restype = ctypes.c_int
+    L.seer_graph_begin.argtypes = [_P]
+    L.seer_graph_begin.restype = ctypes.c_int
+    L.seer_graph_end.argtypes = [_P, ctypes.POINTER(_P)]
+    L.seer_graph_end.restype = ctypes.c_int
+    L.seer_graph_launch.argtypes = [_P, _P]
+    L.seer_graph_launch.restype = ctypes.c_int
+    L.seer_graph_destroy.argtypes = [_P]
+    L.seer_graph_destroy.restype = ctypes.c_int
     L.seer_last_error.argtypes = []
     L.seer_last_error.restype = ctypes.c_char_p
     L.seer_abi_version.argtypes = []
@@ -221,3 +230,23 @@ def seer_batch_repack(desc, srcs, dsts, cu_src, win_off, win_len, keep_len, batc
         ctypes.byref(desc), src_arr, dst_arr, n, _ptr(cu_src), _ptr(win_off), _ptr(win_len),
         _ptr(keep_len), int(batch), _ptr(cu_dst), _ptr(seqused), _ptr(route), _ptr(ctrl_dev),
         _ptr(ctrl_host), _stream(stream)))
+
+
+def seer_graph_begin(stream):
+    """Start recording the seer calls issued on `stream` (a created stream)."""
+    _check(load_library().seer_graph_begin(_stream(stream)))
+
+
+def seer_graph_end(stream):
+    """End the recording; returns the graph handle (an int)."""
+    g = _P()
+    _check(load_library().seer_graph_end(_stream(stream), ctypes.byref(g)))
+    return g.value
+
+
+def seer_graph_launch(graph, stream=None):
+    _check(load_library().seer_graph_launch(graph, _stream(stream)))
+
+
+def seer_graph_destroy(graph):
+    _check(load_library().seer_graph_destroy(graph))

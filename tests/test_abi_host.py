@@ -175,3 +175,27 @@ def test_kv_export_argument_errors(S):
     assert call(dst=FAKE + 4) == S.SEER_EINVAL                    # misaligned destination
     assert call(ws_bytes=1024) == S.SEER_EWORKSPACE
     assert call(ws=FAKE + 16) == S.SEER_EINVAL                    # misaligned workspace
+
+
+def test_graph_argument_errors(S):
+    L = S.load_library()
+    g = ctypes.c_void_p(123)
+    assert L.seer_graph_begin(None) == S.SEER_EINVAL
+    assert "stream" in S.seer_last_error()
+    assert L.seer_graph_end(FAKE, None) == S.SEER_EINVAL
+    assert L.seer_graph_end(None, ctypes.byref(g)) == S.SEER_EINVAL
+    assert g.value is None                      # cleared on error
+    assert L.seer_graph_launch(None, FAKE) == S.SEER_EINVAL
+    assert L.seer_graph_destroy(None) == S.SEER_OK
+
+
+def test_graph_shapes():
+    from paper_2607_14557_amd.runner import graph_shape
+    g = 256
+    shapes = [graph_shape(r, g) for r in range(0, 200 * g, 37)]
+    assert shapes == sorted(shapes)
+    assert sorted(set(s // g for s in shapes))[:9] == [1, 2, 3, 4, 6, 8, 12, 16, 24]
+    for r in range(1, 200 * g, 53):
+        s = graph_shape(r, g)
+        assert s % g == 0 and s >= r
+        assert s <= max(2 * g, 1.5 * (-(-r // g) * g))
