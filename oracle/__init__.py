@@ -15,6 +15,8 @@ Modules (each function cites the passage of the paper it follows):
   pipeline  -- step 0 detection, one-shot truncation, truncated steps
   kvcache   -- truncated steps on the window rows with the prefix's keys and
                values cached (Appendix D, KV-cache compatibility)
+  rope      -- rotary position embedding of queries and keys (the paper is
+               silent on positions; RoFormer's definition, rotate-half pairs)
 
 Parity status: every function here is pinned by CPU tests against values
 fixed by the mathematics (brute force, closed forms, invariants, planted
@@ -28,3 +30,4 @@ from .route import (bucket_set, bucket_of, padding_waste_ratio, coarse_class,
                     route_batch, repack_rows, RouteResult)
 from .pipeline import run_pipeline, PipelineResult
 from .kvcache import prefix_kv, layer_forward_cached_rows, layer_forward_cached
+from .rope import rope_angles, apply_rope

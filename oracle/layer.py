@@ -7,8 +7,10 @@ SwiGLU MLP.  Attention follows the Sec. 3.6 equations: logits q.k/sqrt(d_h),
 a softmax over every key of the same sequence, a weighted sum of values.
 
 Readings where the paper is silent: pre-norm RMSNorm (gain g, eps 1e-5) before
-attention and before the MLP, no biases, no positional encoding, scale
-1/sqrt(head_dim).  Rows of a sequence at index >= ``used`` are inert padding:
+attention and before the MLP, no biases, scale 1/sqrt(head_dim), and by default
+no positional encoding; with ``rope_theta`` set, queries and keys are rotated
+by their position in the sequence (``rope.apply_rope``; position = row index
+plus ``pos_offset``).  Rows of a sequence at index >= ``used`` are inert padding:
 they are not attention keys and receive no attention output; the rest of the
 layer applies to them row by row.
 
@@ -17,6 +19,8 @@ directly from the definitions: softmax is evaluated on the full logit row,
 not online.
 """
 import numpy as np
+
+from .rope import apply_rope
 
 
 def silu(z):
@@ -58,7 +62,8 @@ def _w(W, name):
     return np.asarray(W[name], np.float64)
 
 
-def layer_forward_rows(x_seq, used, W, n_heads, rms_eps, rows, want_act=False):
+def layer_forward_rows(x_seq, used, W, n_heads, rms_eps, rows, want_act=False, rope_theta=None,
+                       pos_offset=0):
     """Layer outputs for selected rows of one sequence.
 
     x_seq: [S, d] rows of one sequence; ``used``: rows [0, used) are real,
@@ -77,6 +82,9 @@ def layer_forward_rows(x_seq, used, W, n_heads, rms_eps, rows, want_act=False):
     xr = x_seq[rows]
     ar = rms_norm(xr, g1, rms_eps)
     q = ar @ _w(W, "wq").T
+    if rope_theta:
+        k = apply_rope(k, pos_offset + np.arange(used), n_heads, rope_theta)
+        q = apply_rope(q, pos_offset + rows, n_heads, rope_theta)
     o = np.zeros_like(xr)
     real = rows < used
     if used > 0 and np.any(real):
@@ -95,7 +103,7 @@ def layer_forward_rows(x_seq, used, W, n_heads, rms_eps, rows, want_act=False):
     return out
 
 
-def layer_forward(x, cu_seqlens, W, n_heads, rms_eps, seqused=None, act_eps=None):
+def layer_forward(x, cu_seqlens, W, n_heads, rms_eps, seqused=None, act_eps=None, rope_theta=None):
     """One layer over packed sequences (rows of sequence b are cu[b]..cu[b+1]).
 
     Returns (y [T, d] float64, counts [T] int64 or None).  ``counts`` is the
@@ -114,7 +122,7 @@ def layer_forward(x, cu_seqlens, W, n_heads, rms_eps, seqused=None, act_eps=None
         if S == 0:
             continue
         r = layer_forward_rows(x[s0:s1], used, W, n_heads, rms_eps, np.arange(S),
-                               want_act=act_eps is not None)
+                               want_act=act_eps is not None, rope_theta=rope_theta)
         y[s0:s1] = r["y"]
         if act_eps is not None:
             counts[s0:s1] = near_zero_count(r["act"], act_eps)
