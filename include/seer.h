@@ -72,6 +72,13 @@ typedef struct seer_dims {
   int32_t d_ff;        /* SwiGLU intermediate size I */
   int32_t dtype;       /* SEER_DTYPE_* */
   float rms_eps;       /* RMSNorm epsilon (1e-5 for the LLaDA-shaped layer) */
+  float rope_theta;    /* 0: no positional encoding (the paper's layer equations have
+                          none).  > 1: rotary embedding of q and k (RoFormer's
+                          definition, rotate-half pairs): features j and j + head_dim/2
+                          of each head turn by pos * rope_theta^(-2 j / head_dim), pos
+                          being the row's index in its sequence (plus the cached prefix
+                          length in seer_layer_forward_cached).  The angle is reduced in
+                          fp64 and evaluated by the hardware sine/cosine in fp32. */
 } seer_dims;
 
 /* Source weights of one layer (device pointers, dtype = dims.dtype, [out, in]):
@@ -342,7 +349,7 @@ int seer_graph_destroy(seer_graph_t graph);
 const char* seer_last_error(void);
 
 /* ABI version of this library (major * 100 + minor). */
-int32_t seer_abi_version(void);
+int32_t seer_abi_version(void);   /* 101: seer_dims.rope_theta */
 
 #ifdef __cplusplus
 }

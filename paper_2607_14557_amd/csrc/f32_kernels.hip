@@ -211,4 +211,38 @@ int launch_attn_f32(const AttnParams& p, hipStream_t s) {
   return hipGetLastError() == hipSuccess ? 0 : -1;
 }
 
+// ---------------------------------------------------------------------------
+// Rotary embedding of the q and k columns of an fp32 qkv buffer, in place: one
+// thread per (row, q|k, head, pair j < head_dim / 2); pair (j, j + head_dim/2)
+// of the head turns by 2 pi * frac(pos[r] * freq[j]).
+__global__ __launch_bounds__(256) void rope_f32_kernel(float* qkv, int d, int head_dim, const int* m_ptr,
+                                                       int m_ub, const int* pos, const double* freq) {
+  const int M = rows_from(m_ptr, m_ub);
+  const int half = head_dim >> 1;
+  const int per_row = d;                 // 2 d columns rotated in pairs: d pairs per row
+  const long long t = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  const int row = (int)(t / per_row);
+  if (row >= M) return;
+  const int k = (int)(t % per_row);      // pair index over q and k
+  const int head = k / half, j = k % half;
+  float* x = qkv + (size_t)row * 3 * d + head * head_dim + j;
+  double rv = (double)pos[row] * freq[j];
+  rv -= floor(rv);
+  const float a = (float)rv;
+  const float sn = __builtin_amdgcn_sinf(a), cs = __builtin_amdgcn_cosf(a);
+  const float x1 = x[0], x2 = x[half];
+  x[0] = x1 * cs - x2 * sn;
+  x[half] = x2 * cs + x1 * sn;
+}
+
+int launch_rope_f32(float* qkv, int d, int n_heads, int head_dim, const int* m_ptr, int m_ub,
+                    const int* pos, const double* freq, hipStream_t s) {
+  (void)n_heads;
+  if (head_dim % 2 != 0) return -1;
+  const long long work = (long long)m_ub * d;
+  dim3 grid((unsigned)((work + 255) / 256)), block(256);
+  hipLaunchKernelGGL(rope_f32_kernel, grid, block, 0, s, qkv, d, head_dim, m_ptr, m_ub, pos, freq);
+  return hipGetLastError() == hipSuccess ? 0 : -1;
+}
+
 }  // namespace seer

@@ -310,6 +310,38 @@ __device__ __forceinline__ void gemm_tile(const GemmParams& p, uint8_t* smem, in
 #pragma unroll
     for (int i = 0; i < RDEPTH; ++i) fetch(i, rq[i]);
   }
+  // Rotary embedding of the q and k heads.  The wave's 128 columns are one
+  // head, and feature c of the head sits in tile j = c / 32, register
+  // 4 (c % 32 / 8) + c % 4 of lane half (c % 8) / 4; so the partner c + 64
+  // is in tile j + 2 of the same lane and register.
+  constexpr bool kRope = EPI == EPI_SCALE && BN == 256;
+  const bool rope_on = kRope && p.rope_pos != nullptr && n0 + wn * (BN / 2) < p.rope_col1;
+  int rpos[4] = {0, 0, 0, 0};
+  if (rope_on) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      int row = m0 + wm * 128 + i * 32 + fr;
+      row = row < M ? row : M - 1;
+      rpos[i] = p.rope_pos[row];
+    }
+  }
+  auto rope_block = [&](int i) {
+    const double pos = (double)rpos[i];
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          double rv = pos * p.rope_freq[32 * j + 8 * q + cq + e];
+          rv -= floor(rv);
+          const float t = (float)rv;            // revolutions in [0, 1)
+          const float sn = __builtin_amdgcn_sinf(t), cs = __builtin_amdgcn_cosf(t);
+          const float a = acc[i][j][4 * q + e], b = acc[i][j + 2][4 * q + e];
+          acc[i][j][4 * q + e] = a * cs - b * sn;
+          acc[i][j + 2][4 * q + e] = b * cs + a * sn;
+        }
+  };
   // V columns of the QKV projection are stored as fp16 (block-uniform)
   const bool to_f16 = EPI == EPI_SCALE && p.f16_col0 > 0 && n0 >= p.f16_col0;
 
@@ -426,6 +458,9 @@ __device__ __forceinline__ void gemm_tile(const GemmParams& p, uint8_t* smem, in
         if (ok && fhalf == 0) atomicAdd(p.cnt + row, nz);
       }
     } else {
+      if constexpr (kRope) {
+        if (rope_on) rope_block(i);
+      }
       const u32x4_t* rr = rq[i % RDEPTH];
       if (EPI == EPI_SCALE && to_f16)
         store_block(std::true_type{}, i, rr);
@@ -471,6 +506,8 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmParams p) {
 }
 
 int launch_gemm_bf16(int epi, const GemmParams& p, hipStream_t s) {
+  // the rotary pairs of a head span both column halves of a 256x128 unit
+  if (p.rope_pos && (epi != EPI_SCALE || p.n_units > 0 || p.rope_col1 % 128 != 0)) return -1;
   const int tiles_m = (p.m_ub + BM - 1) / BM;
   const int tiles_n = p.N / 256;
   // the split last round adds at most n_units / 2 units

@@ -40,6 +40,12 @@ struct GemmParams {
   // tiles leave a last round of r <= n_units / 2 tiles, those r tiles run as
   // 2 r halves of 256x128.  0 disables the split.
   int n_units;
+  // bf16 SCALE only: rotary embedding of output columns < rope_col1 (whole
+  // 128-wide heads): row r's pair (c, c + 64) of each head is rotated by
+  // 2 pi * frac(rope_pos[r] * rope_freq[c % 64]); null: none
+  const int* rope_pos;
+  const double* rope_freq;
+  int rope_col1;
 };
 
 // bf16 operands; requires N % 256 == 0, K % 128 == 0, 16-byte aligned rows.
@@ -49,9 +55,29 @@ int launch_gemm_bf16(int epi, const GemmParams& p, hipStream_t s);
 // fp32 operands, any N and K.  For SWIGLU*, B = Wg, B2 = Wu, both [N=I, K].
 int launch_gemm_f32(int epi, const GemmParams& p, hipStream_t s);
 
-// inv_rms[r] = 1 / sqrt(mean_j x[r,j]^2 + eps) for r < M.
+// Row positions and rotary frequencies for the rotary embedding of q and k:
+// pos[r] = r - cu[b] + (cu_kv ? cu_kv[b+1] - cu_kv[b] : 0) for the sequence b
+// holding row r < M, and freq[j] = theta^(-2 j / head_dim) / (2 pi) (in
+// revolutions per position) for j < head_dim / 2.
+struct RopeArgs {
+  const int* cu;
+  int B;
+  const int* cu_kv;
+  int* pos;
+  double* freq;
+  float theta;
+  int head_dim;
+};
+
+// inv_rms[r] = 1 / sqrt(mean_j x[r,j]^2 + eps) for r < M; with rope, also
+// the rotary positions and frequencies above.
 int launch_rms_inv(bool bf16, const void* x, int ld, int d, const int* m_ptr, int m_ub,
-                   float eps, float* out, hipStream_t s);
+                   float eps, float* out, hipStream_t s, const RopeArgs* rope = nullptr);
+
+// fp32: rotate the q and k columns of qkv ([M, 3d]) in place with the
+// positions and frequencies written by launch_rms_inv.
+int launch_rope_f32(float* qkv, int d, int n_heads, int head_dim, const int* m_ptr, int m_ub,
+                    const int* pos, const double* freq, hipStream_t s);
 
 struct AttnParams {
   const void* qkv;       // [T, 3d]: q | k | v, head h at columns h*dh of each

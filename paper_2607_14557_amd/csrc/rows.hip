@@ -10,11 +10,26 @@ namespace seer {
 // GEMM: (x * inv_rms) W^T = inv_rms * (x W^T).
 template <bool BF16>
 __global__ __launch_bounds__(256) void rms_inv_kernel(const void* x, int ld, int d, const int* m_ptr,
-                                                      int m_ub, float eps, float* out) {
+                                                      int m_ub, float eps, float* out, RopeArgs rope) {
   const int M = rows_from(m_ptr, m_ub);
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
+  if (rope.pos && blockIdx.x == 0 && threadIdx.x < rope.head_dim / 2) {
+    const int j = threadIdx.x;
+    rope.freq[j] = pow((double)rope.theta, -2.0 * j / rope.head_dim) / 6.283185307179586;   // / (2 pi)
+  }
   if (row >= M) return;
+  if (rope.pos && lane == 0) {
+    // sequence of the row: the last b with cu[b] <= row
+    int lo = 0, hi = rope.B - 1;
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (rope.cu[mid] <= row) lo = mid;
+      else hi = mid - 1;
+    }
+    const int pre = rope.cu_kv ? rope.cu_kv[lo + 1] - rope.cu_kv[lo] : 0;
+    rope.pos[row] = row - rope.cu[lo] + (pre > 0 ? pre : 0);
+  }
   float acc = 0.0f;
   if constexpr (BF16) {
     const uint16_t* xr = static_cast<const uint16_t*>(x) + (size_t)row * ld;
@@ -38,12 +53,14 @@ __global__ __launch_bounds__(256) void rms_inv_kernel(const void* x, int ld, int
 }
 
 int launch_rms_inv(bool bf16, const void* x, int ld, int d, const int* m_ptr, int m_ub, float eps,
-                   float* out, hipStream_t s) {
+                   float* out, hipStream_t s, const RopeArgs* rope) {
   dim3 grid((m_ub + 3) / 4), block(256);
+  RopeArgs r{};
+  if (rope) r = *rope;
   if (bf16)
-    hipLaunchKernelGGL(rms_inv_kernel<true>, grid, block, 0, s, x, ld, d, m_ptr, m_ub, eps, out);
+    hipLaunchKernelGGL(rms_inv_kernel<true>, grid, block, 0, s, x, ld, d, m_ptr, m_ub, eps, out, r);
   else
-    hipLaunchKernelGGL(rms_inv_kernel<false>, grid, block, 0, s, x, ld, d, m_ptr, m_ub, eps, out);
+    hipLaunchKernelGGL(rms_inv_kernel<false>, grid, block, 0, s, x, ld, d, m_ptr, m_ub, eps, out, r);
   return hipGetLastError() == hipSuccess ? 0 : -1;
 }
 

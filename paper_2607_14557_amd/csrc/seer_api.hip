@@ -47,6 +47,10 @@ int check_dims(const seer_dims* d) {
     return fail(SEER_EINVAL, "n_heads * head_dim (%d) != d_model (%d)", d->n_heads * d->head_dim,
                 d->d_model);
   if (!(d->rms_eps >= 0.0f) || !isfinite(d->rms_eps)) return fail(SEER_EINVAL, "rms_eps must be finite and >= 0");
+  if (!(d->rope_theta >= 0.0f) || !isfinite(d->rope_theta) || (d->rope_theta > 0.0f && d->rope_theta <= 1.0f))
+    return fail(SEER_EINVAL, "rope_theta must be 0 (no rotary embedding) or finite and > 1");
+  if (d->rope_theta > 0.0f && d->head_dim % 2 != 0)
+    return fail(SEER_EUNSUPPORTED, "the rotary embedding needs an even head_dim");
   if (d->dtype == SEER_DTYPE_BF16) {
     if (d->d_model % 256 != 0 || d->d_ff % 128 != 0 || d->head_dim != 128)
       return fail(SEER_EUNSUPPORTED,
@@ -61,7 +65,7 @@ int check_dims(const seer_dims* d) {
 }
 
 struct WsLayout {
-  size_t qkv, o, h1, act, inv1, inv2, h1lo, total;
+  size_t qkv, o, h1, act, inv1, inv2, h1lo, pos, freq, total;
 };
 
 WsLayout ws_layout(const seer_dims* d, int rows) {
@@ -79,6 +83,9 @@ WsLayout ws_layout(const seer_dims* d, int rows) {
   // residual add
   L.h1lo = d->dtype == SEER_DTYPE_BF16 ? off : L.h1;
   if (d->dtype == SEER_DTYPE_BF16) off = up256(off + R * d->d_model * 2);
+  // rotary embedding: per-row positions and the per-pair frequencies
+  L.pos = off;  off = up256(off + R * 4);
+  L.freq = off; off = up256(off + 64 * 8);
   L.total = off;
   return L;
 }
@@ -89,7 +96,7 @@ extern "C" {
 
 const char* seer_last_error(void) { return g_err.c_str(); }
 
-int32_t seer_abi_version(void) { return 100; }
+int32_t seer_abi_version(void) { return 101; }
 
 size_t seer_prepacked_bytes(const seer_dims* dims) {
   if (check_dims(dims) != SEER_OK) return 0;
@@ -166,6 +173,9 @@ static int layer_forward_impl(const seer_dims* dims, const void* w_packed, const
   float* inv1 = reinterpret_cast<float*>(ws + L.inv1);
   float* inv2 = reinterpret_cast<float*>(ws + L.inv2);
   void* h1lo = ws + L.h1lo;
+  const bool rope = dims->rope_theta > 0.0f;
+  int* rpos = reinterpret_cast<int*>(ws + L.pos);
+  double* rfreq = reinterpret_cast<double*>(ws + L.freq);
   int n_units = 0;                      // CUs: sizes the split of a partly filled last GEMM round
   if (bf16) {
     int dev = 0;
@@ -181,9 +191,14 @@ static int layer_forward_impl(const seer_dims* dims, const void* w_packed, const
 
   auto mark = [&](int k) { return ev ? hipEventRecord(ev[k], stream) : hipSuccess; };
   if (mark(0) != hipSuccess) return hip_fail("event record");
-  // 1. RMSNorm statistics of the layer input
-  if (seer::launch_rms_inv(bf16, x_in, d, d, m_ptr, R, dims->rms_eps, inv1, stream))
-    return hip_fail("rms launch");
+  // 1. RMSNorm statistics of the layer input (+ rotary positions)
+  {
+    seer::RopeArgs ra{};
+    ra.cu = cu_seqlens; ra.B = batch; ra.cu_kv = cu_kv; ra.pos = rpos; ra.freq = rfreq;
+    ra.theta = dims->rope_theta; ra.head_dim = dims->head_dim;
+    if (seer::launch_rms_inv(bf16, x_in, d, d, m_ptr, R, dims->rms_eps, inv1, stream, rope ? &ra : nullptr))
+      return hip_fail("rms launch");
+  }
   // 2. QKV projection, RMSNorm folded in as a row scale
   if (mark(1) != hipSuccess) return hip_fail("event record");
   {
@@ -193,7 +208,17 @@ static int layer_forward_impl(const seer_dims* dims, const void* w_packed, const
     g.m_ptr = m_ptr; g.m_ub = R; g.N = 3 * d; g.K = d;
     g.lda = d; g.ldb = d; g.ldc = 3 * d;
     g.f16_col0 = bf16 ? 2 * d : 0;     // V goes to the attention's fp16 PV product
+    if (rope && bf16) {
+      // q and k rotated in the epilogue; the rotary pairs need whole 256-wide
+      // tiles, so no split last round
+      g.rope_pos = rpos; g.rope_freq = rfreq; g.rope_col1 = 2 * d;
+      g.n_units = 0;
+    }
     if (gemm(seer::EPI_SCALE, g, stream)) return hip_fail("qkv gemm launch");
+    if (rope && !bf16 &&
+        seer::launch_rope_f32(static_cast<float*>(qkv), d, dims->n_heads, dims->head_dim, m_ptr, R, rpos, rfreq,
+                              stream))
+      return hip_fail("rope launch");
   }
   // 3. bidirectional varlen attention
   if (mark(2) != hipSuccess) return hip_fail("event record");

@@ -26,9 +26,9 @@ import torch
 from . import seer as S
 
 
-def dims_for(d_model, n_heads, head_dim, d_ff, dtype, rms_eps=1e-5):
+def dims_for(d_model, n_heads, head_dim, d_ff, dtype, rms_eps=1e-5, rope_theta=0.0):
     return S.seer_dims(d_model, n_heads, head_dim, d_ff,
-                       S.SEER_DTYPE_BF16 if dtype == "bf16" else S.SEER_DTYPE_F32, rms_eps)
+                       S.SEER_DTYPE_BF16 if dtype == "bf16" else S.SEER_DTYPE_F32, rms_eps, rope_theta)
 
 
 def torch_dtype(dtype):

@@ -34,7 +34,7 @@ class SeerError(RuntimeError):
 class seer_dims(ctypes.Structure):
     _fields_ = [("d_model", ctypes.c_int32), ("n_heads", ctypes.c_int32),
                 ("head_dim", ctypes.c_int32), ("d_ff", ctypes.c_int32),
-                ("dtype", ctypes.c_int32), ("rms_eps", ctypes.c_float)]
+                ("dtype", ctypes.c_int32), ("rms_eps", ctypes.c_float), ("rope_theta", ctypes.c_float)]
 
 
 class seer_layer_weights(ctypes.Structure):

@@ -34,7 +34,7 @@ def test_every_declared_symbol_is_exported(S):
     for n in names:
         assert hasattr(lib, n), n
     assert set(names) == set(S.EXPORTED)
-    assert S.seer_abi_version() == 100
+    assert S.seer_abi_version() == 101
 
 
 def dims(S, d=4096, h=32, dh=128, i=12288, dtype=1):
@@ -48,6 +48,17 @@ def test_dims_validation(S):
     assert S.seer_prepacked_bytes(dims(S, d=4000, h=32, dh=125)) == 0     # bf16 needs d % 256
     assert S.seer_prepacked_bytes(dims(S, d=256, h=4, dh=64, i=688, dtype=2)) > 0
     assert S.seer_prepacked_bytes(dims(S, dtype=7)) == 0
+    d = dims(S)
+    d.rope_theta = 500000.0
+    assert S.seer_prepacked_bytes(d) == 436207616
+    for bad in (0.5, 1.0, -1.0, float("inf"), float("nan")):
+        d.rope_theta = bad
+        assert S.seer_prepacked_bytes(d) == 0, bad
+        assert "rope_theta" in S.seer_last_error()
+    d = dims(S, d=260, h=4, dh=65, i=688, dtype=2)
+    assert S.seer_prepacked_bytes(d) > 0
+    d.rope_theta = 10000.0
+    assert S.seer_prepacked_bytes(d) == 0 and "even head_dim" in S.seer_last_error()
 
 
 def test_workspace_layout_is_consistent(S):

@@ -1,0 +1,157 @@
+"""GPU parity of the rotary embedding of q and k (seer_dims.rope_theta).
+
+Teacher-forced against the oracle (oracle.rope, oracle.layer with
+rope_theta):
+  * the rotated q | k columns of the QKV projection: the oracle projects the
+    GPU's own layer input and rotates in fp64 (fp32 bar 1e-5, bf16 bar 1e-2:
+    one rounding of the stored q, k);
+  * layer outputs of sampled rows of every sequence (fp32 1e-4, bf16 2e-2),
+    on the fp32 tiny layer, the bf16 ragged batch and the LLaDA-shaped B=1
+    layer (positions up to 1816);
+  * the cached-prefix step: prefix keys exported rotated, window rows at
+    positions P + i; equal to the full truncated step's window rows and to
+    the oracle's cached layer.
+"""
+import numpy as np
+import pytest
+
+from gpu_util import dev, host, log, rel_err, upload_weights, view_ws
+from oracle.kvcache import layer_forward_cached_rows
+from oracle.layer import layer_forward_rows, rms_norm
+from oracle.rope import apply_rope
+from workloads import WORKLOADS
+from workloads.generate import make_workload
+
+pytestmark = pytest.mark.gpu
+TOL = {"bf16": 2e-2, "f32": 1e-4}
+QK_TOL = {"bf16": 1e-2, "f32": 1e-5}
+THETA = {"tiny_f32": 10000.0, "small_bf16_ragged": 500000.0, "llada_b1": 500000.0, "small_bf16_stack": 10000.0}
+
+
+@pytest.fixture(scope="module")
+def S():
+    from paper_2607_14557_amd import seer
+    seer.load_library()
+    return seer
+
+
+def _stack(w, theta, max_rows, layers):
+    from paper_2607_14557_amd.runner import SeerStack, dims_for
+    sh = w.shape
+    dims = dims_for(sh.d_model, sh.n_heads, sh.head_dim, sh.d_ff, w.dtype, w.rms_eps, rope_theta=theta)
+    st = SeerStack(dims, len(layers), max_rows)
+    for l, W in enumerate(layers):
+        st.set_layer(l, upload_weights(W, w.dtype))
+    return st
+
+
+@pytest.mark.parametrize("name", ["tiny_f32", "small_bf16_ragged", "llada_b1"])
+def test_rope_layer(S, name):
+    import torch
+    w = WORKLOADS[name]
+    sh = w.shape
+    d, H, B = sh.d_model, sh.n_heads, w.batch
+    theta = THETA[name]
+    log("rope %s: inputs (theta %g)" % (name, theta))
+    layers, batch = make_workload(w)
+    T = w.rows_full
+    st = _stack(w, theta, T, layers[:1])
+    x = dev(batch.x, w.dtype)
+    cu = dev(batch.cu_seqlens)
+    y = torch.empty_like(x)
+    S.seer_layer_forward_varlen(st.dims, st.packed[0], x, y, T, cu, None, B, 0.0, None, st.workspace)
+    torch.cuda.synchronize()
+    off = S.seer_layer_workspace_offsets(st.dims, T)
+    qk = host(view_ws(st.workspace, off[0], T, 3 * d, w.dtype))[:, :2 * d]
+    yh, xh = host(y), host(x)
+    W = {k: np.asarray(v, np.float64) for k, v in layers[0].items()}
+    cu_h = np.asarray(batch.cu_seqlens, np.int64)
+    rng = np.random.default_rng(5)
+    worst_qk = worst_y = 0.0
+    for b in sorted({0, B // 2, B - 1}):
+        s0, s1 = int(cu_h[b]), int(cu_h[b + 1])
+        n = s1 - s0
+        rows = np.array(sorted({0, 1, n - 1} | set(int(i) for i in rng.integers(0, n, 5))))
+        a = rms_norm(xh[s0:s1][rows], W["g1"], w.rms_eps)
+        q_ref = apply_rope(a @ W["wq"].T, rows, H, theta)
+        k_ref = apply_rope(a @ W["wk"].T, rows, H, theta)
+        e_qk = max(rel_err(qk[s0 + rows, :d], q_ref), rel_err(qk[s0 + rows, d:], k_ref))
+        ref = layer_forward_rows(xh[s0:s1], n, W, H, w.rms_eps, rows, rope_theta=theta)["y"]
+        e_y = rel_err(yh[s0 + rows], ref)
+        log("  seq %d (%d rows): q|k rel err %.3e, y rel err %.3e over %d rows" % (b, n, e_qk, e_y, len(rows)))
+        worst_qk, worst_y = max(worst_qk, e_qk), max(worst_y, e_y)
+    assert worst_qk <= QK_TOL[w.dtype]
+    assert worst_y <= TOL[w.dtype]
+    # the embedding is really applied: the same layer without it differs
+    from paper_2607_14557_amd.runner import dims_for
+    d0 = dims_for(sh.d_model, sh.n_heads, sh.head_dim, sh.d_ff, w.dtype, w.rms_eps)
+    y0 = torch.empty_like(x)
+    S.seer_layer_forward_varlen(d0, st.packed[0], x, y0, T, cu, None, B, 0.0, None, st.workspace)
+    torch.cuda.synchronize()
+    assert rel_err(host(y0), yh) > 1e-3
+
+
+def test_rope_cached_step(S):
+    import torch
+    name = "small_bf16_stack"
+    w = WORKLOADS[name]
+    sh = w.shape
+    d, H, B, L = sh.d_model, sh.n_heads, w.batch, w.n_layers
+    theta = THETA[name]
+    layers, batch = make_workload(w)
+    granule = 256
+    T = w.rows_full
+    cap = ((T + granule - 1) // granule) * granule + granule
+    st = _stack(w, theta, cap, layers)
+    x = dev(batch.x, w.dtype)
+    cu, off, wl = dev(batch.cu_seqlens), dev(batch.win_off), dev(batch.win_len)
+    keep = np.minimum(batch.planted + 1, batch.win_len).astype(np.int64)
+    kp = dev(keep)
+    P = np.asarray(batch.win_off, np.int64)
+    log("rope cached %s: full truncated step + export" % name)
+    x_t = torch.empty(cap, d, dtype=st.dtype, device="cuda")
+    cu_t = torch.empty(B + 1, dtype=torch.int32, device="cuda")
+    used_t = torch.empty(B, dtype=torch.int32, device="cuda")
+    route_t = torch.empty(B, 3, dtype=torch.int32, device="cuda")
+    desc = S.seer_repack_desc(S.SEER_ROUTE_HYBRID, 1, 5, granule, d * 2, cap, 0, 0)
+    S.seer_batch_repack(desc, [x], [x_t], cu, off, wl, kp, B, cu_t, used_t, route_t)
+    cu_kv_h = np.concatenate([[0], np.cumsum(P)]).astype(np.int64)
+    kv_rows = int(cu_kv_h[-1])
+    cu_kv = dev(cu_kv_h)
+    caches = st.alloc_kv_caches(kv_rows)
+    y_full = st.forward_export(x_t, cu_t, used_t, B, cap, caches, cu_kv, kv_rows,
+                               out=torch.empty_like(x_t))
+    x_w, cu_w, used_w, _ = st.window_rows(x, cu, off, wl, kp, B, cap, granule=granule)
+    log("rope cached %s: cached step" % name)
+    ins = [x_w.clone()]
+    cur = x_w.clone()
+    for l in range(L):
+        nxt = torch.empty_like(cur)
+        S.seer_layer_forward_cached(st.dims, st.packed[l], cur, nxt, cap, cu_w, used_w, B, caches[l], cu_kv,
+                                    kv_rows, st.workspace)
+        ins.append(nxt)
+        cur = nxt
+    torch.cuda.synchronize()
+    cu_t_h, cu_w_h = host(cu_t), host(cu_w)
+    yf, yc = host(y_full), host(cur)
+    worst = 0.0
+    for b in range(B):
+        a = yf[cu_t_h[b] + P[b]:cu_t_h[b] + P[b] + keep[b]]
+        c = yc[cu_w_h[b]:cu_w_h[b] + keep[b]]
+        worst = max(worst, rel_err(c, a))
+    log("  cached vs full step, window rows: max rel diff %.3e" % worst)
+    assert worst <= TOL["bf16"]
+    # teacher-forced: layer 0 and the last layer of the first and last sequence
+    for l in sorted({0, L - 1}):
+        W = {k: np.asarray(v, np.float64) for k, v in layers[l].items()}
+        kc = caches[l][:, :d].float().cpu().numpy().astype(np.float64)
+        vc = caches[l][:, d:].contiguous().view(torch.float16).float().cpu().numpy().astype(np.float64)
+        for b in sorted({0, B - 1}):
+            r0, n = int(cu_w_h[b]), int(cu_w_h[b + 1] - cu_w_h[b])
+            rows = np.array(sorted({0, int(keep[b]) - 1, n - 1}))
+            ref = layer_forward_cached_rows(host(ins[l][r0:r0 + n]), int(keep[b]), kc[cu_kv_h[b]:cu_kv_h[b + 1]],
+                                            vc[cu_kv_h[b]:cu_kv_h[b + 1]], W, H, w.rms_eps, rows=rows,
+                                            rope_theta=theta)["y"]
+            e = rel_err(host(ins[l + 1][r0:r0 + n])[rows], ref)
+            log("  layer %d seq %d: rel err %.3e" % (l, b, e))
+            assert e <= TOL["bf16"]
