@@ -148,7 +148,7 @@ def bench_stack(args, w):
     T = w.rows_full
     granule = 256
     cap = ((T + granule - 1) // granule) * granule + granule
-    dims = dims_for(d, sh.n_heads, sh.head_dim, I, "bf16", w.rms_eps)
+    dims = dims_for(d, sh.n_heads, sh.head_dim, I, "bf16", w.rms_eps, rope_theta=args.rope)
     st = SeerStack(dims, L, cap)
     for l in range(L):
         Wl = layer_weights_torch(w, l, dev)
@@ -261,12 +261,31 @@ def bench_stack(args, w):
         t_cached = timed(lambda: st.forward_cached(x_w, cu_w, used_w, B, max(rows_w, 1), kv[0], kv[1], kv[2],
                                                    stream=sp))
     t_graph = {}
+    host_ms = {}
     if args.graph:
         log("timing one replay of each recorded step")
         if kv is None:
-            t_graph["trunc"] = timed(lambda: graphs["trunc"].run(r.routed["capacity_rows"]))
+            eager_fn = lambda: st.forward(r.x_trunc, r.cu_trunc, r.seqused, B, r.rows_ub, stream=sp)
+            graph_fn = lambda: graphs["trunc"].run(r.routed["capacity_rows"])
+            t_graph["trunc"] = timed(graph_fn)
         else:
-            t_graph["cached"] = timed(lambda: graphs["cached"].run(r.cached[3]))
+            x_w, cu_w, used_w, rows_w = r.cached
+            eager_fn = lambda: st.forward_cached(x_w, cu_w, used_w, B, rows_w, kv[0], kv[1], kv[2], stream=sp)
+            graph_fn = lambda: graphs["cached"].run(rows_w)
+            t_graph["cached"] = timed(graph_fn)
+
+        # host time to enqueue one step (the GPU is idle at the start of each)
+        def enqueue_ms(fn, reps=5):
+            best = None
+            for _ in range(reps):
+                torch.cuda.synchronize()
+                t0 = time.perf_counter()
+                fn()
+                dt = (time.perf_counter() - t0) * 1e3
+                best = dt if best is None else min(best, dt)
+            torch.cuda.synchronize()
+            return best
+        host_ms = {"eager": enqueue_ms(eager_fn), "graph": enqueue_ms(graph_fn)}
     # the dominant kernel: gate/up GEMM of a truncated step, timed inside one layer
     ev = [hip.event() for _ in range(8)]
     y = torch.empty(cap, d, dtype=torch.bfloat16, device=dev)
@@ -286,7 +305,8 @@ def bench_stack(args, w):
         "warmup": args.warmup, "ms_per_step": round(ms_job, 3), "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
         "data": "synthetic (seeded; random-init LLaDA-8B-shaped %d-layer stack, planted EOS suffixes)" % L,
-        "config": {"workload": w.name, "batch": B, "visual_prefix": w.n_visual, "prompt": w.n_prompt,
+        "config": {"workload": w.name, "rope_theta": args.rope, "batch": B, "visual_prefix": w.n_visual,
+                   "prompt": w.n_prompt,
                    "window": w.window, "layers": L, "detection_layer": w.l_det,
                    "denoising_steps_per_job": n_den, "sum_keep_len": int(keep.sum()), "rows_full": T,
                    "rows_trunc": rows_t, "d_model": d, "heads": sh.n_heads, "head_dim": sh.head_dim,
@@ -304,6 +324,8 @@ def bench_stack(args, w):
         "trunc_step_ms_graph": round(t_graph["trunc"], 3) if "trunc" in t_graph else None,
         "cached_step_ms_graph": round(t_graph["cached"], 3) if "cached" in t_graph else None,
         "graph_shapes": {k: sorted(g.graphs) for k, g in graphs.items()} if args.graph else None,
+        "host_enqueue_ms_eager": round(host_ms["eager"], 3) if host_ms else None,
+        "host_enqueue_ms_graph": round(host_ms["graph"], 3) if host_ms else None,
         "cpu_baseline": None,
         "cpu_baseline_note": "one oracle step of a 32-layer stack takes hours; the default workload's line "
                              "carries the CPU baseline",
@@ -328,6 +350,8 @@ def main():
                     help="skip the separate untruncated-step and cached-prefix-step timings (they "
                          "launch the gate/up GEMM kernel at other sizes, which a per-kernel profile "
                          "would mix in)")
+    ap.add_argument("--rope", type=float, default=0.0,
+                    help="rotary embedding of q and k with this theta (0: none, the paper's layer)")
     ap.add_argument("--graph", action="store_true",
                     help="32-layer stacks: the host polls the pinned control word of each repack and "
                          "replays the truncated (or cached) steps from HIP graphs recorded per 1-D graph "
@@ -375,7 +399,7 @@ def main():
     layers, batch = make_workload(w)
     log("  inputs ready in %.1f s" % (time.perf_counter() - t0))
     dev = torch.device("cuda:0")
-    dims = dims_for(d, sh.n_heads, sh.head_dim, I, "bf16", w.rms_eps)
+    dims = dims_for(d, sh.n_heads, sh.head_dim, I, "bf16", w.rms_eps, rope_theta=args.rope)
     T = w.rows_full
     granule = 256
     cap = ((T + granule - 1) // granule) * granule
@@ -551,7 +575,7 @@ def main():
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
         "data": "synthetic (seeded; random-init LLaDA-8B-shaped layer, planted EOS suffixes)",
-        "config": {"workload": w.name, "batch": w.batch, "visual_prefix": w.n_visual,
+        "config": {"workload": w.name, "rope_theta": args.rope, "batch": w.batch, "visual_prefix": w.n_visual,
                    "prompt": w.n_prompt, "window": w.window, "layers": w.n_layers,
                    "d_model": d, "heads": sh.n_heads, "head_dim": sh.head_dim, "d_ff": I,
                    "policy": args.policy, "denoising_steps_per_bench_step": 2,
@@ -583,11 +607,13 @@ def main():
         torch.neg(a, out=b)
         torch.cuda.synchronize()
         del a, b
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and not args.rope:
         log("CPU baseline (oracle on host cores)")
         out["cpu_baseline"] = cpu_baseline(w, layers, batch, args.cpu_seconds)
     else:
         out["cpu_baseline"] = None
+        if args.rope:
+            out["cpu_baseline_note"] = "the CPU baseline is taken on the layer without rotary embedding"
     print(json.dumps(out), flush=True)
 
 
