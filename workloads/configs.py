@@ -50,6 +50,11 @@ class Workload:
     noise_std: float = 0.01    # std of the per-position noise added to the EOS vector
     weight_std: float = 0.02
     rms_eps: float = 1e-5
+    # confounders for the detector-sensitivity sweeps: (runs per sequence, longest
+    # run) of content positions replaced by EOS rows before the planted boundary
+    dips: Tuple[int, int] = (0, 0)
+    # layers whose gate/up weights define the planted EOS direction (None: l_det)
+    eos_layers: Optional[Tuple[int, ...]] = None
 
     @property
     def prefix_len(self) -> int:
@@ -122,6 +127,22 @@ WORKLOADS["small_bf16_stack"] = Workload(
     name="small_bf16_stack", shape=SMALL_BF16, n_layers=3, l_det=1, batch=3,
     n_visual=150, n_prompt=20, window=200, dtype="bf16",
     boundary=("uniform", 20, 180), seed=707, act_eps=act_eps_for(SMALL_BF16))
+
+# Detector-sensitivity sweeps (look-ahead, tau_jump x gamma, detection layer):
+# six layers with the EOS direction planted at layer 3, EOS rows with strong
+# per-position noise (a noisy padding plateau), and up to two runs of one or
+# two EOS rows inside the content, which a look-ahead of 2 mistakes for the
+# boundary.
+WORKLOADS["sweep_small"] = Workload(
+    name="sweep_small", shape=SMALL_BF16, n_layers=6, l_det=3, batch=64,
+    n_visual=64, n_prompt=16, window=256, dtype="bf16",
+    boundary=("uniform", 24, 224), seed=808, act_eps=act_eps_for(SMALL_BF16),
+    noise_std=10.0, dips=(2, 2))
+WORKLOADS["sweep_llada"] = Workload(
+    name="sweep_llada", shape=LLADA8B, n_layers=6, l_det=3, batch=32,
+    n_visual=256, n_prompt=32, window=512, dtype="bf16",
+    boundary=("uniform", 32, 448), seed=909, act_eps=act_eps_for(LLADA8B),
+    noise_std=10.0, dips=(2, 2))
 
 WORKLOAD_ORDER = ["tiny_f32", "llada_b1", "llada_b16_ragged",
                   "llada32_multicrop_b8", "llada32_video_b4"]

@@ -13,11 +13,15 @@ Recipe (one base seed per workload, split into independent streams):
   * window positions before the planted boundary b ~ N(0, 1) per element;
   * window positions >= b: one shared EOS vector plus N(0, 0.01^2) noise;
   * planted b fixed, log-uniform (b = round(exp(U(ln lo, ln hi)))) or uniform
-    integer in [lo, hi] per sequence.
+    integer in [lo, hi] per sequence;
+  * optional confounders (sweep workloads): up to n runs per sequence of
+    1..r content positions replaced by EOS rows (same vector and noise),
+    starting at position >= 1 and ending >= 2 positions before b, disjoint.
 
 The shared EOS vector is e = A * sqrt(d) * v, where v is the unit eigenvector of
-the smallest eigenvalue of Wg^T Wg + Wu^T Wu of the detection layer (the input
-direction the SwiGLU amplifies least), with the sign fixed so that its largest
+the smallest eigenvalue of Wg^T Wg + Wu^T Wu of the detection layer, summed over
+several layers for the sweep workloads (the input direction the SwiGLU
+amplifies least), with the sign fixed so that its largest
 magnitude component is positive.  With random weights every other input
 direction has the same expected activation statistics, so a generic EOS vector
 plants no boundary; the least-amplified direction makes the suffix rows'
@@ -25,7 +29,7 @@ activations cluster near zero, which is the behaviour the method relies on for
 padding tokens (Sec. 1 and Sec. 3.2).
 """
 from dataclasses import dataclass
-from typing import List, Optional
+from typing import List, Optional, Tuple
 
 import numpy as np
 
@@ -53,9 +57,9 @@ def weight_shapes(w: Workload):
 
 def _streams(w: Workload):
     ss = np.random.SeedSequence(w.seed)
-    kids = ss.spawn(6)
+    kids = ss.spawn(7)
     return {"weights": kids[0], "boundary": kids[1], "visual": kids[2],
-            "prompt": kids[3], "content": kids[4], "noise": kids[5]}
+            "prompt": kids[3], "content": kids[4], "noise": kids[5], "dips": kids[6]}
 
 
 def layer_weights(w: Workload, layer: int) -> dict:
@@ -95,17 +99,23 @@ def layer_weights_torch(w: Workload, layer: int, device):
     return out
 
 
-def eos_vector(wg: np.ndarray, wu: np.ndarray, amplitude: float, dtype: str) -> np.ndarray:
-    """The planted EOS embedding: least SwiGLU-amplified direction, scaled."""
-    import scipy.linalg
+def gate_up_gram(wg: np.ndarray, wu: np.ndarray) -> np.ndarray:
     g = wg.astype(np.float64)
     u = wu.astype(np.float64)
-    gram = g.T @ g + u.T @ u
+    return g.T @ g + u.T @ u
+
+
+def eos_vector(wg: np.ndarray, wu: np.ndarray, amplitude: float, dtype: str, gram=None) -> np.ndarray:
+    """The planted EOS embedding: least SwiGLU-amplified direction, scaled.
+    ``gram`` (optional) replaces Wg^T Wg + Wu^T Wu, e.g. summed over layers."""
+    import scipy.linalg
+    if gram is None:
+        gram = gate_up_gram(wg, wu)
+    d = gram.shape[0]
     _, vecs = scipy.linalg.eigh(gram, subset_by_index=[0, 0])
     v = vecs[:, 0]
     if v[np.argmax(np.abs(v))] < 0:
         v = -v
-    d = wg.shape[1]
     return round_to_dtype(amplitude * np.sqrt(d) * v, dtype)
 
 
@@ -136,6 +146,7 @@ class Batch:
     win_len: np.ndarray      # [B] int32
     planted: np.ndarray      # [B] int64 planted boundary (first EOS position)
     eos: np.ndarray          # [d] float32
+    dips: Optional[List[List[Tuple[int, int]]]] = None   # per sequence: (start, length) window positions
 
 
 def make_batch(w: Workload, eos: np.ndarray) -> Batch:
@@ -146,6 +157,8 @@ def make_batch(w: Workload, eos: np.ndarray) -> Batch:
     rp = np.random.default_rng(st["prompt"])
     rc = np.random.default_rng(st["content"])
     rn = np.random.default_rng(st["noise"])
+    rd = np.random.default_rng(st["dips"])
+    dips = []
     S = w.seq_len_full
     x = np.empty((w.batch * S, d), np.float32)
     for b in range(w.batch):
@@ -159,12 +172,26 @@ def make_batch(w: Workload, eos: np.ndarray) -> Batch:
         n_eos = w.window - nb
         noise = rn.standard_normal((n_eos, d), dtype=np.float32) * np.float32(w.noise_std)
         x[r2 + nb:r2 + w.window] = eos[None, :] + noise
+        runs = []
+        n_runs, max_len = w.dips
+        for _ in range(n_runs):
+            ln = int(rd.integers(1, max_len + 1))
+            last = nb - 2 - ln                 # the run ends >= 2 positions before b
+            if last < 1:
+                continue
+            st0 = int(rd.integers(1, last + 1))
+            if any(st0 < s1 + l1 + 1 and s1 < st0 + ln + 1 for s1, l1 in runs):
+                continue                       # keep runs disjoint and apart
+            dn = rd.standard_normal((ln, d), dtype=np.float32) * np.float32(w.noise_std)
+            x[r2 + st0:r2 + st0 + ln] = eos[None, :] + dn
+            runs.append((st0, ln))
+        dips.append(sorted(runs))
     x = round_to_dtype(x, w.dtype)
     cu = (np.arange(w.batch + 1, dtype=np.int64) * S).astype(np.int32)
     win_off = np.full(w.batch, w.prefix_len, np.int32)
     win_len = np.full(w.batch, w.window, np.int32)
     return Batch(x=x, cu_seqlens=cu, win_off=win_off, win_len=win_len,
-                 planted=planted, eos=eos)
+                 planted=planted, eos=eos, dips=dips)
 
 
 def make_stack_batch(w: Workload, device) -> Batch:
@@ -174,11 +201,15 @@ def make_stack_batch(w: Workload, device) -> Batch:
     and up weights (read back to the host), so the planted suffix matches the
     weights the stack actually runs with.
     """
-    det = layer_weights_torch(w, w.l_det, device)
-    wg = det["wg"].float().cpu().numpy()
-    wu = det["wu"].float().cpu().numpy()
-    del det
-    return make_batch(w, eos_vector(wg, wu, w.eos_amplitude, w.dtype))
+    gram = None
+    for l in (w.eos_layers or (w.l_det,)):
+        det = layer_weights_torch(w, l, device)
+        g = det["wg"].double()
+        u = det["wu"].double()
+        gl = (g.T @ g + u.T @ u).cpu().numpy()
+        gram = gl if gram is None else gram + gl
+        del det, g, u
+    return make_batch(w, eos_vector(None, None, w.eos_amplitude, w.dtype, gram=gram))
 
 
 def make_workload(w: Workload, with_weights: bool = True):
@@ -188,6 +219,10 @@ def make_workload(w: Workload, with_weights: bool = True):
     shapes); the stacks draw weights on the device (layer_weights_torch).
     """
     layers: List[dict] = [layer_weights(w, l) for l in range(w.n_layers)] if with_weights else []
-    det = layers[w.l_det] if with_weights else layer_weights(w, w.l_det)
-    eos = eos_vector(det["wg"], det["wu"], w.eos_amplitude, w.dtype)
+    gram = None
+    for l in (w.eos_layers or (w.l_det,)):
+        det = layers[l] if with_weights else layer_weights(w, l)
+        gl = gate_up_gram(det["wg"], det["wu"])
+        gram = gl if gram is None else gram + gl
+    eos = eos_vector(None, None, w.eos_amplitude, w.dtype, gram=gram)
     return layers, make_batch(w, eos)
