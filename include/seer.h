@@ -19,6 +19,8 @@
  *   seer_layer_forward_cached  prefix keys/values cached (Appendix D)
  *   seer_graph_*               record a launch sequence once, replay it
  *                              (graph-compatible paths, Sec. 3.5)
+ *   seer_lm_head_predict,      synthetic LM head (argmax + confidence) and
+ *   seer_remask_step           low-confidence remasking between steps
  *
  * Conventions shared by every call:
  *   - Buffers are owned by the caller.  Pointers are device pointers unless a
@@ -316,6 +318,40 @@ int seer_batch_repack(const seer_repack_desc* desc, const void* const* src,
                       const int32_t* keep_len, int32_t batch, int32_t* cu_dst,
                       int32_t* seqused, int32_t* route, seer_route_ctrl* ctrl_dev,
                       seer_route_ctrl* ctrl_host, hipStream_t stream);
+
+/* ---- synthetic LM head and remasking sampler -----------------------------
+ * Makes synthetic denoising steps differ (Sec. 3.1: every step predicts all
+ * masked positions at once).  The paper leaves the sampler to its backbones;
+ * this follows the low-confidence remasking of the LLaDA family with a random
+ * head.  bf16 layers only.
+ *
+ * seer_lm_head_predict: for rows r < cu_seqlens[batch] of x [rows_ub, d]:
+ * logits l = RMSNorm(x_r) (unit gain, dims->rms_eps) . w_lm^T, w_lm [vocab, d]
+ * bf16 ([out, in]); pred[r] = argmax_v l_v (the smallest v among equal
+ * maxima), conf[r] = its softmax probability 1 / sum_v exp(l_v - l_max).
+ * Logits are fp32 (bf16 products, fp32 accumulation) and never stored: the
+ * GEMM epilogue keeps a {max, sum exp, argmax} partial per row and 128
+ * columns, merged by a second kernel.  vocab % 256 == 0.  Workspace: at
+ * least seer_lm_head_workspace_bytes(dims, vocab, rows_ub), 256-byte aligned.
+ * Errors: EINVAL (null pointers, sizes < 1, alignment), EUNSUPPORTED (fp32,
+ * vocab), EWORKSPACE.
+ *
+ * seer_remask_step: per sequence b (rows [cu_seqlens[b], cu_seqlens[b+1]), the
+ * first min(seqused[b], max_used) of them real; seqused may be NULL): among
+ * the real positions with tokens[r] == -1 (masked), n of them, commit the
+ * k = ceil(n / steps_left) with the largest conf (ties to the smaller
+ * position): tokens[r] = pred[r] (clamped to [0, vocab)).  Then write every
+ * row of the sequence to x_next: emb[tokens[r]] if committed, the x0 row if
+ * still masked, zero past the real rows.  x_next may alias x0 (a committed
+ * row's x0 row is never read again).  max_used <= 8192.  Errors: EINVAL,
+ * EUNSUPPORTED (fp32, max_used). */
+size_t seer_lm_head_workspace_bytes(const seer_dims* dims, int32_t vocab, int32_t rows_ub);
+int seer_lm_head_predict(const seer_dims* dims, const void* w_lm, int32_t vocab, const void* x, int32_t rows_ub,
+                         const int32_t* cu_seqlens, int32_t batch, int32_t* pred, float* conf, void* workspace,
+                         size_t workspace_bytes, hipStream_t stream);
+int seer_remask_step(const seer_dims* dims, const int32_t* cu_seqlens, const int32_t* seqused, int32_t batch,
+                     int32_t max_used, int32_t steps_left, const int32_t* pred, const float* conf, int32_t* tokens,
+                     const void* x0, const void* emb, int32_t vocab, void* x_next, hipStream_t stream);
 
 /* ---- recorded launch sequences (Sec. 3.5) -------------------------------
  * The graph-compatible execution paths replay a fixed launch sequence.  Every

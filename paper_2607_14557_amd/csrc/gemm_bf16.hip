@@ -304,7 +304,7 @@ __device__ __forceinline__ void gemm_tile(const GemmParams& p, uint8_t* smem, in
   for (int i = 0; i < 4; ++i) {
     int row = m0 + wm * 128 + i * 32 + fr;
     row = row < M ? row : M - 1;
-    rsv[i] = (EPI == EPI_SCALE || kGlu) ? p.rs[row] : 1.0f;
+    rsv[i] = (EPI == EPI_SCALE || EPI == EPI_ARGMAX || kGlu) ? p.rs[row] : 1.0f;
   }
   if constexpr (kRes) {
 #pragma unroll
@@ -457,6 +457,37 @@ __device__ __forceinline__ void gemm_tile(const GemmParams& p, uint8_t* smem, in
         nz += __shfl_xor(nz, 32, kWave);
         if (ok && fhalf == 0) atomicAdd(p.cnt + row, nz);
       }
+    } else if constexpr (EPI == EPI_ARGMAX) {
+      // the lane's 64 columns of its row in increasing order, so a strict >
+      // keeps the smallest column among equal maxima; then the lane pair
+      const float sc = rsv[i];
+      const int cb = n0 + wn * (BN / 2) + cq;
+      float m = -INFINITY;
+      int a = cb;
+#pragma unroll
+      for (int j = 0; j < NJ; ++j)
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const float v = acc[i][j][4 * q + e] * sc;
+            if (v > m) { m = v; a = cb + 32 * j + 8 * q + e; }
+          }
+      float sum = 0.0f;
+#pragma unroll
+      for (int j = 0; j < NJ; ++j)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) sum += __expf(acc[i][j][r] * sc - m);
+      const float m2 = __shfl_xor(m, 32, kWave);
+      const float s2 = __shfl_xor(sum, 32, kWave);
+      const int a2 = __shfl_xor(a, 32, kWave);
+      const float mm = fmaxf(m, m2);
+      const float st = sum * __expf(m - mm) + s2 * __expf(m2 - mm);
+      const int at = (m2 > m || (m2 == m && a2 < a)) ? a2 : a;
+      if (ok && fhalf == 0) {
+        ArgmaxPartial* dst = static_cast<ArgmaxPartial*>(p.C) + (size_t)row * p.ldc + (n0 + wn * (BN / 2)) / 128;
+        *reinterpret_cast<u32x4_t*>(dst) = u32x4_t{__float_as_uint(mm), __float_as_uint(st), (uint32_t)at, 0u};
+      }
     } else {
       if constexpr (kRope) {
         if (rope_on) rope_block(i);
@@ -506,8 +537,10 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmParams p) {
 }
 
 int launch_gemm_bf16(int epi, const GemmParams& p, hipStream_t s) {
-  // the rotary pairs of a head span both column halves of a 256x128 unit
+  // the rotary pairs of a head span both column halves of a 256x128 unit, and
+  // the argmax partials are per 128 columns of a 256-wide tile
   if (p.rope_pos && (epi != EPI_SCALE || p.n_units > 0 || p.rope_col1 % 128 != 0)) return -1;
+  if (epi == EPI_ARGMAX && p.n_units > 0) return -1;
   const int tiles_m = (p.m_ub + BM - 1) / BM;
   const int tiles_n = p.N / 256;
   // the split last round adds at most n_units / 2 units
@@ -522,6 +555,7 @@ int launch_gemm_bf16(int epi, const GemmParams& p, hipStream_t s) {
       hipLaunchKernelGGL(gemm_bf16_kernel<EPI_RESID_SPLIT>, grid, block, 0, s, p); break;
     case EPI_RESID_PAIR:
       hipLaunchKernelGGL(gemm_bf16_kernel<EPI_RESID_PAIR>, grid, block, 0, s, p); break;
+    case EPI_ARGMAX: hipLaunchKernelGGL(gemm_bf16_kernel<EPI_ARGMAX>, grid, block, 0, s, p); break;
     default: return -1;
   }
   return hipGetLastError() == hipSuccess ? 0 : -1;

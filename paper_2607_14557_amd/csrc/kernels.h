@@ -8,10 +8,21 @@ namespace seer {
 
 // SCALE: C = acc * rs[r]; RESID: C = R + acc; SWIGLU(_COUNT): gate/up pairs;
 // RESID_SPLIT: v = R + acc, C = bf16(v), C2 = bf16(v - C) (bf16 only);
-// RESID_PAIR: C = bf16(R + R2 + acc) (bf16 only).
+// RESID_PAIR: C = bf16(R + R2 + acc) (bf16 only);
+// ARGMAX: no output matrix; per row and 128-column block of l = acc * rs[r],
+// the partial {max, sum exp(l - max), argmax column} (bf16 only, see
+// ArgmaxPartial).
 enum Epilogue {
   EPI_SCALE = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_SWIGLU_COUNT = 3,
-  EPI_RESID_SPLIT = 4, EPI_RESID_PAIR = 5
+  EPI_RESID_SPLIT = 4, EPI_RESID_PAIR = 5, EPI_ARGMAX = 6
+};
+
+// One row's partial over 128 columns (EPI_ARGMAX): C is ArgmaxPartial[M][N/128].
+struct ArgmaxPartial {
+  float max;
+  float sum;     // sum of exp(l - max) over the block
+  int arg;       // smallest column reaching max
+  int pad;
 };
 
 // C[M,N] = A[M,K] * B[N,K]^T with a fused epilogue.  M is read on the device
@@ -155,6 +166,33 @@ struct KvExportParams {
   int rows_ub;          // rows of the qkv region
 };
 int launch_kv_export(const KvExportParams& p, int kv_rows_ub, hipStream_t s);
+
+// Per row r < M (M from m_ptr): merge the n_part ArgmaxPartial entries into
+// the prediction (smallest column among equal maxima) and its softmax
+// probability 1 / sum_p sum_p exp(max_p - max).
+int launch_argmax_reduce(const void* partials, int n_part, const int* m_ptr, int m_ub, int* pred, float* conf,
+                         hipStream_t s);
+
+// Remasking step, one workgroup per sequence (rows [cu[b], cu[b+1]), the
+// first used[b] real): commit the ceil(n / steps_left) most confident masked
+// positions (tokens == -1), ties to the smaller position, then write the next
+// input rows: emb[token] if committed, x0 row if masked, zero past used.
+struct RemaskParams {
+  const int* cu;
+  const int* used;
+  int B;
+  int max_used;          // bound on used[b] (clamps it)
+  int steps_left;
+  const int* pred;
+  const float* conf;
+  int* tokens;
+  const uint16_t* x0;    // [rows, d] bf16
+  const uint16_t* emb;   // [vocab, d] bf16
+  int vocab;
+  uint16_t* x_next;      // [rows, d] bf16
+  int d;
+};
+int launch_remask(const RemaskParams& p, hipStream_t s);
 
 struct PrepackParams {
   const void* wq; const void* wk; const void* wv; const void* wo;

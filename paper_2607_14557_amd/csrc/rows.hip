@@ -428,4 +428,124 @@ int launch_prepack(const PrepackParams& p, hipStream_t s) {
   return hipGetLastError() == hipSuccess ? 0 : -1;
 }
 
+// ---------------------------------------------------------------------------
+// LM-head prediction: one wave per row merges the row's 128-column partials
+// in column order (a strict > keeps the smallest column among equal maxima).
+__global__ __launch_bounds__(256) void argmax_reduce_kernel(const ArgmaxPartial* part, int n_part, const int* m_ptr,
+                                                            int m_ub, int* pred, float* conf) {
+  const int M = rows_from(m_ptr, m_ub);
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (row >= M) return;
+  const ArgmaxPartial* pr = part + (size_t)row * n_part;
+  float m = -INFINITY, sum = 0.0f;
+  int a = 0x7fffffff;
+  for (int k = lane; k < n_part; k += 64) {
+    const ArgmaxPartial v = pr[k];
+    if (v.max > m) {
+      sum = sum * __expf(m - v.max) + v.sum;
+      m = v.max;
+      a = v.arg;
+    } else {
+      sum += v.sum * __expf(v.max - m);
+    }
+  }
+  // lanes hold disjoint column sets: merge by (max desc, column asc)
+  for (int off = 32; off > 0; off >>= 1) {
+    const float m2 = __shfl_xor(m, off, 64);
+    const float s2 = __shfl_xor(sum, off, 64);
+    const int a2 = __shfl_xor(a, off, 64);
+    const float mm = fmaxf(m, m2);
+    const float e1 = m == -INFINITY ? 0.0f : __expf(m - mm);
+    const float e2 = m2 == -INFINITY ? 0.0f : __expf(m2 - mm);
+    const int at = (m2 > m || (m2 == m && a2 < a)) ? a2 : a;
+    sum = sum * e1 + s2 * e2;
+    m = mm;
+    a = at;
+  }
+  if (lane == 0) {
+    pred[row] = a;
+    conf[row] = 1.0f / sum;
+  }
+}
+
+int launch_argmax_reduce(const void* partials, int n_part, const int* m_ptr, int m_ub, int* pred, float* conf,
+                         hipStream_t s) {
+  dim3 grid((m_ub + 3) / 4), block(256);
+  hipLaunchKernelGGL(argmax_reduce_kernel, grid, block, 0, s, static_cast<const ArgmaxPartial*>(partials), n_part,
+                     m_ptr, m_ub, pred, conf);
+  return hipGetLastError() == hipSuccess ? 0 : -1;
+}
+
+// ---------------------------------------------------------------------------
+// Remasking step: one workgroup of 256 per sequence.  A masked position's
+// rank is the number of masked positions with a larger (confidence, -position)
+// key; the k = ceil(n / steps_left) of rank < k are committed.  Keys are
+// unique, so the selection is exact and independent of the thread order.
+constexpr int kRemaskPerThread = 32;   // up to 8192 positions per sequence
+
+__global__ __launch_bounds__(256) void remask_kernel(RemaskParams p) {
+  const int b = blockIdx.x;
+  const int tid = threadIdx.x;
+  const int r0 = p.cu[b];
+  const int rows = p.cu[b + 1] - r0;
+  int used = p.used ? p.used[b] : rows;
+  used = used < 0 ? 0 : (used > rows ? rows : used);
+  used = used > p.max_used ? p.max_used : used;
+  __shared__ int s_cnt;
+  if (tid == 0) s_cnt = 0;
+  __syncthreads();
+  int local = 0;
+  for (int i = tid; i < used; i += 256) local += p.tokens[r0 + i] < 0;
+  if (local) atomicAdd(&s_cnt, local);
+  __syncthreads();
+  const int n = s_cnt;
+  const int k = p.steps_left <= 1 ? n : (n + p.steps_left - 1) / p.steps_left;
+  // decisions first (every thread reads the step's token state), then commits
+  bool commit[kRemaskPerThread];
+#pragma unroll
+  for (int t = 0; t < kRemaskPerThread; ++t) {
+    const int i = tid + 256 * t;
+    commit[t] = false;
+    if (i >= used || p.tokens[r0 + i] >= 0 || k == 0) continue;
+    const float ci = p.conf[r0 + i];
+    int rank = 0;
+    for (int j = 0; j < used && rank < k; ++j) {
+      if (p.tokens[r0 + j] >= 0) continue;
+      const float cj = p.conf[r0 + j];
+      rank += (cj > ci) || (cj == ci && j < i);
+    }
+    commit[t] = rank < k;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int t = 0; t < kRemaskPerThread; ++t) {
+    const int i = tid + 256 * t;
+    if (commit[t]) {
+      int tok = p.pred[r0 + i];
+      tok = tok < 0 ? 0 : (tok >= p.vocab ? p.vocab - 1 : tok);
+      p.tokens[r0 + i] = tok;
+    }
+  }
+  __syncthreads();
+  // next input rows, 16-byte chunks
+  const int chunks = p.d >> 3;
+  for (int c = tid; c < rows * chunks; c += 256) {
+    const int i = c / chunks, ch = c % chunks;
+    uint4 v = make_uint4(0u, 0u, 0u, 0u);
+    if (i < used) {
+      const int tok = p.tokens[r0 + i];
+      const uint16_t* src = tok >= 0 ? p.emb + (size_t)tok * p.d : p.x0 + (size_t)(r0 + i) * p.d;
+      v = reinterpret_cast<const uint4*>(src)[ch];
+    }
+    reinterpret_cast<uint4*>(p.x_next + (size_t)(r0 + i) * p.d)[ch] = v;
+  }
+}
+
+int launch_remask(const RemaskParams& p, hipStream_t s) {
+  if (p.max_used > 256 * kRemaskPerThread || p.d % 8 != 0) return -1;
+  hipLaunchKernelGGL(remask_kernel, dim3(p.B), dim3(256), 0, s, p);
+  return hipGetLastError() == hipSuccess ? 0 : -1;
+}
+
 }  // namespace seer

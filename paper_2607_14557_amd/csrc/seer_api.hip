@@ -399,6 +399,66 @@ int seer_batch_repack(const seer_repack_desc* desc, const void* const* src, void
   return ok();
 }
 
+// ---- synthetic LM head and remasking sampler --------------------------------
+
+static size_t lm_partials_offset(int32_t rows_ub) { return up256((size_t)rows_ub * 4); }
+
+size_t seer_lm_head_workspace_bytes(const seer_dims* dims, int32_t vocab, int32_t rows_ub) {
+  if (check_dims(dims) != SEER_OK || vocab <= 0 || rows_ub < 0) return 0;
+  return lm_partials_offset(rows_ub) + up256((size_t)rows_ub * (size_t)(vocab / 128) * sizeof(seer::ArgmaxPartial));
+}
+
+int seer_lm_head_predict(const seer_dims* dims, const void* w_lm, int32_t vocab, const void* x, int32_t rows_ub,
+                         const int32_t* cu_seqlens, int32_t batch, int32_t* pred, float* conf, void* workspace,
+                         size_t workspace_bytes, hipStream_t stream) {
+  int rc = check_dims(dims);
+  if (rc) return rc;
+  if (dims->dtype != SEER_DTYPE_BF16) return fail(SEER_EUNSUPPORTED, "the LM head runs on bf16 layers only");
+  if (!w_lm || !x || !cu_seqlens || !pred || !conf || !workspace)
+    return fail(SEER_EINVAL, "a required pointer is NULL");
+  if (vocab <= 0 || vocab % 256 != 0) return fail(SEER_EUNSUPPORTED, "vocab must be a positive multiple of 256 (got %d)", vocab);
+  if (batch < 1 || rows_ub < 1) return fail(SEER_EINVAL, "batch and rows_ub must be >= 1");
+  if (!aligned(w_lm, 16) || !aligned(x, 16) || !aligned(workspace, 256))
+    return fail(SEER_EINVAL, "w_lm and x need 16-byte, workspace 256-byte alignment");
+  const size_t need = seer_lm_head_workspace_bytes(dims, vocab, rows_ub);
+  if (workspace_bytes < need) return fail(SEER_EWORKSPACE, "workspace holds %zu bytes, need %zu", workspace_bytes, need);
+  uint8_t* ws = static_cast<uint8_t*>(workspace);
+  float* inv = reinterpret_cast<float*>(ws);
+  void* part = ws + lm_partials_offset(rows_ub);
+  const int* m_ptr = cu_seqlens + batch;
+  const int d = dims->d_model;
+  if (seer::launch_rms_inv(true, x, d, d, m_ptr, rows_ub, dims->rms_eps, inv, stream)) return hip_fail("rms launch");
+  seer::GemmParams g{};
+  g.A = x; g.B = w_lm; g.C = part; g.rs = inv;
+  g.m_ptr = m_ptr; g.m_ub = rows_ub; g.N = vocab; g.K = d;
+  g.lda = d; g.ldb = d; g.ldc = vocab / 128;
+  g.n_units = 0;                        // partials per 128 columns of whole 256-wide tiles
+  if (seer::launch_gemm_bf16(seer::EPI_ARGMAX, g, stream)) return hip_fail("lm head gemm launch");
+  if (seer::launch_argmax_reduce(part, vocab / 128, m_ptr, rows_ub, pred, conf, stream))
+    return hip_fail("argmax reduce launch");
+  return ok();
+}
+
+int seer_remask_step(const seer_dims* dims, const int32_t* cu_seqlens, const int32_t* seqused, int32_t batch,
+                     int32_t max_used, int32_t steps_left, const int32_t* pred, const float* conf, int32_t* tokens,
+                     const void* x0, const void* emb, int32_t vocab, void* x_next, hipStream_t stream) {
+  int rc = check_dims(dims);
+  if (rc) return rc;
+  if (dims->dtype != SEER_DTYPE_BF16) return fail(SEER_EUNSUPPORTED, "the sampler runs on bf16 layers only");
+  if (!cu_seqlens || !pred || !conf || !tokens || !x0 || !emb || !x_next)
+    return fail(SEER_EINVAL, "a required pointer is NULL");
+  if (batch < 1 || vocab < 1 || steps_left < 1) return fail(SEER_EINVAL, "batch, vocab and steps_left must be >= 1");
+  if (max_used < 0 || max_used > 8192) return fail(SEER_EUNSUPPORTED, "max_used must be in [0, 8192] (got %d)", max_used);
+  if (!aligned(x0, 16) || !aligned(emb, 16) || !aligned(x_next, 16)) return fail(SEER_EINVAL, "rows need 16-byte alignment");
+  seer::RemaskParams p{};
+  p.cu = cu_seqlens; p.used = seqused; p.B = batch; p.max_used = max_used; p.steps_left = steps_left;
+  p.pred = pred; p.conf = conf; p.tokens = tokens;
+  p.x0 = static_cast<const uint16_t*>(x0); p.emb = static_cast<const uint16_t*>(emb); p.vocab = vocab;
+  p.x_next = static_cast<uint16_t*>(x_next); p.d = dims->d_model;
+  if (seer::launch_remask(p, stream)) return hip_fail("remask launch");
+  return ok();
+}
+
 // ---- recorded launch sequences (Sec. 3.5, graph-compatible paths) ----------
 
 struct seer_graph_ {

@@ -152,6 +152,39 @@ class StepGraphs:
         self.graphs.clear()
 
 
+class SyntheticSampler:
+    """LM head and low-confidence remasking between denoising steps, on
+    window-only rows (the layout of the cached-prefix steps): after a step,
+    every masked window position gets a prediction and a confidence, the most
+    confident are committed, and the next step's input rows are rebuilt from
+    the committed tokens' embeddings (uncommitted rows keep their step-0
+    input).  Token state: tokens[r] == -1 while masked."""
+
+    def __init__(self, dims, w_lm, emb, rows_ub, device="cuda"):
+        self.dims = dims
+        self.w_lm, self.emb = w_lm, emb
+        self.vocab = int(w_lm.shape[0])
+        self.rows_ub = int(rows_ub)
+        self.ws_bytes = S.seer_lm_head_workspace_bytes(dims, self.vocab, self.rows_ub)
+        self.workspace = torch.empty(self.ws_bytes, dtype=torch.uint8, device=device)
+        self.pred = torch.empty(self.rows_ub, dtype=torch.int32, device=device)
+        self.conf = torch.empty(self.rows_ub, dtype=torch.float32, device=device)
+        self.tokens = torch.full((self.rows_ub,), -1, dtype=torch.int32, device=device)
+
+    def reset(self):
+        self.tokens.fill_(-1)
+
+    def predict(self, h, cu, batch, rows_ub, stream=None):
+        S.seer_lm_head_predict(self.dims, self.w_lm, self.vocab, h, rows_ub, cu, batch, self.pred, self.conf,
+                               self.workspace, self.ws_bytes, stream=stream)
+
+    def step(self, h, cu, used, batch, rows_ub, x0, x_next, steps_left, max_used, stream=None):
+        """Predict on the step's output rows h, commit, write the next inputs."""
+        self.predict(h, cu, batch, rows_ub, stream=stream)
+        S.seer_remask_step(self.dims, cu, used, batch, max_used, steps_left, self.pred, self.conf, self.tokens,
+                           x0, self.emb, self.vocab, x_next, stream=stream)
+
+
 class SeerStack:
     """A stack of prepacked layers plus the scratch the ABI calls need."""
 

@@ -22,7 +22,8 @@ EXPORTED = ("seer_prepacked_bytes", "seer_prepack_weights", "seer_layer_workspac
             "seer_layer_workspace_offsets", "seer_layer_forward_varlen",
             "seer_layer_forward_varlen_timed", "seer_step0_detect", "seer_batch_repack",
             "seer_layer_forward_cached", "seer_kv_export", "seer_graph_begin", "seer_graph_end",
-            "seer_graph_launch", "seer_graph_destroy", "seer_last_error", "seer_abi_version")
+            "seer_graph_launch", "seer_graph_destroy", "seer_lm_head_workspace_bytes",
+            "seer_lm_head_predict", "seer_remask_step", "seer_last_error", "seer_abi_version")
 
 
 class SeerError(RuntimeError):
@@ -105,6 +106,13 @@ def load_library():
     L.seer_layer_forward_cached.restype = ctypes.c_int
     L.seer_kv_export.argtypes = [ctypes.POINTER(seer_dims), _P, ctypes.c_size_t, _I, _P, _I, _P, _I, _P, _P]
     L.seer_kv_export.restype = ctypes.c_int
+    L.seer_lm_head_workspace_bytes.argtypes = [ctypes.POINTER(seer_dims), _I, _I]
+    L.seer_lm_head_workspace_bytes.restype = ctypes.c_size_t
+    L.seer_lm_head_predict.argtypes = [ctypes.POINTER(seer_dims), _P, _I, _P, _I, _P, _I, _P, _P, _P,
+                                       ctypes.c_size_t, _P]
+    L.seer_lm_head_predict.restype = ctypes.c_int
+    L.seer_remask_step.argtypes = [ctypes.POINTER(seer_dims), _P, _P, _I, _I, _I, _P, _P, _P, _P, _P, _I, _P, _P]
+    L.seer_remask_step.restype = ctypes.c_int
     L.seer_graph_begin.argtypes = [_P]
     L.seer_graph_begin.restype = ctypes.c_int
     L.seer_graph_end.argtypes = [_P, ctypes.POINTER(_P)]
@@ -250,3 +258,22 @@ def seer_graph_launch(graph, stream=None):
 
 def seer_graph_destroy(graph):
     _check(load_library().seer_graph_destroy(graph))
+
+
+def seer_lm_head_workspace_bytes(dims, vocab, rows_ub):
+    return load_library().seer_lm_head_workspace_bytes(ctypes.byref(dims), int(vocab), int(rows_ub))
+
+
+def seer_lm_head_predict(dims, w_lm, vocab, x, rows_ub, cu_seqlens, batch, pred, conf, workspace,
+                         workspace_bytes=None, stream=None):
+    nbytes = workspace_bytes if workspace_bytes is not None else workspace.numel() * workspace.element_size()
+    _check(load_library().seer_lm_head_predict(
+        ctypes.byref(dims), _ptr(w_lm), int(vocab), _ptr(x), int(rows_ub), _ptr(cu_seqlens), int(batch),
+        _ptr(pred), _ptr(conf), _ptr(workspace), nbytes, _stream(stream)))
+
+
+def seer_remask_step(dims, cu_seqlens, seqused, batch, max_used, steps_left, pred, conf, tokens, x0, emb, vocab,
+                     x_next, stream=None):
+    _check(load_library().seer_remask_step(
+        ctypes.byref(dims), _ptr(cu_seqlens), _ptr(seqused), int(batch), int(max_used), int(steps_left),
+        _ptr(pred), _ptr(conf), _ptr(tokens), _ptr(x0), _ptr(emb), int(vocab), _ptr(x_next), _stream(stream)))

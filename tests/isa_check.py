@@ -20,6 +20,11 @@ def _regs(tok):
     return [int(m.group(1))] if m else []
 
 
+def _returns_data(op):
+    return op.startswith(("ds_read", "ds_bpermute", "ds_permute", "ds_swizzle", "ds_append", "ds_consume")) \
+        or "_rtn" in op
+
+
 def _instrs(lines):
     for l in lines:
         s = l.strip()
@@ -28,8 +33,8 @@ def _instrs(lines):
 
 
 class _Sim:
-    """LDS operations (reads and writes) retire in issue order and all count
-    against lgkmcnt: lgkmcnt(N) guarantees every LDS op but the newest N has
+    """LDS operations (reads, writes, cross-lane permutes) retire in issue
+    order and all count against lgkmcnt: lgkmcnt(N) guarantees every LDS op but the newest N has
     retired (scalar loads share the counter but only make more retire, so
     ignoring them is conservative).  Destination registers of unretired
     reads are the ones nothing else may touch."""
@@ -48,11 +53,13 @@ class _Sim:
             live = set(self.queue)
             self.pending = {r: k for r, k in self.pending.items() if k in live}
             return None
-        if op.startswith("ds_read") or op.startswith("ds_write"):
+        if op.startswith("ds_"):
+            # every LDS instruction counts against lgkmcnt (cross-lane ds_bpermute
+            # and friends included); those that return data write their first operand
             touched = [r for x in ops[1:] for r in _regs(x) if r in self.pending]
             self.seq += 1
             self.queue.append(self.seq)
-            if op.startswith("ds_read"):
+            if _returns_data(op):
                 for r in _regs(ops[0]):
                     self.pending[r] = self.seq
             else:

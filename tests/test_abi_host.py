@@ -210,3 +210,26 @@ def test_graph_shapes():
         s = graph_shape(r, g)
         assert s % g == 0 and s >= r
         assert s <= max(2 * g, 1.5 * (-(-r // g) * g))
+
+
+def test_sampler_argument_errors(S):
+    L = S.load_library()
+    d = dims(S)
+    assert S.seer_lm_head_workspace_bytes(d, 126464, 1000) >= 1000 * (126464 // 128) * 16
+    args = lambda **kw: [kw.get(k, v) for k, v in [
+        ("dims", ctypes.byref(d)), ("w", FAKE), ("vocab", 126464), ("x", FAKE), ("rows", 100), ("cu", FAKE),
+        ("batch", 1), ("pred", FAKE), ("conf", FAKE), ("ws", FAKE), ("ws_bytes", 1 << 40), ("stream", None)]]
+    assert L.seer_lm_head_predict(*args(w=None)) == S.SEER_EINVAL
+    assert L.seer_lm_head_predict(*args(vocab=1000)) == S.SEER_EUNSUPPORTED
+    assert L.seer_lm_head_predict(*args(rows=0)) == S.SEER_EINVAL
+    assert L.seer_lm_head_predict(*args(ws_bytes=16)) == S.SEER_EWORKSPACE
+    d32 = dims(S, d=256, h=4, dh=64, i=688, dtype=2)
+    assert L.seer_lm_head_predict(*args(dims=ctypes.byref(d32))) == S.SEER_EUNSUPPORTED
+    rargs = lambda **kw: [kw.get(k, v) for k, v in [
+        ("dims", ctypes.byref(d)), ("cu", FAKE), ("used", None), ("batch", 2), ("max_used", 100), ("steps", 3),
+        ("pred", FAKE), ("conf", FAKE), ("tokens", FAKE), ("x0", FAKE), ("emb", FAKE), ("vocab", 10),
+        ("x_next", FAKE), ("stream", None)]]
+    assert L.seer_remask_step(*rargs(tokens=None)) == S.SEER_EINVAL
+    assert L.seer_remask_step(*rargs(steps=0)) == S.SEER_EINVAL
+    assert L.seer_remask_step(*rargs(max_used=8193)) == S.SEER_EUNSUPPORTED
+    assert L.seer_remask_step(*rargs(x0=FAKE + 8)) == S.SEER_EINVAL

@@ -105,6 +105,19 @@ def gate_up_gram(wg: np.ndarray, wu: np.ndarray) -> np.ndarray:
     return g.T @ g + u.T @ u
 
 
+def lm_head_torch(w: Workload, vocab: int, device, seed_offset: int = 0):
+    """Synthetic LM head [vocab, d] and token embedding table [vocab, d] (bf16
+    on the device): head ~ N(0, weight_std^2), embeddings ~ N(0, 1) like the
+    content rows.  Inputs only; drawn by torch's device generator."""
+    import torch
+    gen = torch.Generator(device=device)
+    gen.manual_seed(int(w.seed) * 1000 + 997 + seed_offset)
+    d = w.shape.d_model
+    head = torch.empty(vocab, d, device=device, dtype=torch.float32).normal_(0.0, w.weight_std, generator=gen)
+    emb = torch.empty(vocab, d, device=device, dtype=torch.float32).normal_(0.0, 1.0, generator=gen)
+    return head.to(torch.bfloat16), emb.to(torch.bfloat16)
+
+
 def eos_vector(wg: np.ndarray, wu: np.ndarray, amplitude: float, dtype: str, gram=None) -> np.ndarray:
     """The planted EOS embedding: least SwiGLU-amplified direction, scaled.
     ``gram`` (optional) replaces Wg^T Wg + Wu^T Wu, e.g. summed over layers."""
