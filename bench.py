@@ -38,6 +38,7 @@ if ROOT not in sys.path:
 METRIC = "effective gen tokens/sec per denoising step (B=16 ragged); MFMA util %"
 PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 matrix peak
 PEAK_HBM_GBS = 8000.0
+VOCAB = 126464          # LLaDA-8B vocabulary size (the synthetic LM head's width)
 
 
 # HBM traffic of the dominant kernel per launch, from two rocprofv3 --pmc passes
@@ -136,8 +137,9 @@ def bench_stack(args, w):
     import numpy as np
     import torch
     from paper_2607_14557_amd import seer as S
-    from paper_2607_14557_amd.runner import SeerStack, StepGraphs, dims_for, pinned_ctrl, poll_ctrl
-    from workloads.generate import layer_weights_torch, make_stack_batch
+    from paper_2607_14557_amd.runner import (SeerStack, StepGraphs, SyntheticSampler, dims_for, pinned_ctrl,
+                                             poll_ctrl)
+    from workloads.generate import layer_weights_torch, lm_head_torch, make_stack_batch
 
     sh = w.shape
     d, I, B, L = sh.d_model, sh.d_ff, w.batch, w.n_layers
@@ -178,9 +180,18 @@ def bench_stack(args, w):
         kv = (caches, cu_kv, kv_rows)
         log("  prefix K/V caches: %d rows x %d layers (%.1f GB)" % (kv_rows, L, kv_rows * 2 * d * 2 * L / 1e9))
 
+    smp = None
+    if args.sampler:
+        w_lm, emb = lm_head_torch(w, VOCAB, dev)
+        smp = SyntheticSampler(dims, w_lm, emb, cap)
+        x_cur = torch.empty(cap, d, dtype=torch.bfloat16, device=dev)
+        log("  synthetic LM head and embeddings: vocab %d (%.1f GB)" % (VOCAB, 2 * VOCAB * d * 2 / 1e9))
+
     def job():
         if args.graph:
             return job_graph()
+        if smp is not None:
+            return job_sampled()
         r = st.step0(x, cu, off, wl, B, T, w.l_det, w.act_eps, granule=granule, trunc_capacity=cap, stream=sp)
         if kv is None:
             for _ in range(n_trunc):
@@ -194,6 +205,24 @@ def bench_stack(args, w):
         st.forward_export(r.x_trunc, r.cu_trunc, r.seqused, B, cap, caches, cu_kv, kv_rows, stream=sp)
         for _ in range(n_trunc - 1):
             st.forward_cached(x_w, cu_w, used_w, B, max(rows_w, 1), caches, cu_kv, kv_rows, stream=sp)
+        r.cached = (x_w, cu_w, used_w, rows_w)
+        return r
+
+    def job_sampled():
+        # cached steps whose inputs evolve: LM head + remasking after each one
+        r = st.step0(x, cu, off, wl, B, T, w.l_det, w.act_eps, granule=granule, trunc_capacity=cap, stream=sp)
+        caches, cu_kv, kv_rows = kv
+        x_w, cu_w, used_w, _ = st.window_rows(x, cu, off, wl, r.keep_len, B, cap, granule=granule, stream=sp)
+        rows_w = int(cu_w[B].item())
+        rows_w = max(1, ((rows_w + granule - 1) // granule) * granule)
+        st.forward_export(r.x_trunc, r.cu_trunc, r.seqused, B, cap, caches, cu_kv, kv_rows, stream=sp)
+        smp.reset()
+        x_cur[:rows_w].copy_(x_w[:rows_w])
+        n = n_trunc - 1
+        for s_ in range(n):
+            h = st.forward_cached(x_cur, cu_w, used_w, B, rows_w, caches, cu_kv, kv_rows, stream=sp)
+            # the next inputs overwrite x_cur: layer 0 has consumed it
+            smp.step(h, cu_w, used_w, B, rows_w, x_w, x_cur, n - s_, w.window, stream=sp)
         r.cached = (x_w, cu_w, used_w, rows_w)
         return r
 
@@ -260,6 +289,13 @@ def bench_stack(args, w):
         x_w, cu_w, used_w, rows_w = r.cached
         t_cached = timed(lambda: st.forward_cached(x_w, cu_w, used_w, B, max(rows_w, 1), kv[0], kv[1], kv[2],
                                                    stream=sp))
+    t_sampler = None
+    if smp is not None:
+        x_w, cu_w, used_w, rows_w = r.cached
+        h = st.buf[0]
+        t_sampler = timed(lambda: smp.step(h, cu_w, used_w, B, rows_w, x_w, x_cur, 2, w.window, stream=sp))
+        committed = int((smp.tokens[:rows_w] >= 0).sum().item())
+        log("  sampler: %d of %d window rows committed after the job" % (committed, int(used_w.sum().item())))
     t_graph = {}
     host_ms = {}
     if args.graph:
@@ -300,7 +336,8 @@ def bench_stack(args, w):
     value = int(keep.sum()) * n_den / (ms_job * 1e-3)
     out = {
         "metric": "effective gen tokens/sec over step 0 + %d truncated denoising steps (%d-layer stack%s)"
-                  % (n_trunc, L, ", prefix K/V cached after the first truncated step" if kv else ""),
+                  % (n_trunc, L, (", prefix K/V cached after the first truncated step" if kv else "")
+                     + (", LM head + remasking after each cached step" if smp is not None else "")),
         "value": round(value, 1), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(ms_job, 3), "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
@@ -321,6 +358,7 @@ def bench_stack(args, w):
         "cached_step_ms": None if t_cached is None else round(t_cached, 3),
         "speedup_cached_vs_trunc": None if t_cached is None else round(t_trunc / t_cached, 3),
         "graph": bool(args.graph),
+        "sampler": {"vocab": VOCAB, "ms_per_step": round(t_sampler, 3)} if t_sampler is not None else None,
         "trunc_step_ms_graph": round(t_graph["trunc"], 3) if "trunc" in t_graph else None,
         "cached_step_ms_graph": round(t_graph["cached"], 3) if "cached" in t_graph else None,
         "graph_shapes": {k: sorted(g.graphs) for k, g in graphs.items()} if args.graph else None,
@@ -356,6 +394,9 @@ def main():
                     help="32-layer stacks: the host polls the pinned control word of each repack and "
                          "replays the truncated (or cached) steps from HIP graphs recorded per 1-D graph "
                          "shape of the routed capacity")
+    ap.add_argument("--sampler", action="store_true",
+                    help="32-layer stacks with --kv-cache: a synthetic LM head (vocab %d) and low-confidence "
+                         "remasking after every cached step, so each step's inputs differ" % VOCAB)
     ap.add_argument("--kv-cache", action="store_true",
                     help="32-layer stacks: after step 0, one full truncated step caches every layer's "
                          "prefix keys/values and the remaining steps run on the kept window rows")
@@ -383,10 +424,13 @@ def main():
         args.warmup = 5 if w.n_layers == 1 else 1
     if w.dtype != "bf16":
         raise SystemExit("bench.py times bf16 workloads")
+    if args.sampler and (args.graph or not args.kv_cache):
+        print("--sampler needs --kv-cache and excludes --graph", file=sys.stderr)
+        sys.exit(2)
     if w.n_layers > 1:
         return bench_stack(args, w)
-    if args.graph or args.kv_cache:
-        print("--graph and --kv-cache apply to the layer stacks (--workload llada32_video_b4 or "
+    if args.graph or args.kv_cache or args.sampler:
+        print("--graph, --kv-cache and --sampler apply to the layer stacks (--workload llada32_video_b4 or "
               "llada32_multicrop_b8)", file=sys.stderr)
         sys.exit(2)
     sh = w.shape
