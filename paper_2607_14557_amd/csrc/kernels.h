@@ -173,8 +173,9 @@ int launch_kv_export(const KvExportParams& p, int kv_rows_ub, hipStream_t s);
 int launch_argmax_reduce(const void* partials, int n_part, const int* m_ptr, int m_ub, int* pred, float* conf,
                          hipStream_t s);
 
-// Remasking step, one workgroup per sequence (rows [cu[b], cu[b+1]), the
-// first used[b] real): commit the ceil(n / steps_left) most confident masked
+// Remasking step (two launches: the decision, one workgroup per sequence,
+// then the rows) over rows [cu[b], cu[b+1]) of sequence b, the first used[b]
+// real: commit the ceil(n / steps_left) most confident masked
 // positions (tokens == -1), ties to the smaller position, then write the next
 // input rows: emb[token] if committed, x0 row if masked, zero past used.
 struct RemaskParams {

@@ -478,13 +478,20 @@ int launch_argmax_reduce(const void* partials, int n_part, const int* m_ptr, int
 }
 
 // ---------------------------------------------------------------------------
-// Remasking step: one workgroup of 256 per sequence.  A masked position's
-// rank is the number of masked positions with a larger (confidence, -position)
-// key; the k = ceil(n / steps_left) of rank < k are committed.  Keys are
-// unique, so the selection is exact and independent of the thread order.
-constexpr int kRemaskPerThread = 32;   // up to 8192 positions per sequence
+// Remasking step.  Decision: one workgroup of 1024 per sequence stages the
+// keys of its positions in LDS (confidence if masked, -1 if committed; a
+// softmax probability is > 0), so a masked position's rank -- the number of
+// masked positions with a larger (confidence, -position) key -- is a sweep of
+// LDS broadcasts; the k = ceil(n / steps_left) of rank < k are committed.
+// Keys are unique, so the selection is exact and independent of the thread
+// order.  Rows: a second launch writes the next input rows, 8 workgroups per
+// sequence.
+constexpr int kRemaskThreads = 1024;
+constexpr int kRemaskPerThread = 8;    // up to 8192 positions per sequence
 
-__global__ __launch_bounds__(256) void remask_kernel(RemaskParams p) {
+__global__ __launch_bounds__(kRemaskThreads) void remask_decide_kernel(RemaskParams p) {
+  __shared__ float s_key[kRemaskThreads * kRemaskPerThread];
+  __shared__ int s_cnt;
   const int b = blockIdx.x;
   const int tid = threadIdx.x;
   const int r0 = p.cu[b];
@@ -492,46 +499,52 @@ __global__ __launch_bounds__(256) void remask_kernel(RemaskParams p) {
   int used = p.used ? p.used[b] : rows;
   used = used < 0 ? 0 : (used > rows ? rows : used);
   used = used > p.max_used ? p.max_used : used;
-  __shared__ int s_cnt;
   if (tid == 0) s_cnt = 0;
   __syncthreads();
   int local = 0;
-  for (int i = tid; i < used; i += 256) local += p.tokens[r0 + i] < 0;
+  for (int i = tid; i < used; i += kRemaskThreads) {
+    const bool masked = p.tokens[r0 + i] < 0;
+    s_key[i] = masked ? p.conf[r0 + i] : -1.0f;
+    local += masked;
+  }
   if (local) atomicAdd(&s_cnt, local);
   __syncthreads();
   const int n = s_cnt;
   const int k = p.steps_left <= 1 ? n : (n + p.steps_left - 1) / p.steps_left;
-  // decisions first (every thread reads the step's token state), then commits
-  bool commit[kRemaskPerThread];
 #pragma unroll
   for (int t = 0; t < kRemaskPerThread; ++t) {
-    const int i = tid + 256 * t;
-    commit[t] = false;
-    if (i >= used || p.tokens[r0 + i] >= 0 || k == 0) continue;
-    const float ci = p.conf[r0 + i];
+    const int i = tid + kRemaskThreads * t;
+    if (i >= used || k == 0) continue;
+    const float ci = s_key[i];
+    if (ci < 0.0f) continue;
     int rank = 0;
     for (int j = 0; j < used && rank < k; ++j) {
-      if (p.tokens[r0 + j] >= 0) continue;
-      const float cj = p.conf[r0 + j];
+      const float cj = s_key[j];
       rank += (cj > ci) || (cj == ci && j < i);
     }
-    commit[t] = rank < k;
-  }
-  __syncthreads();
-#pragma unroll
-  for (int t = 0; t < kRemaskPerThread; ++t) {
-    const int i = tid + 256 * t;
-    if (commit[t]) {
+    if (rank < k) {
       int tok = p.pred[r0 + i];
       tok = tok < 0 ? 0 : (tok >= p.vocab ? p.vocab - 1 : tok);
-      p.tokens[r0 + i] = tok;
+      p.tokens[r0 + i] = tok;        // only this thread reads or writes entry i from here on
     }
   }
-  __syncthreads();
-  // next input rows, 16-byte chunks
+}
+
+constexpr int kRemaskRowSplit = 8;
+
+__global__ __launch_bounds__(256) void remask_rows_kernel(RemaskParams p) {
+  const int b = blockIdx.x;
+  const int r0 = p.cu[b];
+  const int rows = p.cu[b + 1] - r0;
+  int used = p.used ? p.used[b] : rows;
+  used = used < 0 ? 0 : (used > rows ? rows : used);
+  used = used > p.max_used ? p.max_used : used;
+  const int per = (rows + kRemaskRowSplit - 1) / kRemaskRowSplit;
+  const int i0 = blockIdx.y * per;
+  const int i1 = i0 + per < rows ? i0 + per : rows;
   const int chunks = p.d >> 3;
-  for (int c = tid; c < rows * chunks; c += 256) {
-    const int i = c / chunks, ch = c % chunks;
+  for (int c = threadIdx.x; c < (i1 - i0) * chunks; c += 256) {
+    const int i = i0 + c / chunks, ch = c % chunks;
     uint4 v = make_uint4(0u, 0u, 0u, 0u);
     if (i < used) {
       const int tok = p.tokens[r0 + i];
@@ -543,8 +556,10 @@ __global__ __launch_bounds__(256) void remask_kernel(RemaskParams p) {
 }
 
 int launch_remask(const RemaskParams& p, hipStream_t s) {
-  if (p.max_used > 256 * kRemaskPerThread || p.d % 8 != 0) return -1;
-  hipLaunchKernelGGL(remask_kernel, dim3(p.B), dim3(256), 0, s, p);
+  if (p.max_used > kRemaskThreads * kRemaskPerThread || p.d % 8 != 0) return -1;
+  hipLaunchKernelGGL(remask_decide_kernel, dim3(p.B), dim3(kRemaskThreads), 0, s, p);
+  if (hipGetLastError() != hipSuccess) return -1;
+  hipLaunchKernelGGL(remask_rows_kernel, dim3(p.B, kRemaskRowSplit), dim3(256), 0, s, p);
   return hipGetLastError() == hipSuccess ? 0 : -1;
 }
 
