@@ -482,13 +482,13 @@ int seer_graph_end(hipStream_t stream, seer_graph_t* graph) {
   if (stream == nullptr) return fail(SEER_EINVAL, "stream is NULL");
   hipGraph_t g = nullptr;
   if (hipStreamEndCapture(stream, &g) != hipSuccess || g == nullptr) {
-    if (g) hipGraphDestroy(g);
+    if (g) (void)hipGraphDestroy(g);
     return hip_fail("hipStreamEndCapture (a call recorded since seer_graph_begin failed, or the stream "
                     "was not being recorded)");
   }
   hipGraphExec_t exec = nullptr;
   if (hipGraphInstantiate(&exec, g, nullptr, nullptr, 0) != hipSuccess) {
-    hipGraphDestroy(g);
+    (void)hipGraphDestroy(g);
     return hip_fail("hipGraphInstantiate");
   }
   *graph = new seer_graph_{g, exec};
