@@ -51,7 +51,11 @@ def poll_ctrl(ctrl_host, timeout_s=30.0):
     before enqueuing the repack."""
     a = ctrl_host.numpy()
     t_end = time.monotonic() + timeout_s
+    spins = 0
     while int(a[8]) != 1:
+        spins += 1
+        if spins > 1000:
+            time.sleep(5e-5)           # past the first ~100 us, yield the core between reads
         if time.monotonic() > t_end:
             raise TimeoutError("control word not written within %.0f s" % timeout_s)
     v = [int(a[i]) for i in range(9)]
@@ -100,9 +104,14 @@ def record(fn, stream):
     S.seer_graph_begin(stream)
     try:
         fn()
-    finally:
-        handle = S.seer_graph_end(stream)
-    return SeerGraph(handle)
+    except BaseException:
+        # close the recording, drop what it holds, and report fn's error
+        try:
+            S.seer_graph_destroy(S.seer_graph_end(stream))
+        except S.SeerError:
+            pass
+        raise
+    return SeerGraph(S.seer_graph_end(stream))
 
 
 @dataclass
