@@ -484,13 +484,13 @@ int launch_argmax_reduce(const void* partials, int n_part, const int* m_ptr, int
 // masked positions with a larger (confidence, -position) key -- is a sweep of
 // LDS broadcasts; the k = ceil(n / steps_left) of rank < k are committed.
 // Keys are unique, so the selection is exact and independent of the thread
-// order.  Rows: a second launch writes the next input rows, 8 workgroups per
+// order.  Rows: a second launch writes the next input rows, 64 workgroups per
 // sequence.
 constexpr int kRemaskThreads = 1024;
 constexpr int kRemaskPerThread = 8;    // up to 8192 positions per sequence
 
 __global__ __launch_bounds__(kRemaskThreads) void remask_decide_kernel(RemaskParams p) {
-  __shared__ float s_key[kRemaskThreads * kRemaskPerThread];
+  __shared__ __attribute__((aligned(16))) float s_key[kRemaskThreads * kRemaskPerThread];
   __shared__ int s_cnt;
   const int b = blockIdx.x;
   const int tid = threadIdx.x;
@@ -502,9 +502,9 @@ __global__ __launch_bounds__(kRemaskThreads) void remask_decide_kernel(RemaskPar
   if (tid == 0) s_cnt = 0;
   __syncthreads();
   int local = 0;
-  for (int i = tid; i < used; i += kRemaskThreads) {
-    const bool masked = p.tokens[r0 + i] < 0;
-    s_key[i] = masked ? p.conf[r0 + i] : -1.0f;
+  for (int i = tid; i < ((used + 7) & ~7); i += kRemaskThreads) {
+    const bool masked = i < used && p.tokens[r0 + i] < 0;
+    s_key[i] = i < used ? (masked ? p.conf[r0 + i] : -1.0f) : -2.0f;
     local += masked;
   }
   if (local) atomicAdd(&s_cnt, local);
@@ -517,10 +517,17 @@ __global__ __launch_bounds__(kRemaskThreads) void remask_decide_kernel(RemaskPar
     if (i >= used || k == 0) continue;
     const float ci = s_key[i];
     if (ci < 0.0f) continue;
+    // eight keys per step (two 16-byte LDS reads in flight); keys past `used`
+    // are -2 (below every key), so whole steps need no bounds test
     int rank = 0;
-    for (int j = 0; j < used && rank < k; ++j) {
-      const float cj = s_key[j];
-      rank += (cj > ci) || (cj == ci && j < i);
+    for (int j0 = 0; j0 < used && rank < k; j0 += 8) {
+      const f32x4_t c0 = *reinterpret_cast<const f32x4_t*>(&s_key[j0]);
+      const f32x4_t c1 = *reinterpret_cast<const f32x4_t*>(&s_key[j0 + 4]);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        rank += (c0[e] > ci) || (c0[e] == ci && j0 + e < i);
+        rank += (c1[e] > ci) || (c1[e] == ci && j0 + 4 + e < i);
+      }
     }
     if (rank < k) {
       int tok = p.pred[r0 + i];
@@ -530,7 +537,7 @@ __global__ __launch_bounds__(kRemaskThreads) void remask_decide_kernel(RemaskPar
   }
 }
 
-constexpr int kRemaskRowSplit = 8;
+constexpr int kRemaskRowSplit = 64;
 
 __global__ __launch_bounds__(256) void remask_rows_kernel(RemaskParams p) {
   const int b = blockIdx.x;
