@@ -334,7 +334,7 @@ int seer_batch_repack(const seer_repack_desc* desc, const void* const* src,
  * columns, merged by a second kernel.  vocab % 256 == 0.  Workspace: at
  * least seer_lm_head_workspace_bytes(dims, vocab, rows_ub), 256-byte aligned.
  * Errors: EINVAL (null pointers, sizes < 1, alignment), EUNSUPPORTED (fp32,
- * vocab), EWORKSPACE.
+ * vocab, w_lm or x of 4 GiB or more), EWORKSPACE.
  *
  * seer_remask_step: per sequence b (rows [cu_seqlens[b], cu_seqlens[b+1]), the
  * first min(seqused[b], max_used) of them real; seqused may be NULL): among

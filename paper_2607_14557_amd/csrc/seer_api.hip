@@ -418,6 +418,9 @@ int seer_lm_head_predict(const seer_dims* dims, const void* w_lm, int32_t vocab,
     return fail(SEER_EINVAL, "a required pointer is NULL");
   if (vocab <= 0 || vocab % 256 != 0) return fail(SEER_EUNSUPPORTED, "vocab must be a positive multiple of 256 (got %d)", vocab);
   if (batch < 1 || rows_ub < 1) return fail(SEER_EINVAL, "batch and rows_ub must be >= 1");
+  // the GEMM addresses its operands with 32-bit byte offsets
+  if ((size_t)vocab * dims->d_model * 2 >= ((size_t)1 << 32) || (size_t)rows_ub * dims->d_model * 2 >= ((size_t)1 << 32))
+    return fail(SEER_EUNSUPPORTED, "w_lm and x must each stay below 4 GiB");
   if (!aligned(w_lm, 16) || !aligned(x, 16) || !aligned(workspace, 256))
     return fail(SEER_EINVAL, "w_lm and x need 16-byte, workspace 256-byte alignment");
   const size_t need = seer_lm_head_workspace_bytes(dims, vocab, rows_ub);

@@ -223,6 +223,7 @@ def test_sampler_argument_errors(S):
     assert L.seer_lm_head_predict(*args(vocab=1000)) == S.SEER_EUNSUPPORTED
     assert L.seer_lm_head_predict(*args(rows=0)) == S.SEER_EINVAL
     assert L.seer_lm_head_predict(*args(ws_bytes=16)) == S.SEER_EWORKSPACE
+    assert L.seer_lm_head_predict(*args(vocab=524288)) == S.SEER_EUNSUPPORTED     # 4 GiB of head weights
     d32 = dims(S, d=256, h=4, dh=64, i=688, dtype=2)
     assert L.seer_lm_head_predict(*args(dims=ctypes.byref(d32))) == S.SEER_EUNSUPPORTED
     rargs = lambda **kw: [kw.get(k, v) for k, v in [
