@@ -159,7 +159,9 @@ int seer_layer_workspace_offsets(const seer_dims* dims, int32_t max_rows, size_t
  * the per-position MLP sparsity statistic of Sec. 3.2-3.3.
  * workspace: >= seer_layer_workspace_bytes(dims, total_rows_ub) bytes,
  * 256-byte aligned.  Errors: EINVAL (null pointers, batch < 1,
- * total_rows_ub < 1), EUNSUPPORTED (dims), EWORKSPACE. */
+ * total_rows_ub < 1), EUNSUPPORTED (dims; bf16 with total_rows_ub x
+ * max(3 d_model, d_ff) x 2 bytes >= 4 GiB: the kernels use 32-bit row
+ * offsets), EWORKSPACE. */
 int seer_layer_forward_varlen(const seer_dims* dims, const void* w_packed,
                               const void* x_in, void* x_out, int32_t total_rows_ub,
                               const int32_t* cu_seqlens, const int32_t* seqused,

@@ -160,6 +160,14 @@ static int layer_forward_impl(const seer_dims* dims, const void* w_packed, const
   if (bf16 && (!aligned(w_packed, 256) || !aligned(x_in, 16) || !aligned(x_out, 16)))
     return fail(SEER_EINVAL, "bf16 weights need 256-byte and rows 16-byte alignment");
   if (!aligned(workspace, 256)) return fail(SEER_EINVAL, "workspace must be 256-byte aligned");
+  if (bf16) {
+    // the bf16 kernels address rows with 32-bit byte offsets: the widest row
+    // buffer (qkv, 3 d, or the activations, d_ff) must stay below 4 GiB
+    const size_t wide = (size_t)(3 * dims->d_model > dims->d_ff ? 3 * dims->d_model : dims->d_ff);
+    if ((size_t)total_rows_ub * wide * 2 >= ((size_t)1 << 32))
+      return fail(SEER_EUNSUPPORTED, "total_rows_ub %d too large for the bf16 kernels (rows x %zu bf16 >= 4 GiB)",
+                  total_rows_ub, wide);
+  }
   const WsLayout L = ws_layout(dims, total_rows_ub);
   if (workspace_bytes < L.total)
     return fail(SEER_EWORKSPACE, "workspace holds %zu bytes, need %zu", workspace_bytes, L.total);

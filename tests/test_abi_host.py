@@ -88,6 +88,8 @@ def call_layer(S, d, **kw):
 def test_layer_forward_argument_errors(S):
     d = dims(S)
     assert call_layer(S, d, w=None) == S.SEER_EINVAL
+    assert call_layer(S, d, rows=174763) == S.SEER_EUNSUPPORTED      # 174763 x 12288 x 2 B >= 4 GiB
+    assert "4 GiB" in S.seer_last_error()
     assert call_layer(S, d, cu=None) == S.SEER_EINVAL
     assert call_layer(S, d, batch=0) == S.SEER_EINVAL
     assert call_layer(S, d, rows=0) == S.SEER_EINVAL
