@@ -105,7 +105,11 @@ size_t seer_prepacked_bytes(const seer_dims* dims);
  * seer_prepacked_bytes() bytes, 256-byte aligned): q/k/v stacked, gate and up
  * rows interleaved in blocks of 32 so that one tile holds matching gate and
  * up columns, and the RMSNorm gains folded into the input columns of the
- * projections they feed (exact for unit gains).  The source is not modified. */
+ * projections they feed (exact for unit gains).  bf16 layers also store every
+ * matrix in the matrix cores' operand order (one 1 KiB block per 32 output
+ * rows and 16 input columns) with the q and k rows of each head in 32-row
+ * block order 0, 2, 1, 3; the layout is private to the library and may change
+ * with the ABI version.  The source is not modified. */
 int seer_prepack_weights(const seer_dims* dims, const seer_layer_weights* src,
                          void* dst, size_t dst_bytes, hipStream_t stream);
 
@@ -332,7 +336,7 @@ int seer_batch_repack(const seer_repack_desc* desc, const void* const* src,
  * bf16 ([out, in]); pred[r] = argmax_v l_v (the smallest v among equal
  * maxima), conf[r] = its softmax probability 1 / sum_v exp(l_v - l_max).
  * Logits are fp32 (bf16 products, fp32 accumulation) and never stored: the
- * GEMM epilogue keeps a {max, sum exp, argmax} partial per row and 128
+ * GEMM epilogue keeps a {max, sum exp, argmax} partial per row and 64
  * columns, merged by a second kernel.  vocab % 256 == 0.  Workspace: at
  * least seer_lm_head_workspace_bytes(dims, vocab, rows_ub), 256-byte aligned.
  * Errors: EINVAL (null pointers, sizes < 1, alignment), EUNSUPPORTED (fp32,
@@ -387,7 +391,7 @@ int seer_graph_destroy(seer_graph_t graph);
 const char* seer_last_error(void);
 
 /* ABI version of this library (major * 100 + minor). */
-int32_t seer_abi_version(void);   /* 101: seer_dims.rope_theta */
+int32_t seer_abi_version(void);   /* 102: bf16 weights packed in operand order */
 
 #ifdef __cplusplus
 }

@@ -3,18 +3,30 @@
 //
 // The four projections of the layer (QKV, O, gate/up, down) are the dense
 // contractions of the denoising step (the L*d^2 term of the complexity
-// equation, Sec. 3.1).  Tiling: 256x256 block tile, K step 64, four waves in
-// a 2x2 grid, each wave owning a 128x128 sub-tile as 4x4 tiles of the
-// 32x32x16 bf16 MFMA.  Operand tiles move global -> registers -> LDS through
-// a two-stage LDS ring with two K tiles of look-ahead; the 16-byte chunks of
-// each 128-byte LDS row are XOR-swizzled so that the MFMA fragment reads of
-// 16 consecutive rows land in distinct banks.  Every 16-wide K slice is its
-// own scheduling region in which the next slice's fragments are read first,
-// so LDS latency hides behind a whole slice of MFMAs.
+// equation, Sec. 3.1).  Tiling: 256x256 block tile, K step 64, four waves side
+// by side, each owning all 256 rows and 64 columns of the tile as 8x2 tiles of
+// the 32x32x16 bf16 MFMA.
+//
+// Operands take two different routes:
+//   A (activations, shared by all four waves) moves global -> registers -> LDS
+//     through a two-stage LDS ring with two K tiles of look-ahead; the 16-byte
+//     chunks of each 128-byte LDS row are XOR-swizzled so that the fragment
+//     reads of 16 consecutive rows land in distinct banks;
+//   B (weights, 64 columns private to each wave) never touches LDS: the weight
+//     prepack stores it fragment-major (frag_b_index), so every operand of a
+//     wave is one coalesced 1 KiB load straight into the MFMA registers, issued
+//     one K tile ahead.
+// Every 16-wide K slice is its own scheduling region in which the next slice's
+// A fragments are read first, so LDS latency hides behind a whole slice of
+// MFMAs.
 //
 // Epilogues:
 //   SCALE   C = bf16(acc * rowscale[r])         folded RMSNorm before QKV;
-//           column tiles from f16_col0 on (V) are stored as fp16 instead
+//           column tiles from f16_col0 on (V) are stored as fp16 instead;
+//           columns below perm_col1 come from the head-permuted q/k rows of
+//           the packed weight and are stored back in head order
+//   SCALE_ROPE  as SCALE, and the columns below rope_col1 are rotated
+//           (rotary embedding of q and k) on the way
 //   RESID   C = bf16(R[r,c] + acc)              residual add
 //   RESID_SPLIT v = R[r,c] + acc: C = bf16(v) and residual after O: h1 as a bf16
 //               C2 = bf16(v - C)                high/low pair, exact to ~2^-17
@@ -23,7 +35,9 @@
 //           the packed weight interleaves 32 gate rows with 32 up rows, so a
 //           wave holds matching gate and up columns in its registers
 //   SWIGLU_COUNT  as SWIGLU, plus the per-row count of |act| < eps on the
-//           fp32 values (wave ballot + popcount, one atomic per row and wave)
+//           fp32 values (per-lane tally, one atomic per row and wave)
+//   ARGMAX  per row and 64-column group {max, sum exp(v - max), first argmax}
+//           of acc * rowscale (LM head); B is the caller's row-major matrix
 #include <type_traits>
 
 #include "common.h"
@@ -33,10 +47,10 @@ namespace seer {
 
 namespace {
 
-constexpr int BM = 256, BK = 64;
+constexpr int BK = 64;
 constexpr int NT = 256;
 constexpr int GROUP_M = 4;
-constexpr int ROW_BYTES = BK * 2;                   // 128 bytes per tile row
+constexpr int ROW_BYTES = BK * 2;                   // 128 bytes per A tile row
 
 __device__ __forceinline__ int swz(int r) { return (r & 7) ^ ((r >> 3) & 1); }
 
@@ -63,81 +77,69 @@ __device__ __forceinline__ void raster(int lid, int tiles_m, int tiles_n, int& t
 
 }  // namespace
 
-// Instruction order inside one K slice (masks: 0x008 MFMA, 0x020 VMEM,
-// 0x100 LDS read, 0x200 LDS write).  Per slice: the next slice's fragment
-// reads, a quarter of the next-next tile's global loads and the LDS writes of
-// the next tile (none in the last slice, twice as many in slice 2), spread
-// between the 4 NJ MFMAs.
-template <int BN>
+// Instruction order inside one K slice of a BMT-row tile (masks: 0x008 MFMA,
+// 0x020 VMEM, 0x100 LDS read, 0x200 LDS write).  Per slice: the next slice's
+// BMT/32 fragment reads, paired two to an MFMA; the global loads (BMT/128 of
+// A for tile t+2, two of B for tile t+1), one per MFMA; the LDS writes of A
+// tile t+1 (BMT/128 in slices 0 and 1, twice that in slice 2, none in slice
+// 3), one per MFMA; then the remaining MFMAs.
+template <int BMT>
 __device__ __forceinline__ void seer_slice_schedule(int ks) {
-  if constexpr (BN == 256) {        // 8 reads, 4 loads, 4/8/0 writes, 16 MFMAs
+  constexpr int NR = BMT / 32;
+  constexpr int NV = BMT / 128 + 2;
+  constexpr int NW = BMT / 128;
+  constexpr int NM = 2 * NR;
 #pragma unroll
-    for (int g = 0; g < 4; ++g) {
-      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+  for (int g = 0; g < NR / 2; ++g) {
+    __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+  }
+#pragma unroll
+  for (int g = 0; g < NV; ++g) {
+    __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+  }
+  if (ks < 2) {
+#pragma unroll
+    for (int g = 0; g < NW; ++g) {
+      __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
     }
+    __builtin_amdgcn_sched_group_barrier(0x008, NM - NR / 2 - NV - NW, 0);
+  } else if (ks == 2) {
 #pragma unroll
-    for (int g = 0; g < 4; ++g) {
-      __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+    for (int g = 0; g < 2 * NW; ++g) {
+      __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
     }
-    if (ks < 2) {
-#pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      }
-      __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
-    } else if (ks == 2) {
-#pragma unroll
-      for (int g = 0; g < 8; ++g) {
-        __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      }
-    } else {
-      __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
-    }
-  } else {                          // 6 reads, 3 loads, 3/6/0 writes, 8 MFMAs
-#pragma unroll
-    for (int g = 0; g < 3; ++g) {
-      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-    }
-#pragma unroll
-    for (int g = 0; g < 3; ++g) {
-      __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
-      if (ks < 2) __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);
-      if (ks == 2) __builtin_amdgcn_sched_group_barrier(0x200, 2, 0);
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-    }
-    __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+    __builtin_amdgcn_sched_group_barrier(0x008, NM - NR / 2 - NV - 2 * NW, 0);
+  } else {
+    __builtin_amdgcn_sched_group_barrier(0x008, NM - NR / 2 - NV, 0);
   }
 }
 
-// One BMxBN output tile over the whole K range.  BN = 256 is the main tile
-// (waves of 128x128); BN = 128 (waves of 128x64) serves the halves of the
-// tiles of a partly filled last round.
-template <int EPI, int BN>
+// One BMTx256 output tile over the whole K range.  BMT = 256 is the main
+// tile; BMT = 128 serves the halves of the tiles of a partly filled last
+// round.  Wave w owns columns n0 + 64 w .. +63 and all BMT rows.
+template <int EPI, int BMT>
 __device__ __forceinline__ void gemm_tile(const GemmParams& p, uint8_t* smem, int M, int m0, int n0) {
-  constexpr int NJ = BN / 64;                       // 32-column MFMA tiles per wave
-  constexpr int NB = BN / 32;                       // B chunks per thread per K tile
-  constexpr int BP = NB / 4;                        // ... per slice
-  constexpr int STAGE_BYTES = (BM + BN) * ROW_BYTES;
+  constexpr int NI = BMT / 32;                      // 32-row MFMA tiles per wave = A chunks per thread
+  constexpr int AP = NI / 4;                        // ... per slice
+  constexpr int STAGE_BYTES = BMT * ROW_BYTES;
+  constexpr bool kFragB = EPI != EPI_ARGMAX;        // packed weight, or the caller's row-major matrix
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
-  const int wm = wave >> 1;
-  const int wn = wave & 1;
+  const int wcol = n0 + 64 * wave;                  // first (packed) column of the wave
 
   uint16_t* C = static_cast<uint16_t*>(p.C);
   const uint16_t* R = static_cast<const uint16_t*>(p.R);
 
-  // ---- global -> register -> LDS staging -----------------------------------
-  // Thread t moves 16-byte chunks c = t + 256 i of the 256x64 A tile (i < 8)
-  // and of the BNx64 B tile (i < NB): tile row c / 8, K-chunk c % 8 -- eight
-  // consecutive threads read one 128-byte row segment.  In LDS the chunk lands
-  // at position chunk ^ swz(row).
+  // ---- A: global -> register -> LDS staging ------------------------------
+  // Thread t moves 16-byte chunks c = t + 256 i of the BMTx64 A tile (i < NI):
+  // tile row c / 8, K-chunk c % 8 -- eight consecutive threads read one
+  // 128-byte row segment.  In LDS the chunk lands at position chunk ^ swz(row).
   const int srow = tid >> 3;          // + 32 i
   const int schunk = tid & 7;
   // 32-bit byte offsets from the uniform bases (operands are < 4 GiB); rows of
@@ -145,116 +147,134 @@ __device__ __forceinline__ void gemm_tile(const GemmParams& p, uint8_t* smem, in
   // row = srow + 32 i, so the LDS slot is one base plus an immediate.
   const char* Ab = static_cast<const char*>(p.A);
   const char* Bb = static_cast<const char*>(p.B);
-  uint32_t a_off[8];
+  uint32_t a_off[NI];
 #pragma unroll
-  for (int i = 0; i < 8; ++i) {
+  for (int i = 0; i < NI; ++i) {
     int ga = m0 + srow + 32 * i;
     ga = ga < M ? ga : M - 1;
     a_off[i] = (uint32_t)ga * (uint32_t)p.lda * 2u + (uint32_t)schunk * 16u;
   }
-  const uint32_t b_off = (uint32_t)(n0 + srow) * (uint32_t)p.ldb * 2u + (uint32_t)schunk * 16u;
-  const uint32_t b_step = 32u * (uint32_t)p.ldb * 2u;
   const int s_off = srow * ROW_BYTES + ((schunk ^ swz(srow)) << 4);
-  f32x16_t acc[4][NJ];
-#pragma unroll
-  for (int i = 0; i < 4; ++i)
-#pragma unroll
-    for (int j = 0; j < NJ; ++j)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
-  // Fragment read geometry: lane l reads row (l & 31) of a 32-row MFMA tile
-  // and the 16-byte K-chunk 2*ks + (l >> 5).
+  // Fragment geometry: lane l holds row (l & 31) of a 32-row MFMA tile and
+  // the 8 K values 16 s + 8 (l >> 5) .. +7 of K slice s.
   const int fr = lane & 31;
   const int fsw = swz(fr);
   const int fhalf = lane >> 5;
-  const int a_row0 = (wm * 128 + fr) * ROW_BYTES;
-  const int b_row0 = BM * ROW_BYTES + (wn * (BN / 2) + fr) * ROW_BYTES;
+  const int a_row0 = fr * ROW_BYTES;
 
-  // Software pipeline, two K tiles of look-ahead: while tile t is multiplied
-  // out of LDS stage t%2, tile t+1 (loaded into registers one iteration
-  // earlier) is written into stage (t+1)%2 between the MFMAs, and the loads of
-  // tile t+2 are in flight.  Two register sets alternate, so the loop is
+  // ---- B: straight into the operand registers -----------------------------
+  // Column block j of the wave: lane l takes column wcol + 32 j + l%32.
+  // Fragment-major, its operand of K slice s is the 16 bytes at 16 l of block
+  // (col / 32) * (K / 16) + s; row-major, the 16 bytes at K offset 16 s + 8 (l/32).
+  uint32_t b_off[2];
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    if constexpr (kFragB)
+      b_off[j] = (uint32_t)((wcol >> 5) + j) * (uint32_t)(p.K >> 4) * 1024u + (uint32_t)lane * 16u;
+    else
+      b_off[j] = (uint32_t)(wcol + 32 * j + fr) * (uint32_t)p.ldb * 2u + (uint32_t)fhalf * 16u;
+  }
+  constexpr uint32_t B_TILE = kFragB ? 4096u : 128u;
+  constexpr uint32_t B_SLICE = kFragB ? 1024u : 32u;
+
+  f32x16_t acc[NI][2];
+#pragma unroll
+  for (int i = 0; i < NI; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+
+  // Software pipeline: while tile t is multiplied out of LDS stage t%2 and B
+  // register set t%2, A tile t+1 (loaded into registers one iteration earlier)
+  // is written into stage (t+1)%2 between the MFMAs, and the loads of A tile
+  // t+2 and B tile t+1 are in flight.  Register sets alternate, so the loop is
   // unrolled by two; K/64 is even for every shape the bf16 path accepts.
-  u32x4_t ra0[8], rb0[NB], ra1[8], rb1[NB];
-  bf16x8_t af[2][4], bfr[2][NJ];
+  u32x4_t ra0[NI], ra1[NI];
+  bf16x8_t bq0[2][4], bq1[2][4];
+  bf16x8_t af[2][NI];
   const int KT = p.K / BK;
 
-#define SEER_GLOAD(RA, RB, T, P)                                                    \
+#define SEER_GLOAD_A(RA, T, P)                                                      \
   {                                                                                 \
     const int t_ = (T) < KT ? (T) : KT - 1;                                         \
     const char* ak_ = Ab + (size_t)t_ * (BK * 2);                                   \
-    const char* bk_ = Bb + (size_t)t_ * (BK * 2);                                   \
-    _Pragma("unroll") for (int i = 2 * (P); i < 2 * (P) + 2; ++i)                   \
+    _Pragma("unroll") for (int i = AP * (P); i < AP * (P) + AP; ++i)                \
       RA[i] = *reinterpret_cast<const u32x4_t*>(ak_ + a_off[i]);                    \
-    _Pragma("unroll") for (int i = BP * (P); i < BP * (P) + BP; ++i)                \
-      RB[i] = *reinterpret_cast<const u32x4_t*>(bk_ + b_off + i * b_step);          \
   }
-#define SEER_LSTORE(RA, RB, STG, P)                                                 \
+#define SEER_GLOAD_B(BQ, T, KS)                                                     \
+  {                                                                                 \
+    const int t_ = (T) < KT ? (T) : KT - 1;                                         \
+    const char* bk_ = Bb + (size_t)t_ * B_TILE + (KS) * B_SLICE;                    \
+    _Pragma("unroll") for (int j = 0; j < 2; ++j)                                   \
+      BQ[j][KS] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const u32x4_t*>(bk_ + b_off[j])); \
+  }
+#define SEER_LSTORE(RA, STG, P)                                                     \
   {                                                                                 \
     uint8_t* sa_ = smem + (STG) * STAGE_BYTES + s_off;                              \
-    _Pragma("unroll") for (int i = 2 * (P); i < 2 * (P) + 2; ++i)                   \
+    _Pragma("unroll") for (int i = AP * (P); i < AP * (P) + AP; ++i)                \
       *reinterpret_cast<u32x4_t*>(sa_ + i * 32 * ROW_BYTES) = RA[i];                \
-    _Pragma("unroll") for (int i = BP * (P); i < BP * (P) + BP; ++i)                \
-      *reinterpret_cast<u32x4_t*>(sa_ + (BM + i * 32) * ROW_BYTES) = RB[i];         \
   }
 #define SEER_FLOAD(ST, KS, BUF)                                                     \
   {                                                                                 \
     const int chunk_ = ((2 * (KS) + fhalf) ^ fsw) << 4;                             \
-    _Pragma("unroll") for (int i = 0; i < 4; ++i) {                                 \
+    _Pragma("unroll") for (int i = 0; i < NI; ++i)                                  \
       af[BUF][i] = __builtin_bit_cast(bf16x8_t,                                     \
           *reinterpret_cast<const u32x4_t*>((ST) + a_row0 + i * 32 * ROW_BYTES + chunk_)); \
-      if (i < NJ)                                                                   \
-        bfr[BUF][i] = __builtin_bit_cast(bf16x8_t,                                  \
-            *reinterpret_cast<const u32x4_t*>((ST) + b_row0 + i * 32 * ROW_BYTES + chunk_)); \
-    }                                                                               \
   }
-  // One K tile of 4 slices x (4 NJ) MFMAs.  Each slice is its own scheduling
+  // One K tile of 4 slices x (NI x 2) MFMAs.  Each slice is its own scheduling
   // region (sched_barrier fences) holding the fragment reads of the next
   // slice -- issued first, paired with the first MFMAs, so they have the whole
-  // slice to land -- the global loads of one quarter of tile T+2 and its share
-  // of the LDS writes of tile T+1.  All of tile T+1 is written during slices
-  // 0-2, then one barrier: it publishes tile T+1 (so slice 3 can already read
-  // slice 0 of tile T+1 from the other stage) and, since every read of stage
-  // T%2 has been issued and waited for by then, it also orders those reads
-  // before tile T+2 overwrites the stage during the next tile.
-#define SEER_TILE(T, RA, RB, RN, RNB)                                               \
+  // slice to land -- the global loads of one quarter of A tile T+2 and of
+  // slice s of B tile T+1, and its share of the LDS writes of A tile T+1.  All
+  // of A tile T+1 is written during slices 0-2, then one barrier: it publishes
+  // tile T+1 (so slice 3 can already read slice 0 of tile T+1 from the other
+  // stage) and, since every read of stage T%2 has been issued and waited for
+  // by then, it also orders those reads before tile T+2 overwrites the stage
+  // during the next tile.
+#define SEER_TILE(T, RA, RN, BC, BNX)                                               \
   {                                                                                 \
     const uint8_t* st_ = smem + ((T) & 1) * STAGE_BYTES;                            \
     const uint8_t* sn_ = smem + (((T) + 1) & 1) * STAGE_BYTES;                      \
     _Pragma("unroll") for (int ks = 0; ks < 4; ++ks) {                              \
       const int cur = ks & 1;                                                       \
       SEER_FLOAD(ks < 3 ? st_ : sn_, ks < 3 ? ks + 1 : 0, cur ^ 1);                 \
-      SEER_GLOAD(RN, RNB, (T) + 2, ks);                                             \
-      _Pragma("unroll") for (int i = 0; i < 4; ++i)                                 \
-        _Pragma("unroll") for (int j = 0; j < NJ; ++j)                              \
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[cur][j], af[cur][i], acc[i][j], 0, 0, 0); \
-      if (ks < 2) SEER_LSTORE(RA, RB, ((T) + 1) & 1, ks);                           \
+      SEER_GLOAD_A(RN, (T) + 2, ks);                                                \
+      SEER_GLOAD_B(BNX, (T) + 1, ks);                                               \
+      _Pragma("unroll") for (int i = 0; i < NI; ++i)                                \
+        _Pragma("unroll") for (int j = 0; j < 2; ++j)                               \
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(BC[j][ks], af[cur][i], acc[i][j], 0, 0, 0); \
+      if (ks < 2) SEER_LSTORE(RA, ((T) + 1) & 1, ks);                               \
       if (ks == 2) {                                                                \
-        SEER_LSTORE(RA, RB, ((T) + 1) & 1, 2);                                      \
-        SEER_LSTORE(RA, RB, ((T) + 1) & 1, 3);                                      \
+        SEER_LSTORE(RA, ((T) + 1) & 1, 2);                                          \
+        SEER_LSTORE(RA, ((T) + 1) & 1, 3);                                          \
       }                                                                             \
-      seer_slice_schedule<BN>(ks);                                                \
+      seer_slice_schedule<BMT>(ks);                                                 \
       __builtin_amdgcn_sched_barrier(0);                                            \
       if (ks == 2) __syncthreads();                                                 \
     }                                                                               \
   }
 
-  // prologue: tile 0 -> stage 0 and its first slice into registers, tile 1 in
-  // registers (set 1); tile 2 is loaded into set 0 by the slices of tile 0
+  // prologue: A tile 0 -> stage 0 and its first slice into registers, A tile 1
+  // in registers (set 1), B tile 0 in register set 0; A tile 2 and B tile 1 are
+  // loaded by the slices of tile 0
 #pragma unroll
-  for (int q = 0; q < 4; ++q) SEER_GLOAD(ra0, rb0, 0, q);
+  for (int q = 0; q < 4; ++q) SEER_GLOAD_A(ra0, 0, q);
 #pragma unroll
-  for (int q = 0; q < 4; ++q) SEER_GLOAD(ra1, rb1, 1, q);
+  for (int q = 0; q < 4; ++q) SEER_GLOAD_B(bq0, 0, q);
 #pragma unroll
-  for (int q = 0; q < 4; ++q) SEER_LSTORE(ra0, rb0, 0, q);
+  for (int q = 0; q < 4; ++q) SEER_GLOAD_A(ra1, 1, q);
+#pragma unroll
+  for (int q = 0; q < 4; ++q) SEER_LSTORE(ra0, 0, q);
   __syncthreads();
   SEER_FLOAD(smem, 0, 0);
   for (int kt = 0; kt < KT; kt += 2) {
-    SEER_TILE(kt, ra1, rb1, ra0, rb0);
-    SEER_TILE(kt + 1, ra0, rb0, ra1, rb1);
+    SEER_TILE(kt, ra1, ra0, bq0, bq1);
+    SEER_TILE(kt + 1, ra0, ra1, bq1, bq0);
   }
-#undef SEER_GLOAD
+#undef SEER_GLOAD_A
+#undef SEER_GLOAD_B
 #undef SEER_LSTORE
 #undef SEER_FLOAD
 #undef SEER_TILE
@@ -262,65 +282,73 @@ __device__ __forceinline__ void gemm_tile(const GemmParams& p, uint8_t* smem, in
   // ---- epilogue -----------------------------------------------------------
   // The MFMAs take the B fragment as the matrix-core row operand, so tile
   // (i, j) accumulates the transposed 32x32 block: register r holds output
-  // row m0 + 128 wm + 32 i + lane%32 and column n0 + (BN/2) wn + 32 j + 8 (r/4) +
+  // row m0 + 32 i + lane%32 and packed column wcol + 32 j + 8 (r/4) +
   // 4 (lane/32) + r%4.  Each lane owns one row and four consecutive columns
   // per register quad; lanes l and l+32 hold the two halves of each 8-column
   // group.  Stores and residual loads move 16 bytes (8 columns) per lane, and
   // one v_permlane32_swap per register pair deals them between the two
-  // layouts.  For SWIGLU the gate/up tiles (j = 2h, 2h+1) sit in the same lane
+  // layouts.  For SWIGLU the gate/up tiles (j = 0, 1) sit in the same lane
   // and register; the near-zero count is a per-lane tally of its row, folded
   // over the lane pair.
   constexpr bool kGlu = (EPI == EPI_SWIGLU || EPI == EPI_SWIGLU_COUNT);
   constexpr bool kRes = (EPI == EPI_RESID || EPI == EPI_RESID_SPLIT || EPI == EPI_RESID_PAIR);
   constexpr bool kPair = EPI == EPI_RESID_PAIR;
+  constexpr bool kScale = EPI == EPI_SCALE || EPI == EPI_SCALE_ROPE;
   const int cq = 4 * fhalf;
   // Everything the epilogue reads besides the accumulators is requested ahead
-  // of its use: the row scales of the four 32-row blocks, and the residual
-  // columns of all four blocks (of two blocks ahead for a high/low pair).
-  // Fetched block by block between the stores, each block would wait out a
-  // full memory latency behind the previous block's stores.  Residual word jt
-  // of a block holds columns 16 jt + 8 (lane/32) .. +7 of the lane's row.
-  constexpr int NRQ = (kPair ? 2 : 1) * 2 * NJ;
-  constexpr int RDEPTH = kPair ? 2 : 4;
+  // of its use: the row scales of all 32-row blocks, and the residual columns
+  // of all blocks (of four blocks ahead for a high/low pair).  Fetched block
+  // by block between the stores, each block would wait out a full memory
+  // latency behind the previous block's stores.  Residual word jt of a block
+  // holds columns wcol + 16 jt + 8 (lane/32) .. +7 of the lane's row.
+  constexpr int NRQ = (kPair ? 2 : 1) * 4;
+  constexpr int RDEPTH = kPair ? (NI < 4 ? NI : 4) : NI;
   u32x4_t rq[RDEPTH][NRQ];
-  const int col0 = n0 + wn * (BN / 2) + cq;
-  const int colw = n0 + wn * (BN / 2) + 8 * fhalf;
+  const int colw = wcol + 8 * fhalf;
   auto fetch = [&](int i, u32x4_t* dst) {
-    int row = m0 + wm * 128 + i * 32 + fr;
+    int row = m0 + i * 32 + fr;
     row = row < M ? row : M - 1;             // rows past M are never stored
     if constexpr (kRes) {
       const uint16_t* rb = R + (size_t)row * p.ldr + colw;
 #pragma unroll
-      for (int jt = 0; jt < 2 * NJ; ++jt) dst[jt] = *reinterpret_cast<const u32x4_t*>(rb + 16 * jt);
+      for (int jt = 0; jt < 4; ++jt) dst[jt] = *reinterpret_cast<const u32x4_t*>(rb + 16 * jt);
     }
     if constexpr (kPair) {
       const uint16_t* rb = static_cast<const uint16_t*>(p.R2) + (size_t)row * p.ldr + colw;
 #pragma unroll
-      for (int jt = 0; jt < 2 * NJ; ++jt) dst[2 * NJ + jt] = *reinterpret_cast<const u32x4_t*>(rb + 16 * jt);
+      for (int jt = 0; jt < 4; ++jt) dst[4 + jt] = *reinterpret_cast<const u32x4_t*>(rb + 16 * jt);
     }
   };
-  float rsv[4];
+  float rsv[NI];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    int row = m0 + wm * 128 + i * 32 + fr;
+  for (int i = 0; i < NI; ++i) {
+    int row = m0 + i * 32 + fr;
     row = row < M ? row : M - 1;
-    rsv[i] = (EPI == EPI_SCALE || EPI == EPI_ARGMAX || kGlu) ? p.rs[row] : 1.0f;
+    rsv[i] = (kScale || EPI == EPI_ARGMAX || kGlu) ? p.rs[row] : 1.0f;
   }
   if constexpr (kRes) {
 #pragma unroll
     for (int i = 0; i < RDEPTH; ++i) fetch(i, rq[i]);
   }
-  // Rotary embedding of the q and k heads.  The wave's 128 columns are one
-  // head, and feature c of the head sits in tile j = c / 32, register
-  // 4 (c % 32 / 8) + c % 4 of lane half (c % 8) / 4; so the partner c + 64
-  // is in tile j + 2 of the same lane and register.
-  constexpr bool kRope = EPI == EPI_SCALE && BN == 256;
-  const bool rope_on = kRope && p.rope_pos != nullptr && n0 + wn * (BN / 2) < p.rope_col1;
-  int rpos[4] = {0, 0, 0, 0};
+  // Output column of block j.  Below perm_col1 the packed weight holds each
+  // 128-row head of q and k with its 32-row blocks in the order 0, 2, 1, 3, so
+  // the wave's two blocks are features (32 h, 64 + 32 h) of one head, h = the
+  // wave's 64-column half of the head: a rotary pair (c, c + 64) shares lane
+  // and register.
+  const bool perm = kScale && wcol < p.perm_col1;
+  const int hsel = (wcol >> 6) & 1;
+  int jcol[2];
+#pragma unroll
+  for (int j = 0; j < 2; ++j) jcol[j] = perm ? (wcol & ~127) + 32 * (hsel + 2 * j) : wcol + 32 * j;
+  constexpr bool kRope = EPI == EPI_SCALE_ROPE;
+  const bool rope_on = kRope && wcol < p.rope_col1;
+  int rpos[NI];
+#pragma unroll
+  for (int i = 0; i < NI; ++i) rpos[i] = 0;
   if (rope_on) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      int row = m0 + wm * 128 + i * 32 + fr;
+    for (int i = 0; i < NI; ++i) {
+      int row = m0 + i * 32 + fr;
       row = row < M ? row : M - 1;
       rpos[i] = p.rope_pos[row];
     }
@@ -328,22 +356,20 @@ __device__ __forceinline__ void gemm_tile(const GemmParams& p, uint8_t* smem, in
   auto rope_block = [&](int i) {
     const double pos = (double)rpos[i];
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
+    for (int q = 0; q < 4; ++q)
 #pragma unroll
-      for (int q = 0; q < 4; ++q)
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          double rv = pos * p.rope_freq[32 * j + 8 * q + cq + e];
-          rv -= floor(rv);
-          const float t = (float)rv;            // revolutions in [0, 1)
-          const float sn = __builtin_amdgcn_sinf(t), cs = __builtin_amdgcn_cosf(t);
-          const float a = acc[i][j][4 * q + e], b = acc[i][j + 2][4 * q + e];
-          acc[i][j][4 * q + e] = a * cs - b * sn;
-          acc[i][j + 2][4 * q + e] = b * cs + a * sn;
-        }
+      for (int e = 0; e < 4; ++e) {
+        double rv = pos * p.rope_freq[32 * hsel + 8 * q + cq + e];
+        rv -= floor(rv);
+        const float t = (float)rv;            // revolutions in [0, 1)
+        const float sn = __builtin_amdgcn_sinf(t), cs = __builtin_amdgcn_cosf(t);
+        const float a = acc[i][0][4 * q + e], b = acc[i][1][4 * q + e];
+        acc[i][0][4 * q + e] = a * cs - b * sn;
+        acc[i][1][4 * q + e] = b * cs + a * sn;
+      }
   };
   // V columns of the QKV projection are stored as fp16 (block-uniform)
-  const bool to_f16 = EPI == EPI_SCALE && p.f16_col0 > 0 && n0 >= p.f16_col0;
+  const bool to_f16 = kScale && p.f16_col0 > 0 && n0 >= p.f16_col0;
 
   // Stores: lanes l and l+32 hold the two 4-column halves of each 8-column
   // group of a row.  One v_permlane32_swap per packed register gives lane l
@@ -373,21 +399,21 @@ __device__ __forceinline__ void gemm_tile(const GemmParams& p, uint8_t* smem, in
   // type (F16 is the type of the whole block).
   auto store_block = [&](auto f16_tag, int i, const u32x4_t* rr) {
     constexpr bool F16 = decltype(f16_tag)::value;
-    const int row = m0 + wm * 128 + i * 32 + fr;
+    const int row = m0 + i * 32 + fr;
     if (row >= M) return;
     const float sc = rsv[i];
-    uint16_t* cw = C + (size_t)row * p.ldc + colw;
+    uint16_t* crow = C + (size_t)row * p.ldc + 8 * fhalf;
     uint16_t* cw2 = EPI == EPI_RESID_SPLIT ? static_cast<uint16_t*>(p.C2) + (size_t)row * p.ldc + colw : nullptr;
 #pragma unroll
-    for (int j = 0; j < NJ; ++j) {
+    for (int j = 0; j < 2; ++j) {
       uint2 rv[4], rv2[4];
       if constexpr (kRes) {
         split_pair(rr[2 * j], rv[0], rv[1]);
         split_pair(rr[2 * j + 1], rv[2], rv[3]);
       }
       if constexpr (kPair) {
-        split_pair(rr[2 * NJ + 2 * j], rv2[0], rv2[1]);
-        split_pair(rr[2 * NJ + 2 * j + 1], rv2[2], rv2[3]);
+        split_pair(rr[4 + 2 * j], rv2[0], rv2[1]);
+        split_pair(rr[4 + 2 * j + 1], rv2[2], rv2[3]);
       }
       uint2 pk[4], lo[4];
 #pragma unroll
@@ -395,7 +421,7 @@ __device__ __forceinline__ void gemm_tile(const GemmParams& p, uint8_t* smem, in
         float v[4];
 #pragma unroll
         for (int e = 0; e < 4; ++e) v[e] = acc[i][j][4 * q + e];
-        if constexpr (EPI == EPI_SCALE) {
+        if constexpr (kScale) {
 #pragma unroll
           for (int e = 0; e < 4; ++e) v[e] *= sc;
         }
@@ -409,8 +435,8 @@ __device__ __forceinline__ void gemm_tile(const GemmParams& p, uint8_t* smem, in
           lo[q].y = pack_bf2(v[2] - __uint_as_float(pk[q].y << 16), v[3] - __uint_as_float(pk[q].y & 0xffff0000u));
         }
       }
-      store_pair(cw + 32 * j, pk[0], pk[1]);
-      store_pair(cw + 32 * j + 16, pk[2], pk[3]);
+      store_pair(crow + jcol[j], pk[0], pk[1]);
+      store_pair(crow + jcol[j] + 16, pk[2], pk[3]);
       if constexpr (EPI == EPI_RESID_SPLIT) {
         store_pair(cw2 + 32 * j, lo[0], lo[1]);
         store_pair(cw2 + 32 * j + 16, lo[2], lo[3]);
@@ -419,53 +445,49 @@ __device__ __forceinline__ void gemm_tile(const GemmParams& p, uint8_t* smem, in
   };
 
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int row = m0 + wm * 128 + i * 32 + fr;
+  for (int i = 0; i < NI; ++i) {
+    const int row = m0 + i * 32 + fr;
     const bool ok = row < M;
     if constexpr (kGlu) {
       const float sc = rsv[i];
       int nz = 0;
+      uint2 pk[4];
 #pragma unroll
-      for (int h = 0; h < NJ / 2; ++h) {
-        const int col = (n0 + wn * (BN / 2)) / 2 + 32 * h + cq;
-        uint2 pk[4];
+      for (int q = 0; q < 4; ++q) {
+        float a[4];
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          float a[4];
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            a[e] = silu(acc[i][2 * h][4 * q + e] * sc) * (acc[i][2 * h + 1][4 * q + e] * sc);
-            // |a| < eps as the sign bit of |a| - eps: rounding keeps the sign of a
-            // difference and equality gives +0 (no compare, no SGPR hazard)
-            if constexpr (EPI == EPI_SWIGLU_COUNT) nz += __float_as_uint(fabsf(a[e]) - p.eps) >> 31;
-          }
-          pk[q].x = pack_bf2(a[0], a[1]);
-          pk[q].y = pack_bf2(a[2], a[3]);
+        for (int e = 0; e < 4; ++e) {
+          a[e] = silu(acc[i][0][4 * q + e] * sc) * (acc[i][1][4 * q + e] * sc);
+          // |a| < eps as the sign bit of |a| - eps: rounding keeps the sign of a
+          // difference and equality gives +0 (no compare, no SGPR hazard)
+          if constexpr (EPI == EPI_SWIGLU_COUNT) nz += __float_as_uint(fabsf(a[e]) - p.eps) >> 31;
         }
-        // the swaps are wave-wide: every lane takes part, rows past M store nothing
-        uint16_t* cw = C + (size_t)row * p.ldc + col - cq + 8 * fhalf;
-        const u32x2_t s0x = __builtin_amdgcn_permlane32_swap(pk[0].x, pk[1].x, false, false);
-        const u32x2_t s0y = __builtin_amdgcn_permlane32_swap(pk[0].y, pk[1].y, false, false);
-        const u32x2_t s1x = __builtin_amdgcn_permlane32_swap(pk[2].x, pk[3].x, false, false);
-        const u32x2_t s1y = __builtin_amdgcn_permlane32_swap(pk[2].y, pk[3].y, false, false);
-        if (ok) {
-          *reinterpret_cast<u32x4_t*>(cw) = u32x4_t{s0x[0], s0y[0], s0x[1], s0y[1]};
-          *reinterpret_cast<u32x4_t*>(cw + 16) = u32x4_t{s1x[0], s1y[0], s1x[1], s1y[1]};
-        }
+        pk[q].x = pack_bf2(a[0], a[1]);
+        pk[q].y = pack_bf2(a[2], a[3]);
+      }
+      // the swaps are wave-wide: every lane takes part, rows past M store nothing
+      uint16_t* cw = C + (size_t)row * p.ldc + (wcol >> 1) + 8 * fhalf;
+      const u32x2_t s0x = __builtin_amdgcn_permlane32_swap(pk[0].x, pk[1].x, false, false);
+      const u32x2_t s0y = __builtin_amdgcn_permlane32_swap(pk[0].y, pk[1].y, false, false);
+      const u32x2_t s1x = __builtin_amdgcn_permlane32_swap(pk[2].x, pk[3].x, false, false);
+      const u32x2_t s1y = __builtin_amdgcn_permlane32_swap(pk[2].y, pk[3].y, false, false);
+      if (ok) {
+        *reinterpret_cast<u32x4_t*>(cw) = u32x4_t{s0x[0], s0y[0], s0x[1], s0y[1]};
+        *reinterpret_cast<u32x4_t*>(cw + 16) = u32x4_t{s1x[0], s1y[0], s1x[1], s1y[1]};
       }
       if constexpr (EPI == EPI_SWIGLU_COUNT) {
         nz += __shfl_xor(nz, 32, kWave);
         if (ok && fhalf == 0) atomicAdd(p.cnt + row, nz);
       }
     } else if constexpr (EPI == EPI_ARGMAX) {
-      // the lane's 64 columns of its row in increasing order, so a strict >
+      // the lane's 32 columns of its row in increasing order, so a strict >
       // keeps the smallest column among equal maxima; then the lane pair
       const float sc = rsv[i];
-      const int cb = n0 + wn * (BN / 2) + cq;
+      const int cb = wcol + cq;
       float m = -INFINITY;
       int a = cb;
 #pragma unroll
-      for (int j = 0; j < NJ; ++j)
+      for (int j = 0; j < 2; ++j)
 #pragma unroll
         for (int q = 0; q < 4; ++q)
 #pragma unroll
@@ -475,7 +497,7 @@ __device__ __forceinline__ void gemm_tile(const GemmParams& p, uint8_t* smem, in
           }
       float sum = 0.0f;
 #pragma unroll
-      for (int j = 0; j < NJ; ++j)
+      for (int j = 0; j < 2; ++j)
 #pragma unroll
         for (int r = 0; r < 16; ++r) sum += __expf(acc[i][j][r] * sc - m);
       const float m2 = __shfl_xor(m, 32, kWave);
@@ -485,7 +507,7 @@ __device__ __forceinline__ void gemm_tile(const GemmParams& p, uint8_t* smem, in
       const float st = sum * __expf(m - mm) + s2 * __expf(m2 - mm);
       const int at = (m2 > m || (m2 == m && a2 < a)) ? a2 : a;
       if (ok && fhalf == 0) {
-        ArgmaxPartial* dst = static_cast<ArgmaxPartial*>(p.C) + (size_t)row * p.ldc + (n0 + wn * (BN / 2)) / 128;
+        ArgmaxPartial* dst = static_cast<ArgmaxPartial*>(p.C) + (size_t)row * p.ldc + (wcol >> 6);
         *reinterpret_cast<u32x4_t*>(dst) = u32x4_t{__float_as_uint(mm), __float_as_uint(st), (uint32_t)at, 0u};
       }
     } else {
@@ -493,13 +515,13 @@ __device__ __forceinline__ void gemm_tile(const GemmParams& p, uint8_t* smem, in
         if (rope_on) rope_block(i);
       }
       const u32x4_t* rr = rq[i % RDEPTH];
-      if (EPI == EPI_SCALE && to_f16)
+      if (kScale && to_f16)
         store_block(std::true_type{}, i, rr);
       else
         store_block(std::false_type{}, i, rr);
-      // high/low residuals: the block two ahead goes into the buffer just used
+      // high/low residuals: the block RDEPTH ahead goes into the buffer just used
       if constexpr (kPair) {
-        if (i + RDEPTH < 4) fetch(i + RDEPTH, rq[i % RDEPTH]);
+        if (i + RDEPTH < NI) fetch(i + RDEPTH, rq[i % RDEPTH]);
       }
     }
   }
@@ -507,15 +529,15 @@ __device__ __forceinline__ void gemm_tile(const GemmParams& p, uint8_t* smem, in
 
 // Units of work: the 256x256 tiles, except that when the tiles leave a last
 // round of r < n_units/2 tiles on the n_units workgroups that run at once,
-// each of those r tiles becomes two 256x128 halves (disjoint outputs, no
+// each of those r tiles becomes two 128x256 halves (disjoint outputs, no
 // reduction), so the last round keeps twice as many CUs busy.  Tile geometry
 // follows the real row count read on the device; surplus blocks of the
-// upper-bound grid exit at once.
+// upper-bound grid, and halves that start past the last row, exit at once.
 template <int EPI>
 __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmParams p) {
-  __shared__ __attribute__((aligned(1024))) uint8_t smem[2 * (BM + 256) * ROW_BYTES];
+  __shared__ __attribute__((aligned(1024))) uint8_t smem[2 * 256 * ROW_BYTES];
   const int M = rows_from(p.m_ptr, p.m_ub);
-  const int tiles_m = (M + BM - 1) / BM;
+  const int tiles_m = (M + 255) / 256;
   const int tiles_n = p.N / 256;
   const int ntiles = tiles_m * tiles_n;
   int full = ntiles;
@@ -528,25 +550,30 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmParams p) {
   int tm, tn;
   if (u < full) {
     raster(xcd_remap(u, full), tiles_m, tiles_n, tm, tn);
-    gemm_tile<EPI, 256>(p, smem, M, tm * BM, tn * 256);
+    gemm_tile<EPI, 256>(p, smem, M, tm * 256, tn * 256);
   } else {
     const int v = u - full;
     raster(full + (v >> 1), tiles_m, tiles_n, tm, tn);
-    gemm_tile<EPI, 128>(p, smem, M, tm * BM, tn * 256 + (v & 1) * 128);
+    const int m0 = tm * 256 + (v & 1) * 128;
+    if (m0 >= M) return;
+    gemm_tile<EPI, 128>(p, smem, M, m0, tn * 256);
   }
 }
 
 int launch_gemm_bf16(int epi, const GemmParams& p, hipStream_t s) {
-  // the rotary pairs of a head span both column halves of a 256x128 unit, and
-  // the argmax partials are per 128 columns of a 256-wide tile
-  if (p.rope_pos && (epi != EPI_SCALE || p.n_units > 0 || p.rope_col1 % 128 != 0)) return -1;
-  if (epi == EPI_ARGMAX && p.n_units > 0) return -1;
-  const int tiles_m = (p.m_ub + BM - 1) / BM;
+  // the head permutation and the rotary pairs work on whole 128-wide heads of
+  // the SCALE epilogues, and rotation needs the permuted layout
+  const bool scale = epi == EPI_SCALE || epi == EPI_SCALE_ROPE;
+  if (p.perm_col1 && (!scale || p.perm_col1 % 128 != 0)) return -1;
+  if ((epi == EPI_SCALE_ROPE) != (p.rope_pos != nullptr)) return -1;
+  if (p.rope_pos && (!p.rope_freq || p.rope_col1 % 128 != 0 || p.rope_col1 > p.perm_col1)) return -1;
+  const int tiles_m = (p.m_ub + 255) / 256;
   const int tiles_n = p.N / 256;
   // the split last round adds at most n_units / 2 units
   dim3 grid(tiles_m * tiles_n + (p.n_units > 0 ? p.n_units / 2 : 0)), block(NT);
   switch (epi) {
     case EPI_SCALE: hipLaunchKernelGGL(gemm_bf16_kernel<EPI_SCALE>, grid, block, 0, s, p); break;
+    case EPI_SCALE_ROPE: hipLaunchKernelGGL(gemm_bf16_kernel<EPI_SCALE_ROPE>, grid, block, 0, s, p); break;
     case EPI_RESID: hipLaunchKernelGGL(gemm_bf16_kernel<EPI_RESID>, grid, block, 0, s, p); break;
     case EPI_SWIGLU: hipLaunchKernelGGL(gemm_bf16_kernel<EPI_SWIGLU>, grid, block, 0, s, p); break;
     case EPI_SWIGLU_COUNT:

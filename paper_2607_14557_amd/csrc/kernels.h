@@ -6,18 +6,19 @@
 
 namespace seer {
 
-// SCALE: C = acc * rs[r]; RESID: C = R + acc; SWIGLU(_COUNT): gate/up pairs;
+// SCALE: C = acc * rs[r]; SCALE_ROPE: SCALE with the rotary embedding of the
+// columns < rope_col1 (bf16 only); RESID: C = R + acc; SWIGLU(_COUNT): gate/up pairs;
 // RESID_SPLIT: v = R + acc, C = bf16(v), C2 = bf16(v - C) (bf16 only);
 // RESID_PAIR: C = bf16(R + R2 + acc) (bf16 only);
-// ARGMAX: no output matrix; per row and 128-column block of l = acc * rs[r],
+// ARGMAX: no output matrix; per row and 64-column block of l = acc * rs[r],
 // the partial {max, sum exp(l - max), argmax column} (bf16 only, see
 // ArgmaxPartial).
 enum Epilogue {
   EPI_SCALE = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_SWIGLU_COUNT = 3,
-  EPI_RESID_SPLIT = 4, EPI_RESID_PAIR = 5, EPI_ARGMAX = 6
+  EPI_RESID_SPLIT = 4, EPI_RESID_PAIR = 5, EPI_ARGMAX = 6, EPI_SCALE_ROPE = 7
 };
 
-// One row's partial over 128 columns (EPI_ARGMAX): C is ArgmaxPartial[M][N/128].
+// One row's partial over 64 columns (EPI_ARGMAX): C is ArgmaxPartial[M][N/64].
 struct ArgmaxPartial {
   float max;
   float sum;     // sum of exp(l - max) over the block
@@ -51,15 +52,39 @@ struct GemmParams {
   // tiles leave a last round of r <= n_units / 2 tiles, those r tiles run as
   // 2 r halves of 256x128.  0 disables the split.
   int n_units;
-  // bf16 SCALE only: rotary embedding of output columns < rope_col1 (whole
-  // 128-wide heads): row r's pair (c, c + 64) of each head is rotated by
-  // 2 pi * frac(rope_pos[r] * rope_freq[c % 64]); null: none
+  // bf16 SCALE_ROPE only (and required there): rotary embedding of output
+  // columns < rope_col1 (whole 128-wide heads): row r's pair (c, c + 64) of
+  // each head is rotated by 2 pi * frac(rope_pos[r] * rope_freq[c % 64])
   const int* rope_pos;
   const double* rope_freq;
   int rope_col1;
+  // bf16 SCALE(_ROPE) only: output columns < perm_col1 (whole 128-wide heads) come
+  // from weight rows packed in head-block order 0, 2, 1, 3 (qk_packed_row)
+  // and are stored back in head order; 0 means none.  rope_col1 <= perm_col1.
+  int perm_col1;
 };
 
+// Weight layout of the bf16 GEMM's B operand ("fragment-major"): element
+// (n, k) of a [N, K] matrix (N % 32 == 0, K % 16 == 0) sits at this index, so
+// the 32x32x16 MFMA operand of 32 columns and one 16-wide K slice is one
+// 1 KiB block holding lane l's 8 values (column n % 32 = l % 32, k % 16 in
+// 8 (l / 32) .. +7) at 16 l bytes.
+__host__ __device__ inline size_t frag_b_index(size_t n, size_t k, size_t K) {
+  return ((n / 32) * (K / 16) + k / 16) * 512 + (((k % 16) / 8) * 32 + n % 32) * 8 + k % 8;
+}
+
+// Packed q/k row r (r < 2 d) holds weight row qk_packed_row(r): within each
+// 128-row head the 32-row blocks are in the order 0, 2, 1, 3 (an involution),
+// so one wave's 64 output columns hold the rotary pairs (c, c + 64) of a head.
+__host__ __device__ inline size_t qk_packed_row(size_t r) {
+  const size_t b = (r >> 5) & 3;
+  const size_t nb = b == 1 ? 2 : (b == 2 ? 1 : b);
+  return (r & ~(size_t)127) + nb * 32 + (r & 31);
+}
+
 // bf16 operands; requires N % 256 == 0, K % 128 == 0, 16-byte aligned rows.
+// B is fragment-major (frag_b_index) for every epilogue but ARGMAX, whose B
+// is an ordinary row-major [N, K] matrix (ldb).
 // For SWIGLU*, N is the packed 2*I and C has I columns.
 int launch_gemm_bf16(int epi, const GemmParams& p, hipStream_t s);
 

@@ -359,9 +359,11 @@ int launch_repack(const RepackParams& p, hipStream_t s) {
 }
 
 // ---------------------------------------------------------------------------
-// Weight prepack.  bf16: [Wq;Wk;Wv] (3d x d), Wo, gate/up interleaved in
-// blocks of 32 rows (2I x d), Wd.  fp32: [Wq;Wk;Wv], Wo, Wg, Wu, Wd.  RMSNorm
-// gains multiply the input columns of the projections they feed.
+// Weight prepack.  bf16: [Wq;Wk;Wv] (3d x d, the q and k rows of each head in
+// block order 0, 2, 1, 3: qk_packed_row), Wo, gate/up interleaved in blocks of
+// 32 rows (2I x d), Wd, each stored fragment-major (frag_b_index).  fp32:
+// [Wq;Wk;Wv], Wo, Wg, Wu, Wd, row-major.  RMSNorm gains multiply the input
+// columns of the projections they feed.
 PackedLayout packed_layout(int d, int d_ff, bool bf16) {
   const size_t es = bf16 ? 2 : 4;
   auto up = [](size_t n) { return (n + 127) / 128 * 128; };
@@ -383,11 +385,12 @@ __global__ void prepack_kernel(PrepackParams p, PackedLayout L) {
     if constexpr (BF16) return bf2f(static_cast<const uint16_t*>(src)[idx]);
     else return static_cast<const float*>(src)[idx];
   };
-  auto st = [&](size_t idx, float v, const void* src, size_t sidx, bool scaled) {
+  // packed element (r, k) of a [rows, K] block at base
+  auto st = [&](size_t base, size_t r, size_t k, size_t K, float v, const void* src, size_t sidx, bool scaled) {
     if constexpr (BF16) {
-      dst[idx] = scaled ? f2bf(v) : static_cast<const uint16_t*>(src)[sidx];
+      dst[base + frag_b_index(r, k, K)] = scaled ? f2bf(v) : static_cast<const uint16_t*>(src)[sidx];
     } else {
-      dst[idx] = v;
+      dst[base + r * K + k] = v;
     }
   };
   const size_t stride = (size_t)gridDim.x * blockDim.x;
@@ -395,12 +398,13 @@ __global__ void prepack_kernel(PrepackParams p, PackedLayout L) {
   // q, k, v
   for (size_t e = start; e < (size_t)3 * d * d; e += stride) {
     const size_t r = e / d, k = e % d;
-    const void* src = r < (size_t)d ? p.wq : (r < (size_t)2 * d ? p.wk : p.wv);
-    const size_t sidx = (r % d) * d + k;
+    const size_t wr = (BF16 && r < (size_t)2 * d) ? qk_packed_row(r) : r;
+    const void* src = wr < (size_t)d ? p.wq : (wr < (size_t)2 * d ? p.wk : p.wv);
+    const size_t sidx = (wr % d) * d + k;
     const float g = p.g1 ? p.g1[k] : 1.0f;
-    st(L.qkv + e, ld(src, sidx) * g, src, sidx, p.g1 != nullptr);
+    st(L.qkv, r, k, d, ld(src, sidx) * g, src, sidx, p.g1 != nullptr);
   }
-  for (size_t e = start; e < (size_t)d * d; e += stride) st(L.o + e, ld(p.wo, e), p.wo, e, false);
+  for (size_t e = start; e < (size_t)d * d; e += stride) st(L.o, e / d, e % d, d, ld(p.wo, e), p.wo, e, false);
   for (size_t e = start; e < (size_t)2 * I * d; e += stride) {
     const size_t r = e / d, k = e % d;
     const void* src;
@@ -415,9 +419,9 @@ __global__ void prepack_kernel(PrepackParams p, PackedLayout L) {
     }
     const size_t sidx = sr * d + k;
     const float g = p.g2 ? p.g2[k] : 1.0f;
-    st(L.gu + e, ld(src, sidx) * g, src, sidx, p.g2 != nullptr);
+    st(L.gu, r, k, d, ld(src, sidx) * g, src, sidx, p.g2 != nullptr);
   }
-  for (size_t e = start; e < (size_t)d * I; e += stride) st(L.dn + e, ld(p.wd, e), p.wd, e, false);
+  for (size_t e = start; e < (size_t)d * I; e += stride) st(L.dn, e / I, e % I, I, ld(p.wd, e), p.wd, e, false);
 }
 
 int launch_prepack(const PrepackParams& p, hipStream_t s) {

@@ -96,7 +96,7 @@ extern "C" {
 
 const char* seer_last_error(void) { return g_err.c_str(); }
 
-int32_t seer_abi_version(void) { return 101; }
+int32_t seer_abi_version(void) { return 102; }
 
 size_t seer_prepacked_bytes(const seer_dims* dims) {
   if (check_dims(dims) != SEER_OK) return 0;
@@ -216,13 +216,12 @@ static int layer_forward_impl(const seer_dims* dims, const void* w_packed, const
     g.m_ptr = m_ptr; g.m_ub = R; g.N = 3 * d; g.K = d;
     g.lda = d; g.ldb = d; g.ldc = 3 * d;
     g.f16_col0 = bf16 ? 2 * d : 0;     // V goes to the attention's fp16 PV product
+    g.perm_col1 = bf16 ? 2 * d : 0;    // q and k rows are packed head-permuted
     if (rope && bf16) {
-      // q and k rotated in the epilogue; the rotary pairs need whole 256-wide
-      // tiles, so no split last round
+      // q and k rotated in the epilogue, where each lane holds rotary pairs
       g.rope_pos = rpos; g.rope_freq = rfreq; g.rope_col1 = 2 * d;
-      g.n_units = 0;
     }
-    if (gemm(seer::EPI_SCALE, g, stream)) return hip_fail("qkv gemm launch");
+    if (gemm(rope && bf16 ? seer::EPI_SCALE_ROPE : seer::EPI_SCALE, g, stream)) return hip_fail("qkv gemm launch");
     if (rope && !bf16 &&
         seer::launch_rope_f32(static_cast<float*>(qkv), d, dims->n_heads, dims->head_dim, m_ptr, R, rpos, rfreq,
                               stream))
@@ -413,7 +412,7 @@ static size_t lm_partials_offset(int32_t rows_ub) { return up256((size_t)rows_ub
 
 size_t seer_lm_head_workspace_bytes(const seer_dims* dims, int32_t vocab, int32_t rows_ub) {
   if (check_dims(dims) != SEER_OK || vocab <= 0 || rows_ub < 0) return 0;
-  return lm_partials_offset(rows_ub) + up256((size_t)rows_ub * (size_t)(vocab / 128) * sizeof(seer::ArgmaxPartial));
+  return lm_partials_offset(rows_ub) + up256((size_t)rows_ub * (size_t)(vocab / 64) * sizeof(seer::ArgmaxPartial));
 }
 
 int seer_lm_head_predict(const seer_dims* dims, const void* w_lm, int32_t vocab, const void* x, int32_t rows_ub,
@@ -442,10 +441,10 @@ int seer_lm_head_predict(const seer_dims* dims, const void* w_lm, int32_t vocab,
   seer::GemmParams g{};
   g.A = x; g.B = w_lm; g.C = part; g.rs = inv;
   g.m_ptr = m_ptr; g.m_ub = rows_ub; g.N = vocab; g.K = d;
-  g.lda = d; g.ldb = d; g.ldc = vocab / 128;
-  g.n_units = 0;                        // partials per 128 columns of whole 256-wide tiles
+  g.lda = d; g.ldb = d; g.ldc = vocab / 64;   // one partial per row and 64 columns
+  g.n_units = 0;
   if (seer::launch_gemm_bf16(seer::EPI_ARGMAX, g, stream)) return hip_fail("lm head gemm launch");
-  if (seer::launch_argmax_reduce(part, vocab / 128, m_ptr, rows_ub, pred, conf, stream))
+  if (seer::launch_argmax_reduce(part, vocab / 64, m_ptr, rows_ub, pred, conf, stream))
     return hip_fail("argmax reduce launch");
   return ok();
 }

@@ -34,7 +34,7 @@ def test_every_declared_symbol_is_exported(S):
     for n in names:
         assert hasattr(lib, n), n
     assert set(names) == set(S.EXPORTED)
-    assert S.seer_abi_version() == 101
+    assert S.seer_abi_version() == 102
 
 
 def dims(S, d=4096, h=32, dh=128, i=12288, dtype=1):
