@@ -331,16 +331,25 @@ int seer_batch_repack(const seer_repack_desc* desc, const void* const* src,
  * this follows the low-confidence remasking of the LLaDA family with a random
  * head.  bf16 layers only.
  *
+ * seer_lm_head_prepack: copy the head weight w_lm [vocab, d] (device, bf16,
+ * row-major [out, in]) into `dst` (device, at least vocab * d * 2 bytes,
+ * 256-byte aligned) in the matrix cores' operand order, the form
+ * seer_lm_head_predict reads (same layout as the packed layer weights: one
+ * 1 KiB block per 32 vocabulary rows and 16 input columns).  Once per head.
+ * Errors: EINVAL (null pointers, alignment, dst_bytes too small),
+ * EUNSUPPORTED (fp32, vocab, 4 GiB or more).
+ *
  * seer_lm_head_predict: for rows r < cu_seqlens[batch] of x [rows_ub, d]:
  * logits l = RMSNorm(x_r) (unit gain, dims->rms_eps) . w_lm^T, w_lm [vocab, d]
- * bf16 ([out, in]); pred[r] = argmax_v l_v (the smallest v among equal
+ * bf16 ([out, in]) as packed by seer_lm_head_prepack (w_packed);
+ * pred[r] = argmax_v l_v (the smallest v among equal
  * maxima), conf[r] = its softmax probability 1 / sum_v exp(l_v - l_max).
  * Logits are fp32 (bf16 products, fp32 accumulation) and never stored: the
  * GEMM epilogue keeps a {max, sum exp, argmax} partial per row and 64
  * columns, merged by a second kernel.  vocab % 256 == 0.  Workspace: at
  * least seer_lm_head_workspace_bytes(dims, vocab, rows_ub), 256-byte aligned.
  * Errors: EINVAL (null pointers, sizes < 1, alignment), EUNSUPPORTED (fp32,
- * vocab, w_lm or x of 4 GiB or more), EWORKSPACE.
+ * vocab, w_packed or x of 4 GiB or more), EWORKSPACE.
  *
  * seer_remask_step: per sequence b (rows [cu_seqlens[b], cu_seqlens[b+1]), the
  * first min(seqused[b], max_used) of them real; seqused may be NULL): among
@@ -352,7 +361,9 @@ int seer_batch_repack(const seer_repack_desc* desc, const void* const* src,
  * row's x0 row is never read again).  max_used <= 8192.  Errors: EINVAL,
  * EUNSUPPORTED (fp32, max_used). */
 size_t seer_lm_head_workspace_bytes(const seer_dims* dims, int32_t vocab, int32_t rows_ub);
-int seer_lm_head_predict(const seer_dims* dims, const void* w_lm, int32_t vocab, const void* x, int32_t rows_ub,
+int seer_lm_head_prepack(const seer_dims* dims, const void* w_lm, int32_t vocab, void* dst, size_t dst_bytes,
+                         hipStream_t stream);
+int seer_lm_head_predict(const seer_dims* dims, const void* w_packed, int32_t vocab, const void* x, int32_t rows_ub,
                          const int32_t* cu_seqlens, int32_t batch, int32_t* pred, float* conf, void* workspace,
                          size_t workspace_bytes, hipStream_t stream);
 int seer_remask_step(const seer_dims* dims, const int32_t* cu_seqlens, const int32_t* seqused, int32_t batch,

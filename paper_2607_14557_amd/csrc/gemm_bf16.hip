@@ -37,7 +37,7 @@
 //   SWIGLU_COUNT  as SWIGLU, plus the per-row count of |act| < eps on the
 //           fp32 values (per-lane tally, one atomic per row and wave)
 //   ARGMAX  per row and 64-column group {max, sum exp(v - max), first argmax}
-//           of acc * rowscale (LM head); B is the caller's row-major matrix
+//           of acc * rowscale (LM head)
 #include <type_traits>
 
 #include "common.h"
@@ -126,7 +126,6 @@ __device__ __forceinline__ void gemm_tile(const GemmParams& p, uint8_t* smem, in
   constexpr int NI = BMT / 32;                      // 32-row MFMA tiles per wave = A chunks per thread
   constexpr int AP = NI / 4;                        // ... per slice
   constexpr int STAGE_BYTES = BMT * ROW_BYTES;
-  constexpr bool kFragB = EPI != EPI_ARGMAX;        // packed weight, or the caller's row-major matrix
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -164,19 +163,14 @@ __device__ __forceinline__ void gemm_tile(const GemmParams& p, uint8_t* smem, in
   const int a_row0 = fr * ROW_BYTES;
 
   // ---- B: straight into the operand registers -----------------------------
-  // Column block j of the wave: lane l takes column wcol + 32 j + l%32.
-  // Fragment-major, its operand of K slice s is the 16 bytes at 16 l of block
-  // (col / 32) * (K / 16) + s; row-major, the 16 bytes at K offset 16 s + 8 (l/32).
+  // Column block j of the wave: lane l takes column wcol + 32 j + l%32.  In
+  // the fragment-major weight, its operand of K slice s is the 16 bytes at
+  // 16 l of the 1 KiB block (col / 32) * (K / 16) + s.
   uint32_t b_off[2];
 #pragma unroll
-  for (int j = 0; j < 2; ++j) {
-    if constexpr (kFragB)
-      b_off[j] = (uint32_t)((wcol >> 5) + j) * (uint32_t)(p.K >> 4) * 1024u + (uint32_t)lane * 16u;
-    else
-      b_off[j] = (uint32_t)(wcol + 32 * j + fr) * (uint32_t)p.ldb * 2u + (uint32_t)fhalf * 16u;
-  }
-  constexpr uint32_t B_TILE = kFragB ? 4096u : 128u;
-  constexpr uint32_t B_SLICE = kFragB ? 1024u : 32u;
+  for (int j = 0; j < 2; ++j) b_off[j] = (uint32_t)((wcol >> 5) + j) * (uint32_t)(p.K >> 4) * 1024u + (uint32_t)lane * 16u;
+  constexpr uint32_t B_TILE = 4096u;                // bytes of B per K tile and column block
+  constexpr uint32_t B_SLICE = 1024u;
 
   f32x16_t acc[NI][2];
 #pragma unroll

@@ -83,8 +83,7 @@ __host__ __device__ inline size_t qk_packed_row(size_t r) {
 }
 
 // bf16 operands; requires N % 256 == 0, K % 128 == 0, 16-byte aligned rows.
-// B is fragment-major (frag_b_index) for every epilogue but ARGMAX, whose B
-// is an ordinary row-major [N, K] matrix (ldb).
+// B is fragment-major (frag_b_index); ldb is unused.
 // For SWIGLU*, N is the packed 2*I and C has I columns.
 int launch_gemm_bf16(int epi, const GemmParams& p, hipStream_t s);
 
@@ -234,5 +233,9 @@ struct PackedLayout {
 };
 PackedLayout packed_layout(int d, int d_ff, bool bf16);
 int launch_prepack(const PrepackParams& p, hipStream_t s);
+
+// Copy a row-major bf16 matrix src [N, K] (N % 32 == 0, K % 16 == 0) to dst
+// in the fragment-major order of frag_b_index.
+int launch_pack_frag(const void* src, int N, int K, void* dst, hipStream_t s);
 
 }  // namespace seer

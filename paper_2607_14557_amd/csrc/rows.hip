@@ -432,6 +432,26 @@ int launch_prepack(const PrepackParams& p, hipStream_t s) {
   return hipGetLastError() == hipSuccess ? 0 : -1;
 }
 
+// One 16-byte destination chunk per thread: chunk c is lane c % 64 of block
+// c / 64, i.e. 8 consecutive K values of one row, a 16-byte run of the source.
+__global__ void pack_frag_kernel(const uint4* src, int N, int K, uint4* dst) {
+  const size_t n_chunks = (size_t)N * K / 8;
+  const size_t kb = (size_t)K / 16;
+  for (size_t c = (size_t)blockIdx.x * blockDim.x + threadIdx.x; c < n_chunks; c += (size_t)gridDim.x * blockDim.x) {
+    const size_t blk = c / 64, l = c % 64;
+    const size_t n = (blk / kb) * 32 + l % 32;
+    const size_t k = (blk % kb) * 16 + (l / 32) * 8;
+    dst[c] = src[(n * K + k) / 8];
+  }
+}
+
+int launch_pack_frag(const void* src, int N, int K, void* dst, hipStream_t s) {
+  if (N % 32 != 0 || K % 16 != 0) return -1;
+  hipLaunchKernelGGL(pack_frag_kernel, dim3(4096), dim3(256), 0, s, static_cast<const uint4*>(src), N, K,
+                     static_cast<uint4*>(dst));
+  return hipGetLastError() == hipSuccess ? 0 : -1;
+}
+
 // ---------------------------------------------------------------------------
 // LM-head prediction: one wave per row merges the row's 128-column partials
 // in column order (a strict > keeps the smallest column among equal maxima).

@@ -415,21 +415,41 @@ size_t seer_lm_head_workspace_bytes(const seer_dims* dims, int32_t vocab, int32_
   return lm_partials_offset(rows_ub) + up256((size_t)rows_ub * (size_t)(vocab / 64) * sizeof(seer::ArgmaxPartial));
 }
 
-int seer_lm_head_predict(const seer_dims* dims, const void* w_lm, int32_t vocab, const void* x, int32_t rows_ub,
-                         const int32_t* cu_seqlens, int32_t batch, int32_t* pred, float* conf, void* workspace,
-                         size_t workspace_bytes, hipStream_t stream) {
+// shape checks shared by the head's two calls
+static int check_head(const seer_dims* dims, int32_t vocab, const char* what) {
   int rc = check_dims(dims);
   if (rc) return rc;
   if (dims->dtype != SEER_DTYPE_BF16) return fail(SEER_EUNSUPPORTED, "the LM head runs on bf16 layers only");
-  if (!w_lm || !x || !cu_seqlens || !pred || !conf || !workspace)
-    return fail(SEER_EINVAL, "a required pointer is NULL");
   if (vocab <= 0 || vocab % 256 != 0) return fail(SEER_EUNSUPPORTED, "vocab must be a positive multiple of 256 (got %d)", vocab);
-  if (batch < 1 || rows_ub < 1) return fail(SEER_EINVAL, "batch and rows_ub must be >= 1");
   // the GEMM addresses its operands with 32-bit byte offsets
-  if ((size_t)vocab * dims->d_model * 2 >= ((size_t)1 << 32) || (size_t)rows_ub * dims->d_model * 2 >= ((size_t)1 << 32))
-    return fail(SEER_EUNSUPPORTED, "w_lm and x must each stay below 4 GiB");
-  if (!aligned(w_lm, 16) || !aligned(x, 16) || !aligned(workspace, 256))
-    return fail(SEER_EINVAL, "w_lm and x need 16-byte, workspace 256-byte alignment");
+  if ((size_t)vocab * dims->d_model * 2 >= ((size_t)1 << 32))
+    return fail(SEER_EUNSUPPORTED, "%s must stay below 4 GiB", what);
+  return SEER_OK;
+}
+
+int seer_lm_head_prepack(const seer_dims* dims, const void* w_lm, int32_t vocab, void* dst, size_t dst_bytes,
+                         hipStream_t stream) {
+  int rc = check_head(dims, vocab, "w_lm");
+  if (rc) return rc;
+  if (!w_lm || !dst) return fail(SEER_EINVAL, "w_lm/dst is NULL");
+  if (!aligned(w_lm, 16) || !aligned(dst, 256)) return fail(SEER_EINVAL, "w_lm needs 16-byte, dst 256-byte alignment");
+  const size_t need = (size_t)vocab * dims->d_model * 2;
+  if (dst_bytes < need) return fail(SEER_EINVAL, "dst holds %zu bytes, need %zu", dst_bytes, need);
+  if (seer::launch_pack_frag(w_lm, vocab, dims->d_model, dst, stream)) return hip_fail("pack launch");
+  return ok();
+}
+
+int seer_lm_head_predict(const seer_dims* dims, const void* w_packed, int32_t vocab, const void* x, int32_t rows_ub,
+                         const int32_t* cu_seqlens, int32_t batch, int32_t* pred, float* conf, void* workspace,
+                         size_t workspace_bytes, hipStream_t stream) {
+  int rc = check_head(dims, vocab, "the packed head weight");
+  if (rc) return rc;
+  if (!w_packed || !x || !cu_seqlens || !pred || !conf || !workspace)
+    return fail(SEER_EINVAL, "a required pointer is NULL");
+  if (batch < 1 || rows_ub < 1) return fail(SEER_EINVAL, "batch and rows_ub must be >= 1");
+  if ((size_t)rows_ub * dims->d_model * 2 >= ((size_t)1 << 32)) return fail(SEER_EUNSUPPORTED, "x must stay below 4 GiB");
+  if (!aligned(w_packed, 16) || !aligned(x, 16) || !aligned(workspace, 256))
+    return fail(SEER_EINVAL, "w_packed and x need 16-byte, workspace 256-byte alignment");
   const size_t need = seer_lm_head_workspace_bytes(dims, vocab, rows_ub);
   if (workspace_bytes < need) return fail(SEER_EWORKSPACE, "workspace holds %zu bytes, need %zu", workspace_bytes, need);
   uint8_t* ws = static_cast<uint8_t*>(workspace);
@@ -439,7 +459,7 @@ int seer_lm_head_predict(const seer_dims* dims, const void* w_lm, int32_t vocab,
   const int d = dims->d_model;
   if (seer::launch_rms_inv(true, x, d, d, m_ptr, rows_ub, dims->rms_eps, inv, stream)) return hip_fail("rms launch");
   seer::GemmParams g{};
-  g.A = x; g.B = w_lm; g.C = part; g.rs = inv;
+  g.A = x; g.B = w_packed; g.C = part; g.rs = inv;
   g.m_ptr = m_ptr; g.m_ub = rows_ub; g.N = vocab; g.K = d;
   g.lda = d; g.ldb = d; g.ldc = vocab / 64;   // one partial per row and 64 columns
   g.n_units = 0;

@@ -171,9 +171,14 @@ class SyntheticSampler:
 
     def __init__(self, dims, w_lm, emb, rows_ub, device="cuda"):
         self.dims = dims
-        self.w_lm, self.emb = w_lm, emb
+        self.emb = emb
         self.vocab = int(w_lm.shape[0])
         self.rows_ub = int(rows_ub)
+        # the head weight in the matrix cores' operand order (the row-major
+        # w_lm is not kept)
+        self.w_packed = torch.empty(w_lm.numel() * 2, dtype=torch.uint8, device=device)
+        S.seer_lm_head_prepack(dims, w_lm, self.vocab, self.w_packed)
+        torch.cuda.current_stream(self.w_packed.device).synchronize()   # later calls may use other streams
         self.ws_bytes = S.seer_lm_head_workspace_bytes(dims, self.vocab, self.rows_ub)
         self.workspace = torch.empty(self.ws_bytes, dtype=torch.uint8, device=device)
         self.pred = torch.empty(self.rows_ub, dtype=torch.int32, device=device)
@@ -184,7 +189,7 @@ class SyntheticSampler:
         self.tokens.fill_(-1)
 
     def predict(self, h, cu, batch, rows_ub, stream=None):
-        S.seer_lm_head_predict(self.dims, self.w_lm, self.vocab, h, rows_ub, cu, batch, self.pred, self.conf,
+        S.seer_lm_head_predict(self.dims, self.w_packed, self.vocab, h, rows_ub, cu, batch, self.pred, self.conf,
                                self.workspace, self.ws_bytes, stream=stream)
 
     def step(self, h, cu, used, batch, rows_ub, x0, x_next, steps_left, max_used, stream=None):

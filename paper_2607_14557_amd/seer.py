@@ -22,7 +22,7 @@ EXPORTED = ("seer_prepacked_bytes", "seer_prepack_weights", "seer_layer_workspac
             "seer_layer_workspace_offsets", "seer_layer_forward_varlen",
             "seer_layer_forward_varlen_timed", "seer_step0_detect", "seer_batch_repack",
             "seer_layer_forward_cached", "seer_kv_export", "seer_graph_begin", "seer_graph_end",
-            "seer_graph_launch", "seer_graph_destroy", "seer_lm_head_workspace_bytes",
+            "seer_graph_launch", "seer_graph_destroy", "seer_lm_head_workspace_bytes", "seer_lm_head_prepack",
             "seer_lm_head_predict", "seer_remask_step", "seer_last_error", "seer_abi_version")
 
 
@@ -108,6 +108,8 @@ def load_library():
     L.seer_kv_export.restype = ctypes.c_int
     L.seer_lm_head_workspace_bytes.argtypes = [ctypes.POINTER(seer_dims), _I, _I]
     L.seer_lm_head_workspace_bytes.restype = ctypes.c_size_t
+    L.seer_lm_head_prepack.argtypes = [ctypes.POINTER(seer_dims), _P, _I, _P, ctypes.c_size_t, _P]
+    L.seer_lm_head_prepack.restype = ctypes.c_int
     L.seer_lm_head_predict.argtypes = [ctypes.POINTER(seer_dims), _P, _I, _P, _I, _P, _I, _P, _P, _P,
                                        ctypes.c_size_t, _P]
     L.seer_lm_head_predict.restype = ctypes.c_int
@@ -264,11 +266,17 @@ def seer_lm_head_workspace_bytes(dims, vocab, rows_ub):
     return load_library().seer_lm_head_workspace_bytes(ctypes.byref(dims), int(vocab), int(rows_ub))
 
 
-def seer_lm_head_predict(dims, w_lm, vocab, x, rows_ub, cu_seqlens, batch, pred, conf, workspace,
+def seer_lm_head_prepack(dims, w_lm, vocab, dst, dst_bytes=None, stream=None):
+    nbytes = dst_bytes if dst_bytes is not None else dst.numel() * dst.element_size()
+    _check(load_library().seer_lm_head_prepack(ctypes.byref(dims), _ptr(w_lm), int(vocab), _ptr(dst), nbytes,
+                                               _stream(stream)))
+
+
+def seer_lm_head_predict(dims, w_packed, vocab, x, rows_ub, cu_seqlens, batch, pred, conf, workspace,
                          workspace_bytes=None, stream=None):
     nbytes = workspace_bytes if workspace_bytes is not None else workspace.numel() * workspace.element_size()
     _check(load_library().seer_lm_head_predict(
-        ctypes.byref(dims), _ptr(w_lm), int(vocab), _ptr(x), int(rows_ub), _ptr(cu_seqlens), int(batch),
+        ctypes.byref(dims), _ptr(w_packed), int(vocab), _ptr(x), int(rows_ub), _ptr(cu_seqlens), int(batch),
         _ptr(pred), _ptr(conf), _ptr(workspace), nbytes, _stream(stream)))
 
 

@@ -217,7 +217,17 @@ def test_graph_shapes():
 def test_sampler_argument_errors(S):
     L = S.load_library()
     d = dims(S)
-    assert S.seer_lm_head_workspace_bytes(d, 126464, 1000) >= 1000 * (126464 // 128) * 16
+    assert S.seer_lm_head_workspace_bytes(d, 126464, 1000) >= 1000 * (126464 // 64) * 16
+    pargs = lambda **kw: [kw.get(k, v) for k, v in [
+        ("dims", ctypes.byref(d)), ("w", FAKE), ("vocab", 126464), ("dst", FAKE), ("dst_bytes", 1 << 40),
+        ("stream", None)]]
+    assert L.seer_lm_head_prepack(*pargs(w=None)) == S.SEER_EINVAL
+    assert L.seer_lm_head_prepack(*pargs(dst=None)) == S.SEER_EINVAL
+    assert L.seer_lm_head_prepack(*pargs(dst_bytes=126464 * 4096 * 2 - 1)) == S.SEER_EINVAL
+    assert L.seer_lm_head_prepack(*pargs(vocab=1000)) == S.SEER_EUNSUPPORTED
+    assert L.seer_lm_head_prepack(*pargs(vocab=524288)) == S.SEER_EUNSUPPORTED     # 4 GiB
+    assert L.seer_lm_head_prepack(*pargs(dims=ctypes.byref(dims(S, d=256, h=4, dh=64, i=688, dtype=2)))) \
+        == S.SEER_EUNSUPPORTED
     args = lambda **kw: [kw.get(k, v) for k, v in [
         ("dims", ctypes.byref(d)), ("w", FAKE), ("vocab", 126464), ("x", FAKE), ("rows", 100), ("cu", FAKE),
         ("batch", 1), ("pred", FAKE), ("conf", FAKE), ("ws", FAKE), ("ws_bytes", 1 << 40), ("stream", None)]]

@@ -82,8 +82,15 @@ def test_lm_head_predict(S, case):
     pred = torch.full((rows_ub,), -7, dtype=torch.int32, device="cuda")
     conf = torch.zeros(rows_ub, dtype=torch.float32, device="cuda")
     ws = torch.empty(S.seer_lm_head_workspace_bytes(dims, vocab, rows_ub), dtype=torch.uint8, device="cuda")
-    S.seer_lm_head_predict(dims, w_lm, vocab, x, rows_ub, dev(cu_h), B, pred, conf, ws)
+    packed = torch.empty(vocab * sh.d_model * 2, dtype=torch.uint8, device="cuda")
+    S.seer_lm_head_prepack(dims, w_lm, vocab, packed)
+    S.seer_lm_head_predict(dims, packed, vocab, x, rows_ub, dev(cu_h), B, pred, conf, ws)
     torch.cuda.synchronize()
+    if case == "small":
+        # the operand order, bit for bit: (32-row block, 16-column block, column half, row, 8 columns)
+        w16 = w_lm.view(torch.int16).cpu().numpy()
+        want = w16.reshape(vocab // 32, 32, sh.d_model // 16, 2, 8).transpose(0, 2, 3, 1, 4).reshape(-1)
+        assert np.array_equal(packed.view(torch.int16).cpu().numpy(), want)
     ph, ch = host(pred), host(conf)
     assert np.all(ph[R:] == -7), "rows past cu[B] must not be written"
     rng = np.random.default_rng(3)
