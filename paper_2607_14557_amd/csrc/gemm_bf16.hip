@@ -438,6 +438,18 @@ __device__ __forceinline__ void gemm_tile(const GemmParams& p, uint8_t* smem, in
     }
   };
 
+  // Rotated q/k waves take their own straight-line path (bf16 stores), so
+  // that no accumulator values from rotated and unrotated paths meet.
+  if constexpr (kRope) {
+    if (rope_on) {
+#pragma unroll
+      for (int i = 0; i < NI; ++i) {
+        rope_block(i);
+        store_block(std::false_type{}, i, rq[0]);
+      }
+      return;
+    }
+  }
 #pragma unroll
   for (int i = 0; i < NI; ++i) {
     const int row = m0 + i * 32 + fr;
@@ -505,9 +517,6 @@ __device__ __forceinline__ void gemm_tile(const GemmParams& p, uint8_t* smem, in
         *reinterpret_cast<u32x4_t*>(dst) = u32x4_t{__float_as_uint(mm), __float_as_uint(st), (uint32_t)at, 0u};
       }
     } else {
-      if constexpr (kRope) {
-        if (rope_on) rope_block(i);
-      }
       const u32x4_t* rr = rq[i % RDEPTH];
       if (kScale && to_f16)
         store_block(std::true_type{}, i, rr);
