@@ -19,7 +19,8 @@
  *   seer_layer_forward_cached  prefix keys/values cached (Appendix D)
  *   seer_graph_*               record a launch sequence once, replay it
  *                              (graph-compatible paths, Sec. 3.5)
- *   seer_lm_head_predict,      synthetic LM head (argmax + confidence) and
+ *   seer_lm_head_prepack,      synthetic LM head (one-time weight layout;
+ *   seer_lm_head_predict,      argmax + confidence) and
  *   seer_remask_step           low-confidence remasking between steps
  *
  * Conventions shared by every call:
@@ -27,7 +28,8 @@
  *     parameter says "host".  The library never allocates or frees caller
  *     memory; layer scratch comes from a caller workspace sized by
  *     seer_layer_workspace_bytes().
- *   - Row-major everywhere.  Weights use the [out, in] layout (input features
+ *   - Row-major everywhere, except the packed weights the prepack calls
+ *     produce.  Weights are given in the [out, in] layout (input features
  *     contiguous).  Element type is given by seer_dims.dtype: bf16 (raw
  *     16-bit brain-float bits) or fp32.  Counts, offsets and lengths are int32.
  *   - Packed sequences: sequence b occupies rows [cu_seqlens[b], cu_seqlens[b+1])

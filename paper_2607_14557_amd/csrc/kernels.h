@@ -50,7 +50,7 @@ struct GemmParams {
   int f16_col0;
   // bf16 only: workgroups that run at once (one per CU).  When the 256x256
   // tiles leave a last round of r <= n_units / 2 tiles, those r tiles run as
-  // 2 r halves of 256x128.  0 disables the split.
+  // 2 r halves of 128x256 (split along rows).  0 disables the split.
   int n_units;
   // bf16 SCALE_ROPE only (and required there): rotary embedding of output
   // columns < rope_col1 (whole 128-wide heads): row r's pair (c, c + 64) of
