@@ -77,17 +77,18 @@ __device__ __forceinline__ void raster(int lid, int tiles_m, int tiles_n, int& t
 
 }  // namespace
 
+// s_waitcnt immediate (gfx9 encoding) for vmcnt(vm), lgkmcnt(lgkm), expcnt
+// unconstrained.
+constexpr int waitcnt_imm(int vm, int lgkm) { return ((vm >> 4) << 14) | (lgkm << 8) | (7 << 4) | (vm & 15); }
+
 // Instruction order inside one K slice of a BMT-row tile (masks: 0x008 MFMA,
-// 0x020 VMEM, 0x100 LDS read, 0x200 LDS write).  Per slice: the next slice's
-// BMT/32 fragment reads, paired two to an MFMA; the global loads (BMT/128 of
-// A for tile t+2, two of B for tile t+1), one per MFMA; the LDS writes of A
-// tile t+1 (BMT/128 in slices 0 and 1, twice that in slice 2, none in slice
-// 3), one per MFMA; then the remaining MFMAs.
+// 0x020 VMEM, 0x100 LDS read).  Per slice: the next slice's BMT/32 fragment
+// reads, paired two to an MFMA; the loads (BMT/128 of A tile t+3 into LDS,
+// two of B tile t+1 into registers), one per MFMA; then the remaining MFMAs.
 template <int BMT>
-__device__ __forceinline__ void seer_slice_schedule(int ks) {
+__device__ __forceinline__ void seer_slice_schedule() {
   constexpr int NR = BMT / 32;
   constexpr int NV = BMT / 128 + 2;
-  constexpr int NW = BMT / 128;
   constexpr int NM = 2 * NR;
 #pragma unroll
   for (int g = 0; g < NR / 2; ++g) {
@@ -99,33 +100,18 @@ __device__ __forceinline__ void seer_slice_schedule(int ks) {
     __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
     __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
   }
-  if (ks < 2) {
-#pragma unroll
-    for (int g = 0; g < NW; ++g) {
-      __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-    }
-    __builtin_amdgcn_sched_group_barrier(0x008, NM - NR / 2 - NV - NW, 0);
-  } else if (ks == 2) {
-#pragma unroll
-    for (int g = 0; g < 2 * NW; ++g) {
-      __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-    }
-    __builtin_amdgcn_sched_group_barrier(0x008, NM - NR / 2 - NV - 2 * NW, 0);
-  } else {
-    __builtin_amdgcn_sched_group_barrier(0x008, NM - NR / 2 - NV, 0);
-  }
+  __builtin_amdgcn_sched_group_barrier(0x008, NM - NR / 2 - NV, 0);
 }
 
 // One BMTx256 output tile over the whole K range.  BMT = 256 is the main
 // tile; BMT = 128 serves the halves of the tiles of a partly filled last
 // round.  Wave w owns columns n0 + 64 w .. +63 and all BMT rows.
 template <int EPI, int BMT>
-__device__ __forceinline__ void gemm_tile(const GemmParams& p, uint8_t* smem, int M, int m0, int n0) {
-  constexpr int NI = BMT / 32;                      // 32-row MFMA tiles per wave = A chunks per thread
-  constexpr int AP = NI / 4;                        // ... per slice
-  constexpr int STAGE_BYTES = BMT * ROW_BYTES;
+__device__ __forceinline__ void gemm_tile(const GemmParams& p, uint8_t* st0, uint8_t* st1, uint8_t* st2, uint8_t* st3,
+                                          int M, int m0, int n0) {
+  constexpr int NI = BMT / 32;                      // 32-row MFMA tiles per wave
+  constexpr int NA = BMT / 32;                      // A loads (1 KiB each) per wave and K tile
+  constexpr int AP = NA / 4;                        // ... per slice
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -135,25 +121,33 @@ __device__ __forceinline__ void gemm_tile(const GemmParams& p, uint8_t* smem, in
   uint16_t* C = static_cast<uint16_t*>(p.C);
   const uint16_t* R = static_cast<const uint16_t*>(p.R);
 
-  // ---- A: global -> register -> LDS staging ------------------------------
-  // Thread t moves 16-byte chunks c = t + 256 i of the BMTx64 A tile (i < NI):
-  // tile row c / 8, K-chunk c % 8 -- eight consecutive threads read one
-  // 128-byte row segment.  In LDS the chunk lands at position chunk ^ swz(row).
-  const int srow = tid >> 3;          // + 32 i
-  const int schunk = tid & 7;
-  // 32-bit byte offsets from the uniform bases (operands are < 4 GiB); rows of
-  // A past M re-read row M-1 (never stored).  swz(row) is the same for
-  // row = srow + 32 i, so the LDS slot is one base plus an immediate.
-  const char* Ab = static_cast<const char*>(p.A);
-  const char* Bb = static_cast<const char*>(p.B);
-  uint32_t a_off[NI];
+  // ---- A: straight into a four-stage LDS ring -----------------------------
+  // buffer_load ... lds moves 64 x 16 bytes into 1 KiB of consecutive LDS.
+  // Instruction i of wave w (i < NA) fills tile rows 8 (NA w + i) .. +7 of a
+  // stage; lane l lands at row 8 (NA w + i) + l/8, slot l%8, so it fetches the
+  // K-chunk that the swizzle puts there, (l%8) ^ swz(row).  32-bit byte
+  // offsets from the base (operands are < 4 GiB); rows of A past M re-read
+  // row M-1 (never stored).
+  const int wv = __builtin_amdgcn_readfirstlane(wave);
+  const __amdgpu_buffer_rsrc_t rsa = __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p.A), 0, -1, 0x00020000);
+  uint32_t a_src[NA];
 #pragma unroll
-  for (int i = 0; i < NI; ++i) {
-    int ga = m0 + srow + 32 * i;
+  for (int i = 0; i < NA; ++i) {
+    const int row = 8 * (NA * wave + i) + (lane >> 3);
+    int ga = m0 + row;
     ga = ga < M ? ga : M - 1;
-    a_off[i] = (uint32_t)ga * (uint32_t)p.lda * 2u + (uint32_t)schunk * 16u;
+    a_src[i] = (uint32_t)ga * (uint32_t)p.lda * 2u + (uint32_t)(((lane & 7) ^ swz(row)) << 4);
   }
-  const int s_off = srow * ROW_BYTES + ((schunk ^ swz(srow)) << 4);
+  const int KT = p.K / BK;
+  // quarter q (instructions AP q .. AP q + AP - 1) of A tile t into stage stg
+  auto dma_a = [&](uint8_t* stg, int t, int q) {
+    const int t_ = t < KT ? t : KT - 1;
+    const uint32_t ko = (uint32_t)t_ * (BK * 2);
+#pragma unroll
+    for (int i = AP * q; i < AP * q + AP; ++i)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsa, (lds_void_t*)(stg + 8 * (NA * wv + i) * ROW_BYTES), 16, a_src[i],
+                                               ko, 0, 0);
+  };
 
   // Fragment geometry: lane l holds row (l & 31) of a 32-row MFMA tile and
   // the 8 K values 16 s + 8 (l >> 5) .. +7 of K slice s.
@@ -166,6 +160,7 @@ __device__ __forceinline__ void gemm_tile(const GemmParams& p, uint8_t* smem, in
   // Column block j of the wave: lane l takes column wcol + 32 j + l%32.  In
   // the fragment-major weight, its operand of K slice s is the 16 bytes at
   // 16 l of the 1 KiB block (col / 32) * (K / 16) + s.
+  const char* Bb = static_cast<const char*>(p.B);
   uint32_t b_off[2];
 #pragma unroll
   for (int j = 0; j < 2; ++j) b_off[j] = (uint32_t)((wcol >> 5) + j) * (uint32_t)(p.K >> 4) * 1024u + (uint32_t)lane * 16u;
@@ -180,35 +175,20 @@ __device__ __forceinline__ void gemm_tile(const GemmParams& p, uint8_t* smem, in
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
-  // Software pipeline: while tile t is multiplied out of LDS stage t%2 and B
-  // register set t%2, A tile t+1 (loaded into registers one iteration earlier)
-  // is written into stage (t+1)%2 between the MFMAs, and the loads of A tile
-  // t+2 and B tile t+1 are in flight.  Register sets alternate, so the loop is
-  // unrolled by two; K/64 is even for every shape the bf16 path accepts.
-  u32x4_t ra0[NI], ra1[NI];
+  // Software pipeline: tile t is multiplied out of LDS stage t%4 and B
+  // register set t%2 while A tile t+3 streams into stage (t+3)%4 (the stage of
+  // tile t-1) and B tile t+1 into the other register set.  The loop is
+  // unrolled by four (stages) with a two-tile tail; K/64 is even for every
+  // shape the bf16 path accepts.
   bf16x8_t bq0[2][4], bq1[2][4];
   bf16x8_t af[2][NI];
-  const int KT = p.K / BK;
 
-#define SEER_GLOAD_A(RA, T, P)                                                      \
-  {                                                                                 \
-    const int t_ = (T) < KT ? (T) : KT - 1;                                         \
-    const char* ak_ = Ab + (size_t)t_ * (BK * 2);                                   \
-    _Pragma("unroll") for (int i = AP * (P); i < AP * (P) + AP; ++i)                \
-      RA[i] = *reinterpret_cast<const u32x4_t*>(ak_ + a_off[i]);                    \
-  }
 #define SEER_GLOAD_B(BQ, T, KS)                                                     \
   {                                                                                 \
     const int t_ = (T) < KT ? (T) : KT - 1;                                         \
     const char* bk_ = Bb + (size_t)t_ * B_TILE + (KS) * B_SLICE;                    \
     _Pragma("unroll") for (int j = 0; j < 2; ++j)                                   \
       BQ[j][KS] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const u32x4_t*>(bk_ + b_off[j])); \
-  }
-#define SEER_LSTORE(RA, STG, P)                                                     \
-  {                                                                                 \
-    uint8_t* sa_ = smem + (STG) * STAGE_BYTES + s_off;                              \
-    _Pragma("unroll") for (int i = AP * (P); i < AP * (P) + AP; ++i)                \
-      *reinterpret_cast<u32x4_t*>(sa_ + i * 32 * ROW_BYTES) = RA[i];                \
   }
 #define SEER_FLOAD(ST, KS, BUF)                                                     \
   {                                                                                 \
@@ -217,59 +197,65 @@ __device__ __forceinline__ void gemm_tile(const GemmParams& p, uint8_t* smem, in
       af[BUF][i] = __builtin_bit_cast(bf16x8_t,                                     \
           *reinterpret_cast<const u32x4_t*>((ST) + a_row0 + i * 32 * ROW_BYTES + chunk_)); \
   }
-  // One K tile of 4 slices x (NI x 2) MFMAs.  Each slice is its own scheduling
-  // region (sched_barrier fences) holding the fragment reads of the next
-  // slice -- issued first, paired with the first MFMAs, so they have the whole
-  // slice to land -- the global loads of one quarter of A tile T+2 and of
-  // slice s of B tile T+1, and its share of the LDS writes of A tile T+1.  All
-  // of A tile T+1 is written during slices 0-2, then one barrier: it publishes
-  // tile T+1 (so slice 3 can already read slice 0 of tile T+1 from the other
-  // stage) and, since every read of stage T%2 has been issued and waited for
-  // by then, it also orders those reads before tile T+2 overwrites the stage
-  // during the next tile.
-#define SEER_TILE(T, RA, RN, BC, BNX)                                               \
+  // One K tile of 4 slices x (NI x 2) MFMAs from stage SC.  Each slice is its
+  // own scheduling region (sched_barrier fences) holding the fragment reads of
+  // the next slice -- issued first, paired with the first MFMAs, so they have
+  // the whole slice to land -- a quarter of A tile T+3 (into SF, the stage of
+  // tile T-1, which every wave finished reading before the previous tile's
+  // barrier) and slice s of B tile T+1.  After slice 2 one barrier publishes
+  // A tile T+1 (stage SN) for slice 3's look-ahead read: before it, each wave
+  // waits until its own loads of that tile (issued during tile T-2) have
+  // landed -- at most the 7 slices of loads issued since may be in flight --
+  // and until its LDS reads are done.  The barrier is bare (no fence): a
+  // fence would also wait for the loads of tiles T+2 and T+3.
+#define SEER_TILE(T, SC, SN, SF, BC, BNX)                                           \
   {                                                                                 \
-    const uint8_t* st_ = smem + ((T) & 1) * STAGE_BYTES;                            \
-    const uint8_t* sn_ = smem + (((T) + 1) & 1) * STAGE_BYTES;                      \
     _Pragma("unroll") for (int ks = 0; ks < 4; ++ks) {                              \
       const int cur = ks & 1;                                                       \
-      SEER_FLOAD(ks < 3 ? st_ : sn_, ks < 3 ? ks + 1 : 0, cur ^ 1);                 \
-      SEER_GLOAD_A(RN, (T) + 2, ks);                                                \
+      SEER_FLOAD(ks < 3 ? SC : SN, ks < 3 ? ks + 1 : 0, cur ^ 1);                   \
+      dma_a(SF, (T) + 3, ks);                                                       \
       SEER_GLOAD_B(BNX, (T) + 1, ks);                                               \
       _Pragma("unroll") for (int i = 0; i < NI; ++i)                                \
         _Pragma("unroll") for (int j = 0; j < 2; ++j)                               \
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(BC[j][ks], af[cur][i], acc[i][j], 0, 0, 0); \
-      if (ks < 2) SEER_LSTORE(RA, ((T) + 1) & 1, ks);                               \
-      if (ks == 2) {                                                                \
-        SEER_LSTORE(RA, ((T) + 1) & 1, 2);                                          \
-        SEER_LSTORE(RA, ((T) + 1) & 1, 3);                                          \
-      }                                                                             \
-      seer_slice_schedule<BMT>(ks);                                                 \
+      seer_slice_schedule<BMT>();                                                   \
       __builtin_amdgcn_sched_barrier(0);                                            \
-      if (ks == 2) __syncthreads();                                                 \
+      if (ks == 2) {                                                                \
+        __builtin_amdgcn_s_waitcnt(waitcnt_imm(7 * (AP + 2), 0));                   \
+        asm volatile("s_barrier" ::: "memory");                                     \
+        __builtin_amdgcn_sched_barrier(0);                                          \
+      }                                                                             \
     }                                                                               \
   }
 
-  // prologue: A tile 0 -> stage 0 and its first slice into registers, A tile 1
-  // in registers (set 1), B tile 0 in register set 0; A tile 2 and B tile 1 are
-  // loaded by the slices of tile 0
+  // prologue: A tiles 0, 1, 2 into stages 0, 1, 2 and B tile 0 into set 0;
+  // wait for all but tile 2 (its NA loads may stay in flight)
 #pragma unroll
-  for (int q = 0; q < 4; ++q) SEER_GLOAD_A(ra0, 0, q);
+  for (int q = 0; q < 4; ++q) dma_a(st0, 0, q);
 #pragma unroll
   for (int q = 0; q < 4; ++q) SEER_GLOAD_B(bq0, 0, q);
 #pragma unroll
-  for (int q = 0; q < 4; ++q) SEER_GLOAD_A(ra1, 1, q);
+  for (int q = 0; q < 4; ++q) dma_a(st1, 1, q);
 #pragma unroll
-  for (int q = 0; q < 4; ++q) SEER_LSTORE(ra0, 0, q);
-  __syncthreads();
-  SEER_FLOAD(smem, 0, 0);
-  for (int kt = 0; kt < KT; kt += 2) {
-    SEER_TILE(kt, ra1, ra0, bq0, bq1);
-    SEER_TILE(kt + 1, ra0, ra1, bq1, bq0);
+  for (int q = 0; q < 4; ++q) dma_a(st2, 2, q);
+  __builtin_amdgcn_s_waitcnt(waitcnt_imm(NA, 15));
+  asm volatile("s_barrier" ::: "memory");
+  __builtin_amdgcn_sched_barrier(0);
+  SEER_FLOAD(st0, 0, 0);
+  int kt = 0;
+  for (; kt + 4 <= KT; kt += 4) {
+    SEER_TILE(kt, st0, st1, st3, bq0, bq1);
+    SEER_TILE(kt + 1, st1, st2, st0, bq1, bq0);
+    SEER_TILE(kt + 2, st2, st3, st1, bq0, bq1);
+    SEER_TILE(kt + 3, st3, st0, st2, bq1, bq0);
   }
-#undef SEER_GLOAD_A
+  if (kt < KT) {                                   // K/64 = 2 mod 4
+    SEER_TILE(kt, st0, st1, st3, bq0, bq1);
+    SEER_TILE(kt + 1, st1, st2, st0, bq1, bq0);
+  }
+  // the loads past the last tile (clamped re-reads) land before the epilogue
+  __builtin_amdgcn_s_waitcnt(waitcnt_imm(0, 15));
 #undef SEER_GLOAD_B
-#undef SEER_LSTORE
 #undef SEER_FLOAD
 #undef SEER_TILE
 
@@ -291,12 +277,12 @@ __device__ __forceinline__ void gemm_tile(const GemmParams& p, uint8_t* smem, in
   const int cq = 4 * fhalf;
   // Everything the epilogue reads besides the accumulators is requested ahead
   // of its use: the row scales of all 32-row blocks, and the residual columns
-  // of all blocks (of four blocks ahead for a high/low pair).  Fetched block
+  // four blocks ahead.  Fetched block
   // by block between the stores, each block would wait out a full memory
   // latency behind the previous block's stores.  Residual word jt of a block
   // holds columns wcol + 16 jt + 8 (lane/32) .. +7 of the lane's row.
   constexpr int NRQ = (kPair ? 2 : 1) * 4;
-  constexpr int RDEPTH = kPair ? (NI < 4 ? NI : 4) : NI;
+  constexpr int RDEPTH = NI < 4 ? NI : 4;
   u32x4_t rq[RDEPTH][NRQ];
   const int colw = wcol + 8 * fhalf;
   auto fetch = [&](int i, u32x4_t* dst) {
@@ -522,8 +508,8 @@ __device__ __forceinline__ void gemm_tile(const GemmParams& p, uint8_t* smem, in
         store_block(std::true_type{}, i, rr);
       else
         store_block(std::false_type{}, i, rr);
-      // high/low residuals: the block RDEPTH ahead goes into the buffer just used
-      if constexpr (kPair) {
+      // the block RDEPTH ahead goes into the buffer just used
+      if constexpr (kRes) {
         if (i + RDEPTH < NI) fetch(i + RDEPTH, rq[i % RDEPTH]);
       }
     }
@@ -538,7 +524,12 @@ __device__ __forceinline__ void gemm_tile(const GemmParams& p, uint8_t* smem, in
 // upper-bound grid, and halves that start past the last row, exit at once.
 template <int EPI>
 __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmParams p) {
-  __shared__ __attribute__((aligned(1024))) uint8_t smem[2 * 256 * ROW_BYTES];
+  // the four stages of the A ring, each its own array: the compiler then
+  // orders fragment reads of one stage only after the loads into that stage
+  __shared__ __attribute__((aligned(1024))) uint8_t st0[256 * ROW_BYTES];
+  __shared__ __attribute__((aligned(1024))) uint8_t st1[256 * ROW_BYTES];
+  __shared__ __attribute__((aligned(1024))) uint8_t st2[256 * ROW_BYTES];
+  __shared__ __attribute__((aligned(1024))) uint8_t st3[256 * ROW_BYTES];
   const int M = rows_from(p.m_ptr, p.m_ub);
   const int tiles_m = (M + 255) / 256;
   const int tiles_n = p.N / 256;
@@ -553,13 +544,13 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmParams p) {
   int tm, tn;
   if (u < full) {
     raster(xcd_remap(u, full), tiles_m, tiles_n, tm, tn);
-    gemm_tile<EPI, 256>(p, smem, M, tm * 256, tn * 256);
+    gemm_tile<EPI, 256>(p, st0, st1, st2, st3, M, tm * 256, tn * 256);
   } else {
     const int v = u - full;
     raster(full + (v >> 1), tiles_m, tiles_n, tm, tn);
     const int m0 = tm * 256 + (v & 1) * 128;
     if (m0 >= M) return;
-    gemm_tile<EPI, 128>(p, smem, M, m0, tn * 256);
+    gemm_tile<EPI, 128>(p, st0, st1, st2, st3, M, m0, tn * 256);
   }
 }
 
