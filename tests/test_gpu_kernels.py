@@ -217,9 +217,12 @@ class _Layer:
         return t
 
 
-@pytest.mark.parametrize("dtype", ["bf16", "f32"])
-def test_layer_vs_oracle_ragged(S, dtype):
-    d, H, dh, I = (512, 4, 128, 1024) if dtype == "bf16" else (256, 4, 64, 688)
+# bf16_k640: d_ff = 640 gives the down projection K / 64 = 10 tiles, so the
+# GEMM's four-stage ring ends on its two-tile tail
+@pytest.mark.parametrize("case", ["bf16", "bf16_k640", "f32"])
+def test_layer_vs_oracle_ragged(S, case):
+    dtype = "f32" if case == "f32" else "bf16"
+    d, H, dh, I = {"bf16": (512, 4, 128, 1024), "bf16_k640": (256, 2, 128, 640), "f32": (256, 4, 64, 688)}[case]
     tol = BF16_TOL if dtype == "bf16" else F32_TOL
     rng = np.random.default_rng(42)
     W = _round(_rand_layer(rng, d, I, 0.02), dtype)
@@ -232,7 +235,7 @@ def test_layer_vs_oracle_ragged(S, dtype):
     xd = dev(x, dtype)
     x = host(xd)                                    # exact values the GPU sees
     eps = 0.01 * 0.0004 * d
-    log("layer %s ragged lens=%s" % (dtype, lens))
+    log("layer %s ragged lens=%s (d %d, d_ff %d)" % (dtype, lens, d, I))
     L = _Layer(S, d, H, dh, I, dtype, rows_ub, W)
     y, cnt = L.run(xd, dev(cu), len(lens), eps=eps)
     y = host(y)
