@@ -33,8 +33,7 @@ __global__ __launch_bounds__(256) void rms_inv_kernel(const void* x, int ld, int
   float acc = 0.0f;
   if constexpr (BF16) {
     const uint16_t* xr = static_cast<const uint16_t*>(x) + (size_t)row * ld;
-    for (int j = lane * 8; j < d; j += 512) {
-      const uint4 v = *reinterpret_cast<const uint4*>(xr + j);
+    auto add = [&](const uint4 v) {
       const uint32_t w[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
@@ -43,7 +42,19 @@ __global__ __launch_bounds__(256) void rms_inv_kernel(const void* x, int ld, int
         acc = fmaf(lo, lo, acc);
         acc = fmaf(hi, hi, acc);
       }
+    };
+    // lane l sums chunks j = 8 l + 512 u in increasing u.  Eight chunks (a
+    // whole 4096-wide row) are requested before the first is used, so a row
+    // costs one memory latency, not eight; the summation order is unchanged.
+    int j = lane * 8;
+    for (; j + 512 * 7 < d; j += 512 * 8) {
+      uint4 v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) v[u] = *reinterpret_cast<const uint4*>(xr + j + 512 * u);
+#pragma unroll
+      for (int u = 0; u < 8; ++u) add(v[u]);
     }
+    for (; j < d; j += 512) add(*reinterpret_cast<const uint4*>(xr + j));
   } else {
     const float* xr = static_cast<const float*>(x) + (size_t)row * ld;
     for (int j = lane; j < d; j += 64) acc = fmaf(xr[j], xr[j], acc);
