@@ -49,7 +49,7 @@ VOCAB = 126464          # LLaDA-8B vocabulary size (the synthetic LM head's widt
 TRAFFIC_SOURCES = ("paper_2607_14557_amd/csrc/gemm_bf16.hip", "paper_2607_14557_amd/csrc/kernels.h",
                    "paper_2607_14557_amd/csrc/common.h")
 TRAFFIC = {"sources_sha256": "7a439aa18adbd2863ae15801866a48a967d88c122a11bb5ae1b749a2ba3f819e",
-           "rows": 14280, "fetch_bytes": 4223845621, "write_bytes": 350945280}
+           "rows": 14280, "fetch_bytes": 4223945018, "write_bytes": 350945280}
 
 
 def sources_sha256():
