@@ -10,6 +10,7 @@
  *
  * Entry points (all asynchronous on the given HIP stream):
  *   seer_prepack_weights       one-time weight layout for the layer kernels
+ *   seer_layer_status_reset    clear the status word of a layer workspace
  *   seer_layer_forward_varlen  one bidirectional transformer layer over
  *                              packed variable-length sequences, with the
  *                              optional fused near-zero activation count
@@ -117,13 +118,31 @@ int seer_prepack_weights(const seer_dims* dims, const seer_layer_weights* src,
 
 /* Workspace bytes needed by seer_layer_forward_varlen for up to max_rows
  * packed rows (qkv, attention output, post-attention residual, SwiGLU
- * activations and two per-row RMS statistics). */
+ * activations and two per-row RMS statistics), plus a 256-byte header.
+ *
+ * Status word: the int32 at byte 0 of the workspace (for every rows bound).
+ * Layer calls only ever set bits in it (atomic OR), so it accumulates over
+ * every call made on the workspace until seer_layer_status_reset() clears it;
+ * a new allocation holds arbitrary bits until then.  Bits:
+ *   SEER_STATUS_V_RANGE  a bf16 layer stored a value of V (the attention
+ *                        values, kept in fp16 for the fp16 P V product) whose
+ *                        magnitude exceeded 65504, fp16's largest finite
+ *                        value: it was stored rounded (+-65504 or +-inf) and
+ *                        the attention output of its sequence and head is not
+ *                        meaningful.  Values below 2^-14 are kept as fp16
+ *                        subnormals (absolute precision 2^-24), not flagged. */
+#define SEER_STATUS_V_RANGE 1
 size_t seer_layer_workspace_bytes(const seer_dims* dims, int32_t max_rows);
+
+/* Clear the status word of a layer workspace (device, 256-byte aligned, at
+ * least 256 bytes), asynchronously on `stream` (a kernel, so it can be
+ * recorded).  Errors: EINVAL (NULL or misaligned), EWORKSPACE (too small). */
+int seer_layer_status_reset(void* workspace, size_t workspace_bytes, hipStream_t stream);
 
 /* Byte offsets of the intermediates that the last seer_layer_forward_varlen
  * call on a workspace left there, for a call made with total_rows_ub ==
- * max_rows (the layout depends on that bound).  Element type dims.dtype
- * unless noted:
+ * max_rows (the layout depends on that bound; bytes [0, 256) are the header
+ * with the status word).  Element type dims.dtype unless noted:
  *   offsets[0] qkv  [max_rows, 3*d_model]   q | k | v after the folded RMSNorm
  *                                           (bf16 layers: v is stored as fp16,
  *                                           the type of the attention's P V product)
@@ -150,10 +169,12 @@ int seer_layer_workspace_offsets(const seer_dims* dims, int32_t max_rows, size_t
  *     h1  = x + o Wo^T
  *     b   = RMSNorm(h1) * g2;  act = silu(b Wg^T) * (b Wu^T)
  *     y   = h1 + act Wd^T
- * Precision (bf16 layers): operands bf16, accumulation fp32; q, k, v, o, h1
- * and act are rounded to bf16 where they feed a matrix product; the
- * probabilities of the attention-weighted sum are kept in fp16; the residual
- * h1 enters the final add as a bf16 high/low pair (exact to ~2^-17).
+ * Precision (bf16 layers): operands bf16, accumulation fp32; q, k, o, h1
+ * and act are rounded to bf16 where they feed a matrix product; v and the
+ * probabilities of the attention-weighted sum are kept in fp16 (so |v| must
+ * stay within fp16's range: a larger value sets SEER_STATUS_V_RANGE in the
+ * workspace status word); the residual h1 enters the final add as a bf16
+ * high/low pair (exact to ~2^-17).
  * x_in, x_out: [total_rows_ub, d_model] rows (may not alias).  Only rows
  * [0, cu_seqlens[batch]) are read and written.
  * seqused: optional [batch]; when given, rows at index >= seqused[b] inside
@@ -404,7 +425,7 @@ int seer_graph_destroy(seer_graph_t graph);
 const char* seer_last_error(void);
 
 /* ABI version of this library (major * 100 + minor). */
-int32_t seer_abi_version(void);   /* 102: bf16 weights packed in operand order */
+int32_t seer_abi_version(void);   /* 103: workspace header with the status word */
 
 #ifdef __cplusplus
 }

@@ -8,10 +8,13 @@
 // the 32x32x16 bf16 MFMA.
 //
 // Operands take two different routes:
-//   A (activations, shared by all four waves) moves global -> registers -> LDS
-//     through a two-stage LDS ring with two K tiles of look-ahead; the 16-byte
-//     chunks of each 128-byte LDS row are XOR-swizzled so that the fragment
-//     reads of 16 consecutive rows land in distinct banks;
+//   A (activations, shared by all four waves) goes straight from global memory
+//     into a four-stage LDS ring with direct-to-LDS buffer loads (1 KiB per
+//     instruction, no staging registers), three K tiles ahead; each lane
+//     fetches the 16-byte chunk that the XOR swizzle puts at its LDS position,
+//     so the fragment reads of 16 consecutive rows land in distinct banks;
+//     the four stages are separate arrays and one bare barrier per K tile
+//     publishes the next stage;
 //   B (weights, 64 columns private to each wave) never touches LDS: the weight
 //     prepack stores it fragment-major (frag_b_index), so every operand of a
 //     wave is one coalesced 1 KiB load straight into the MFMA registers, issued
@@ -375,6 +378,8 @@ __device__ __forceinline__ void gemm_tile(const GemmParams& p, uint8_t* st0, uin
     v[3] += __uint_as_float(r.y & 0xffff0000u);
   };
 
+  // largest magnitude this lane stored as fp16 (the range check of V)
+  float f16_max = 0.0f;
   // One 32-row block of the non-GLU epilogues, straight-line for one output
   // type (F16 is the type of the whole block).
   auto store_block = [&](auto f16_tag, int i, const u32x4_t* rr) {
@@ -407,6 +412,10 @@ __device__ __forceinline__ void gemm_tile(const GemmParams& p, uint8_t* st0, uin
         }
         if constexpr (kRes) add_bf4(v, rv[q]);
         if constexpr (kPair) add_bf4(v, rv2[q]);
+        if constexpr (F16) {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) f16_max = fmaxf(f16_max, fabsf(v[e]));
+        }
         pk[q].x = F16 ? pack_h2(v[0], v[1]) : pack_bf2(v[0], v[1]);
         pk[q].y = F16 ? pack_h2(v[2], v[3]) : pack_bf2(v[2], v[3]);
         if constexpr (EPI == EPI_RESID_SPLIT) {
@@ -513,6 +522,11 @@ __device__ __forceinline__ void gemm_tile(const GemmParams& p, uint8_t* st0, uin
         if (i + RDEPTH < NI) fetch(i + RDEPTH, rq[i % RDEPTH]);
       }
     }
+  }
+  // V beyond fp16's finite range was stored rounded (+-65504 or +-inf): report
+  // it (rare; one atomic per offending lane)
+  if constexpr (kScale) {
+    if (to_f16 && p.status && f16_max > 65504.0f) atomicOr(p.status, SEER_STATUS_V_RANGE);
   }
 }
 

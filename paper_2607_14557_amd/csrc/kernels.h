@@ -4,6 +4,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "seer.h"
+
 namespace seer {
 
 // SCALE: C = acc * rs[r]; SCALE_ROPE: SCALE with the rotary embedding of the
@@ -62,6 +64,10 @@ struct GemmParams {
   // from weight rows packed in head-block order 0, 2, 1, 3 (qk_packed_row)
   // and are stored back in head order; 0 means none.  rope_col1 <= perm_col1.
   int perm_col1;
+  // bf16 SCALE(_ROPE) only, optional: status word that receives
+  // SEER_STATUS_V_RANGE (atomic OR) when a column stored as fp16 had a
+  // magnitude above fp16's largest finite value
+  int* status;
 };
 
 // Weight layout of the bf16 GEMM's B operand ("fragment-major"): element

@@ -68,11 +68,16 @@ struct WsLayout {
   size_t qkv, o, h1, act, inv1, inv2, h1lo, pos, freq, total;
 };
 
+// The first 256 bytes of a layer workspace are a header whose first int32 is
+// the status word (same place for every rows bound, so it persists across
+// calls of different sizes on one workspace).
+constexpr size_t WS_HEADER = 256;
+
 WsLayout ws_layout(const seer_dims* d, int rows) {
   const size_t es = d->dtype == SEER_DTYPE_BF16 ? 2 : 4;
   const size_t R = (size_t)(rows > 0 ? rows : 0);
   WsLayout L;
-  size_t off = 0;
+  size_t off = WS_HEADER;
   L.qkv = off; off = up256(off + R * 3 * d->d_model * es);
   L.o = off;   off = up256(off + R * d->d_model * es);
   L.h1 = off;  off = up256(off + R * d->d_model * es);
@@ -96,7 +101,7 @@ extern "C" {
 
 const char* seer_last_error(void) { return g_err.c_str(); }
 
-int32_t seer_abi_version(void) { return 102; }
+int32_t seer_abi_version(void) { return 103; }
 
 size_t seer_prepacked_bytes(const seer_dims* dims) {
   if (check_dims(dims) != SEER_OK) return 0;
@@ -129,6 +134,16 @@ int seer_prepack_weights(const seer_dims* dims, const seer_layer_weights* src, v
 size_t seer_layer_workspace_bytes(const seer_dims* dims, int32_t max_rows) {
   if (check_dims(dims) != SEER_OK || max_rows < 0) return 0;
   return ws_layout(dims, max_rows).total;
+}
+
+int seer_layer_status_reset(void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  if (!workspace) return fail(SEER_EINVAL, "workspace is NULL");
+  if (!aligned(workspace, 256)) return fail(SEER_EINVAL, "workspace must be 256-byte aligned");
+  if (workspace_bytes < WS_HEADER)
+    return fail(SEER_EWORKSPACE, "workspace holds %zu bytes, need at least %zu", workspace_bytes, WS_HEADER);
+  // a kernel, not a memset, so that the call can be recorded
+  if (seer::launch_zero_i32(static_cast<int32_t*>(workspace), 1, stream)) return hip_fail("zero launch");
+  return ok();
 }
 
 int seer_layer_workspace_offsets(const seer_dims* dims, int32_t max_rows, size_t offsets[8]) {
@@ -216,6 +231,7 @@ static int layer_forward_impl(const seer_dims* dims, const void* w_packed, const
     g.m_ptr = m_ptr; g.m_ub = R; g.N = 3 * d; g.K = d;
     g.lda = d; g.ldb = d; g.ldc = 3 * d;
     g.f16_col0 = bf16 ? 2 * d : 0;     // V goes to the attention's fp16 PV product
+    g.status = bf16 ? reinterpret_cast<int*>(ws) : nullptr;   // V beyond fp16 range is reported
     g.perm_col1 = bf16 ? 2 * d : 0;    // q and k rows are packed head-permuted
     if (rope && bf16) {
       // q and k rotated in the epilogue, where each lane holds rotary pairs

@@ -215,9 +215,25 @@ class SeerStack:
         self.packed: List[Optional[torch.Tensor]] = [None] * n_layers
         self.ws_bytes = S.seer_layer_workspace_bytes(dims, self.max_rows)
         self.workspace = torch.empty(self.ws_bytes, dtype=torch.uint8, device=device)
+        S.seer_layer_status_reset(self.workspace, self.ws_bytes)
         d = dims.d_model
         self.buf = [torch.zeros(self.max_rows, d, dtype=self.dtype, device=device) for _ in range(2)]
         self._trunc_bufs = {}
+
+    def layer_status(self, stream=None):
+        """The workspace status word (SEER_STATUS_* bits accumulated by every
+        layer call since construction or the last reset); waits for `stream`."""
+        (stream or torch.cuda.current_stream(self.workspace.device)).synchronize()
+        return int(self.workspace[:4].view(torch.int32).item())
+
+    def check_status(self, stream=None):
+        """Raise SeerError if a layer call reported a value out of range."""
+        st = self.layer_status(stream)
+        if st & S.SEER_STATUS_V_RANGE:
+            raise S.SeerError(S.SEER_EUNSUPPORTED, "an attention value exceeded the fp16 range (|v| > 65504)")
+
+    def reset_status(self, stream=None):
+        S.seer_layer_status_reset(self.workspace, self.ws_bytes, stream=stream)
 
     def set_layer(self, l, weights, stream=None):
         if self.packed[l] is None:
@@ -309,8 +325,28 @@ class SeerStack:
 
     def step0(self, x_full, cu_full, win_off, win_len, batch, rows_full, l_det, act_eps,
               snr=(3, 100, 3, 5, 3), policy=S.SEER_ROUTE_HYBRID, tau_pad=(1, 5), granule=256,
-              trunc_capacity=None, ctrl_host=None, stream=None):
+              trunc_capacity=None, ctrl_host=None, check_status=True, stream=None):
+        """Step 0 (Sec. 3.2-3.5): layers 0..l_det on the full window with the
+        near-zero count at l_det, the SNR scan, routing + compaction of the
+        step-input embeddings and the in-flight residual, then the remaining
+        layers on the compacted batch.
+
+        trunc_capacity: rows of the compacted buffers.  By default the worst
+        case of the routing: every window padded to the longest one,
+        sum(win_off) + batch * max(win_len) rounded up to the granule (read
+        from the device once).  A routed batch that does not fit is reported
+        by the repack kernel in the control word; with ctrl_host it is read
+        from the polled word, otherwise (check_status) from the device copy,
+        and SeerError is raised before any later layer runs; that check also
+        reads the workspace status word (check_status()).  The polled path
+        never waits on the stream: its caller checks the status word when it
+        syncs."""
         dev = self.device
+        if trunc_capacity is None:
+            wo = win_off[:batch].cpu().to(torch.int64)
+            wl_ = win_len[:batch].cpu().to(torch.int64)
+            worst = int(wo.sum()) + batch * int(wl_.max()) if batch > 0 else 0
+            trunc_capacity = max(granule, -(-worst // granule) * granule)
         counts = torch.empty(rows_full, dtype=torch.int32, device=dev)
         cur = x_full
         for l in range(l_det + 1):
@@ -318,7 +354,7 @@ class SeerStack:
             self.layer(l, cur, nxt, cu_full, None, batch, rows_full,
                        act_eps=act_eps, act_count=counts if l == l_det else None, stream=stream)
             cur = nxt
-        cap = trunc_capacity if trunc_capacity is not None else rows_full + granule
+        cap = trunc_capacity
         key = (cap, batch)
         if key not in self._trunc_bufs:
             # compacted buffers, reused by every step0 call of this shape so that
@@ -353,6 +389,12 @@ class SeerStack:
             if routed["status"] != 0:
                 raise S.SeerError(routed["status"], "compacted batch exceeds the %d-row buffers" % cap)
             rows_ub = max(1, min(cap, routed["capacity_rows"]))
+        elif check_status:
+            (stream or torch.cuda.current_stream(ctrl.device)).synchronize()   # the repack has written it
+            status = int(ctrl[7].item())
+            if status != 0:
+                raise S.SeerError(status, "compacted batch exceeds the %d-row buffers" % cap)
+            self.check_status(stream)           # the step-0 layers so far kept V in range
         if l_det + 1 < self.n_layers:
             h_t = self.forward(h_t, cu_t, used, batch, rows_ub, layers=range(l_det + 1, self.n_layers),
                                out=h_t, stream=stream)

@@ -17,9 +17,10 @@ SEER_DTYPE_BF16, SEER_DTYPE_F32 = 1, 2
 SEER_ROUTE_HYBRID, SEER_ROUTE_NAIVE_PAD, SEER_ROUTE_VARLEN_ONLY = 0, 1, 2
 SEER_PATH_STATIC, SEER_PATH_VARLEN, SEER_PATH_EAGER = 0, 1, 2
 SEER_REPACK_WINDOW_ONLY = 1
+SEER_STATUS_V_RANGE = 1
 
 EXPORTED = ("seer_prepacked_bytes", "seer_prepack_weights", "seer_layer_workspace_bytes",
-            "seer_layer_workspace_offsets", "seer_layer_forward_varlen",
+            "seer_layer_status_reset", "seer_layer_workspace_offsets", "seer_layer_forward_varlen",
             "seer_layer_forward_varlen_timed", "seer_step0_detect", "seer_batch_repack",
             "seer_layer_forward_cached", "seer_kv_export", "seer_graph_begin", "seer_graph_end",
             "seer_graph_launch", "seer_graph_destroy", "seer_lm_head_workspace_bytes", "seer_lm_head_prepack",
@@ -87,6 +88,8 @@ def load_library():
     L.seer_prepack_weights.restype = ctypes.c_int
     L.seer_layer_workspace_bytes.argtypes = [ctypes.POINTER(seer_dims), _I]
     L.seer_layer_workspace_bytes.restype = ctypes.c_size_t
+    L.seer_layer_status_reset.argtypes = [_P, ctypes.c_size_t, _P]
+    L.seer_layer_status_reset.restype = ctypes.c_int
     L.seer_layer_workspace_offsets.argtypes = [ctypes.POINTER(seer_dims), _I,
                                                ctypes.POINTER(ctypes.c_size_t)]
     L.seer_layer_workspace_offsets.restype = ctypes.c_int
@@ -176,6 +179,11 @@ def seer_prepack_weights(dims, weights, dst, dst_bytes=None, stream=None):
 
 def seer_layer_workspace_bytes(dims, max_rows):
     return load_library().seer_layer_workspace_bytes(ctypes.byref(dims), int(max_rows))
+
+
+def seer_layer_status_reset(workspace, workspace_bytes=None, stream=None):
+    nbytes = workspace_bytes if workspace_bytes is not None else workspace.numel() * workspace.element_size()
+    _check(load_library().seer_layer_status_reset(_ptr(workspace), nbytes, _stream(stream)))
 
 
 def seer_layer_workspace_offsets(dims, max_rows):

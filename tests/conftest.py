@@ -16,6 +16,12 @@ def pytest_configure(config):
 
 
 def pytest_collection_modifyitems(config, items):
+    # A RuntimeWarning in a GPU test (an invalid cast, an overflow) means the
+    # test read memory the library never wrote or computed outside the range
+    # it meant to: fail instead of printing it.
+    for it in items:
+        if "gpu" in it.keywords:
+            it.add_marker(pytest.mark.filterwarnings("error::RuntimeWarning"))
     # GPU tests need a device; skip them (with a reason) where none is visible.
     try:
         import torch

@@ -53,6 +53,18 @@ def rel_err(got, ref):
     return float(np.max(np.abs(got - ref) / den))
 
 
+def row_errs(got, ref):
+    """Per-row max of |got - ref| / max(|ref|, rms(ref row)) (rel_err per row)."""
+    got = np.asarray(got, np.float64)
+    ref = np.asarray(ref, np.float64)
+    if ref.size == 0:
+        return np.zeros(ref.shape[0])
+    rms = np.sqrt(np.mean(ref * ref, axis=-1, keepdims=True))
+    den = np.maximum(np.abs(ref), rms)
+    den = np.where(den == 0, 1.0, den)
+    return np.max(np.abs(got - ref) / den, axis=-1)
+
+
 def view_ws(workspace, offset, rows, cols, dtype):
     """A typed view of a region of the layer workspace."""
     import torch
@@ -97,18 +109,53 @@ def count_band(b, wg, wu, eps):
     return c_min, c_max, c_ref
 
 
-def check_counts(cnt_gpu, b, wg, wu, eps, d_ff, frac_tol=1e-3):
-    """Gate: every row's count within the fp32-consistent band; the fraction
-    difference to the fp64 count within frac_tol except where the band shows
-    rounding ties.  Returns (max |diff| in counts, number of ambiguous ties)."""
-    c_min, c_max, c_ref = count_band(b, wg, wu, eps)
+def check_counts(cnt_gpu, b, wg, wu, eps, d_ff, frac_tol=1e-3, band=False, chunk=2048):
+    """Gate the per-position sparsity fraction (Sec. 3.2-3.3) against the oracle.
+
+    The oracle recomputes the SwiGLU activations in fp64 from the same MLP
+    input ``b`` (RMS-normalised, teacher-forced from the GPU's own residual)
+    and counts |act| < eps.  The gate is the spec bar itself, with no
+    escape: max over rows of |cnt_gpu - c_ref| / d_ff <= frac_tol.
+    ``band=True`` also evaluates the fp32-consistent count range of
+    ``count_band`` as a diagnostic (reported, not asserted).
+
+    Returns a dict: rows, max_count_diff, max_frac_diff, and with band the
+    number of rows whose count lies outside [c_min, c_max] and the total
+    width of the ranges (rounding ties)."""
+    from oracle.layer import silu
+    from oracle.sparsity import near_zero_count, sparsity_fraction
     cnt_gpu = np.asarray(cnt_gpu, np.int64)
-    bad = np.nonzero((cnt_gpu < c_min) | (cnt_gpu > c_max))[0]
-    assert bad.size == 0, "rows %s: count %s outside [%s, %s]" % (
-        bad[:5], cnt_gpu[bad[:5]], c_min[bad[:5]], c_max[bad[:5]])
-    diff = np.abs(cnt_gpu - c_ref)
-    ties = int(np.sum(c_max - c_min))
-    over = diff / float(d_ff) > frac_tol
-    # a fraction difference above tolerance is only allowed where ties explain it
-    assert np.all(diff[over] <= (c_max - c_min)[over])
-    return int(diff.max()) if diff.size else 0, ties
+    b = np.asarray(b, np.float64)
+    wg = np.asarray(wg, np.float64)
+    wu = np.asarray(wu, np.float64)
+    n = cnt_gpu.shape[0]
+    assert b.shape[0] == n
+    c_ref = np.zeros(n, np.int64)
+    outside, ties = 0, 0
+    for r0 in range(0, n, chunk):
+        bb = b[r0:r0 + chunk]
+        act = silu(bb @ wg.T) * (bb @ wu.T)
+        c_ref[r0:r0 + chunk] = near_zero_count(act, eps)
+        del act
+        if band:
+            c_min, c_max, _ = count_band(bb, wg, wu, eps)
+            cg = cnt_gpu[r0:r0 + chunk]
+            outside += int(np.sum((cg < c_min) | (cg > c_max)))
+            ties += int(np.sum(c_max - c_min))
+    dfrac = np.abs(sparsity_fraction(cnt_gpu, d_ff) - sparsity_fraction(c_ref, d_ff))
+    res = dict(rows=n, max_count_diff=int(np.abs(cnt_gpu - c_ref).max()) if n else 0,
+               max_frac_diff=float(dfrac.max()) if n else 0.0)
+    if band:
+        res.update(band_outside=outside, ties=ties)
+    bad = np.nonzero(dfrac > frac_tol)[0]
+    assert bad.size == 0, "rows %s: sparsity fraction off by %s (counts %s vs oracle %s), bar %g" % (
+        bad[:5], dfrac[bad[:5]], cnt_gpu[bad[:5]], c_ref[bad[:5]], frac_tol)
+    return res
+
+
+def fmt_counts(res):
+    s = "count diff max %d (fraction %.2e) over %d rows" % (res["max_count_diff"], res["max_frac_diff"],
+                                                            res["rows"])
+    if "band_outside" in res:
+        s += ", fp32 band: %d rows outside, %d ties" % (res["band_outside"], res["ties"])
+    return s

@@ -34,7 +34,7 @@ def test_every_declared_symbol_is_exported(S):
     for n in names:
         assert hasattr(lib, n), n
     assert set(names) == set(S.EXPORTED)
-    assert S.seer_abi_version() == 102
+    assert S.seer_abi_version() == 103
 
 
 def dims(S, d=4096, h=32, dh=128, i=12288, dtype=1):
@@ -68,6 +68,8 @@ def test_workspace_layout_is_consistent(S):
     assert 0 < a < b
     off = S.seer_layer_workspace_offsets(d, 2000)
     assert off == sorted(off) and off[7] == b and all(o % 256 == 0 for o in off)
+    # bytes [0, 256) are the header holding the status word, for every rows bound
+    assert off[0] == 256 and S.seer_layer_workspace_offsets(d, 0)[0] == 256
     # bf16: qkv, o, h1 (bf16), act, two fp32 statistics, low part of h1 (bf16)
     assert b >= 2000 * (3 * 4096 * 2 + 4096 * 2 * 2 + 12288 * 2 + 8 + 4096 * 2)
 
@@ -246,3 +248,10 @@ def test_sampler_argument_errors(S):
     assert L.seer_remask_step(*rargs(steps=0)) == S.SEER_EINVAL
     assert L.seer_remask_step(*rargs(max_used=8193)) == S.SEER_EUNSUPPORTED
     assert L.seer_remask_step(*rargs(x0=FAKE + 8)) == S.SEER_EINVAL
+
+
+def test_status_reset_argument_errors(S):
+    L = S.load_library()
+    assert L.seer_layer_status_reset(None, 256, 0) == S.SEER_EINVAL
+    assert L.seer_layer_status_reset(FAKE + 4, 256, 0) == S.SEER_EINVAL
+    assert L.seer_layer_status_reset(FAKE, 255, 0) == S.SEER_EWORKSPACE

@@ -1,33 +1,37 @@
 """GPU parity at full size: the LLaDA-8B-shaped layer, B=1 and the B=16 ragged batch.
 
 These run the exact launch sequence bench.py times (step-0 layer with the
-fused count, SNR scan, routing + compaction, truncated step) and compare with
-the oracle where it finishes in seconds:
-  * boundaries: the oracle's SNR criterion on counts it recomputes from the
-    GPU's own detection-layer residual (teacher-forced) over window positions
-    [0, b_gpu + lookahead) -- exactly the positions that decide whether b_gpu
-    is the first qualifying one -- must give b_gpu; b_gpu must also equal the
-    planted boundary; the untethered oracle pipeline on the first sequences
-    must agree too;
-  * counts: within the fp32-consistent band of the teacher-forced count;
+fused count, SNR scan, routing + compaction, truncated step) and compare every
+output with the oracle:
+  * boundaries: equal to the planted ones; the oracle's SNR criterion on the
+    GPU's counts of the whole window gives the same index; the oracle's own
+    step-0 counts (fp64 from the inputs) give it too;
+  * counts: every window row of every sequence, teacher-forced (the oracle
+    recomputes the MLP activations from the GPU's post-attention residual),
+    sparsity fraction within 1e-3; the untethered fraction difference (the
+    oracle's own step 0 from the inputs) is reported;
   * offsets / routes / compacted rows: bit-exact against the oracle router;
-  * hidden states: sampled rows (first, last, around the cut, random) of the
-    step-0 output and of the truncated step against the oracle's layer
-    evaluated for those rows with keys/values over the whole sequence.
+  * hidden states: every row of the step-0 layer and of the truncated step
+    against the oracle's layer on the same inputs (the layer input of both is
+    an input of the path: the bf16 embeddings, and their compacted rows), max
+    relative error within 2e-2; the 99.9th percentile of the per-row error is
+    reported.
 """
 import numpy as np
 import pytest
 
-import oracle
-from gpu_util import check_counts, dev, host, log, rel_err, view_ws
+from gpu_util import check_counts, dev, fmt_counts, host, log, row_errs, view_ws
 from oracle.detect import detect_boundary
-from oracle.layer import layer_forward_rows, rms_norm
+from oracle.layer import layer_forward, rms_norm
 from oracle.route import repack_rows, route_batch
+from oracle.sparsity import sparsity_fraction
 from workloads import WORKLOADS
 from workloads.generate import make_workload
 
 pytestmark = pytest.mark.gpu
 TOL = 2e-2
+NAMES = ["llada_b1", "llada_b16_ragged"]
+_CACHE = {}
 
 
 @pytest.fixture(scope="module")
@@ -38,7 +42,7 @@ def S():
 
 
 def _run_bench_path(S, w, layers, batch):
-    """The bench.py launch sequence; returns device tensors."""
+    """The bench.py launch sequence; returns host arrays."""
     import torch
     from paper_2607_14557_amd.runner import dims_for
     sh = w.shape
@@ -72,48 +76,58 @@ def _run_bench_path(S, w, layers, batch):
     S.seer_batch_repack(desc, [x, y], [x_t, h_t], cu, off, wl, keep, w.batch, cu_t, used, route, ctrl)
     S.seer_layer_forward_varlen(dims, packed, x_t, y_t, cap, cu_t, used, w.batch, 0.0, None, ws)
     torch.cuda.synchronize()
-    return dict(y=host(y), cnt=host(cnt), h1=h1, bnd=host(bnd), keep=host(keep), x_t=host(x_t),
-                h_t=host(h_t), y_t=host(y_t), cu_t=host(cu_t), used=host(used), route=host(route),
-                ctrl=host(ctrl))
+    out = dict(y=host(y), cnt=host(cnt), h1=h1, bnd=host(bnd), keep=host(keep), x_t=host(x_t),
+               h_t=host(h_t), y_t=host(y_t), cu_t=host(cu_t), used=host(used), route=host(route),
+               ctrl=host(ctrl))
+    del packed, ws, x, y, cnt, x_t, h_t, y_t
+    torch.cuda.empty_cache()
+    return out
 
 
-def _sample_rows(rng, S_len, cut, k=4):
-    rows = {0, S_len - 1, max(cut - 1, 0), min(cut, S_len - 1)}
-    rows |= set(int(r) for r in rng.integers(0, S_len, size=k))
-    return np.array(sorted(rows))
+def _get(S, name):
+    if name not in _CACHE:
+        _CACHE.clear()
+        w = WORKLOADS[name]
+        log("full %s: inputs" % name)
+        layers, batch = make_workload(w)
+        W = {k: np.asarray(v, np.float64) for k, v in layers[0].items()}
+        log("full %s: GPU path" % name)
+        g = _run_bench_path(S, w, layers, batch)
+        _CACHE[name] = (w, W, batch, g)
+    return _CACHE[name]
 
 
-@pytest.mark.parametrize("name,n_seq_check,n_untethered", [("llada_b1", 1, 1),
-                                                           ("llada_b16_ragged", 5, 2)])
-def test_full_size_parity(S, name, n_seq_check, n_untethered):
-    w = WORKLOADS[name]
-    sh = w.shape
-    I = sh.d_ff
-    log("full %s: inputs" % name)
-    layers, batch = make_workload(w)
-    W = {k: np.asarray(v, np.float64) for k, v in layers[0].items()}
-    log("full %s: GPU path" % name)
-    g = _run_bench_path(S, w, layers, batch)
-    S_full = w.seq_len_full
-    P = w.prefix_len
-    rng = np.random.default_rng(5)
+def _report_rows(tag, e):
+    q = float(np.quantile(e, 0.999)) if e.size else 0.0
+    log("  %s: %d rows, max rel err %.3e (row %d), 99.9th percentile %.3e, median %.3e" %
+        (tag, e.size, e.max(), int(e.argmax()), q, float(np.median(e))))
+    return q
 
-    # -- boundaries: planted, and the oracle's criterion on teacher-forced counts
+
+@pytest.mark.parametrize("name", NAMES)
+def test_full_boundaries_and_counts(S, name):
+    w, W, batch, g = _get(S, name)
+    I = w.shape.d_ff
+    S_full, P = w.seq_len_full, w.prefix_len
     np.testing.assert_array_equal(g["bnd"], batch.planted)
     np.testing.assert_array_equal(g["keep"], batch.planted + 1)
-    Wg, Wu = W["wg"], W["wu"]
+    worst = dict(max_count_diff=0, max_frac_diff=0.0)
     for b in range(w.batch):
-        hi = min(int(g["bnd"][b]) + 3, w.window)
         r0 = b * S_full + P
-        bn = rms_norm(g["h1"][r0:r0 + hi], W["g2"], w.rms_eps)
-        cg = g["cnt"][r0:r0 + hi]
-        dmax, ties = check_counts(cg, bn, Wg, Wu, w.act_eps, I)
+        bn = rms_norm(g["h1"][r0:r0 + w.window], W["g2"], w.rms_eps)
+        cg = g["cnt"][r0:r0 + w.window]
+        cr = check_counts(cg, bn, W["wg"], W["wu"], w.act_eps, I)
         ib, kb = detect_boundary(cg, I)
         assert ib == g["bnd"][b], "seq %d: oracle criterion on the GPU counts gives %d" % (b, ib)
-        log("  seq %d: boundary %d, count diff %d (ties %d) over %d positions" %
-            (b, ib, dmax, ties, hi))
+        log("  seq %d: boundary %d, teacher-forced %s" % (b, ib, fmt_counts(cr)))
+        worst = {k: max(worst[k], cr[k]) for k in worst}
+    log("  %s teacher-forced counts, all %d window rows: max diff %d, max fraction diff %.2e" %
+        (name, w.batch * w.window, worst["max_count_diff"], worst["max_frac_diff"]))
 
-    # -- routing and compaction against the oracle router
+
+@pytest.mark.parametrize("name", NAMES)
+def test_full_routing_and_compaction(S, name):
+    w, W, batch, g = _get(S, name)
     rt = route_batch(g["keep"], batch.win_len)
     np.testing.assert_array_equal(g["route"][:, 0], rt.path)
     np.testing.assert_array_equal(g["route"][:, 1], rt.group)
@@ -127,33 +141,49 @@ def test_full_size_parity(S, name, n_seq_check, n_untethered):
     np.testing.assert_array_equal(g["h_t"][:cap_e], exp_h)
     assert g["ctrl"][0] == cu_e[-1] and g["ctrl"][7] == 0 and g["ctrl"][8] == 1
 
-    # -- hidden states on sampled rows (keys/values over whole sequences)
-    for b in range(n_seq_check):
-        s0 = b * S_full
-        xs = x_bf[s0:s0 + S_full]
-        rows = _sample_rows(rng, S_full, P + int(batch.planted[b]))
-        ref = layer_forward_rows(xs, S_full, W, sh.n_heads, w.rms_eps, rows)["y"]
-        e0 = rel_err(g["y"][s0 + rows], ref)
-        t0 = int(g["cu_t"][b])
-        St = int(g["used"][b])
-        rows_t = _sample_rows(rng, St, P + int(batch.planted[b]))
-        ref_t = layer_forward_rows(g["x_t"][t0:t0 + St], St, W, sh.n_heads, w.rms_eps, rows_t)["y"]
-        e1 = rel_err(g["y_t"][t0 + rows_t], ref_t)
-        log("  seq %d: full-window rows err %.3e, truncated-step rows err %.3e" % (b, e0, e1))
-        assert e0 <= TOL and e1 <= TOL
 
-    # -- untethered oracle pipeline on the first sequences
-    for b in range(n_untethered):
+@pytest.mark.parametrize("name", NAMES)
+def test_full_step0_every_row(S, name):
+    """The step-0 layer over the full window, every row of every sequence; its
+    input is the path's input, so this is also the untethered comparison: the
+    oracle's own counts must give the planted boundaries."""
+    w, W, batch, g = _get(S, name)
+    sh = w.shape
+    I = sh.d_ff
+    S_full, P = w.seq_len_full, w.prefix_len
+    x_bf = host(dev(batch.x, "bf16"))
+    errs, dfr = [], 0.0
+    for b in range(w.batch):
         s0 = b * S_full
-        res = oracle.run_pipeline(layers, batch.x[s0:s0 + S_full], [0, S_full], batch.win_off[b:b + 1],
-                                  batch.win_len[b:b + 1], sh.n_heads, I, w.rms_eps, w.act_eps, w.l_det)
-        assert int(res.boundary[0]) == int(g["bnd"][b])
-        diff = np.abs(res.counts[P:] - g["cnt"][s0 + P:s0 + S_full])
+        sl = slice(s0, s0 + S_full)
+        y_ref, c_ref = layer_forward(x_bf[sl], [0, S_full], W, sh.n_heads, w.rms_eps, act_eps=w.act_eps)
+        e = row_errs(g["y"][sl], y_ref)
+        errs.append(e)
+        ib, _ = detect_boundary(c_ref[P:], I)
+        assert ib == batch.planted[b], "seq %d: the oracle's own counts give %d" % (b, ib)
+        d_un = np.abs(sparsity_fraction(g["cnt"][sl][P:], I) - sparsity_fraction(c_ref[P:], I)).max()
+        dfr = max(dfr, float(d_un))
+        log("  seq %d: step-0 rows max rel err %.3e; untethered window fraction diff %.2e" %
+            (b, e.max(), d_un))
+        assert e.max() <= TOL, "seq %d row %d: %.3e" % (b, int(e.argmax()), e.max())
+    _report_rows("%s step-0 layer" % name, np.concatenate(errs))
+    log("  %s untethered sparsity fraction diff max %.2e (reported)" % (name, dfr))
+
+
+@pytest.mark.parametrize("name", NAMES)
+def test_full_truncated_step_every_row(S, name):
+    """One truncated denoising step over the compacted batch, every kept row."""
+    w, W, batch, g = _get(S, name)
+    sh = w.shape
+    tot = int(g["cu_t"][-1])
+    y_ref, _ = layer_forward(g["x_t"][:tot], g["cu_t"], W, sh.n_heads, w.rms_eps, seqused=g["used"])
+    errs = []
+    for b in range(w.batch):
         t0 = int(g["cu_t"][b])
-        St = int(g["used"][b])
-        e = rel_err(g["y_t"][t0:t0 + St], res.y_step[:St])
-        e0 = rel_err(g["h_t"][t0:t0 + St], res.y_step0[:St])
-        log("  untethered seq %d: boundary %d, window count diff max %d (fraction %.2e), "
-            "step-0 err %.3e, truncated step err %.3e" %
-            (b, res.boundary[0], diff.max(), diff.max() / I, e0, e))
-        assert e <= TOL and e0 <= TOL
+        sl = slice(t0, t0 + int(g["used"][b]))
+        errs.append(row_errs(g["y_t"][sl], y_ref[sl]))
+        pad = slice(t0 + int(g["used"][b]), int(g["cu_t"][b + 1]))
+        assert np.all(g["y_t"][pad] == 0.0), "seq %d: padding rows must stay zero" % b
+    e = np.concatenate(errs)
+    _report_rows("%s truncated step" % name, e)
+    assert e.max() <= TOL, "row %d: %.3e" % (int(e.argmax()), e.max())

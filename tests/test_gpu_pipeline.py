@@ -12,7 +12,7 @@ import numpy as np
 import pytest
 
 import oracle
-from gpu_util import check_counts, dev, host, log, rel_err, upload_weights, view_ws
+from gpu_util import check_counts, dev, fmt_counts, host, log, rel_err, upload_weights, view_ws
 from oracle.layer import layer_forward, rms_norm
 from oracle.route import repack_rows
 from workloads import WORKLOADS
@@ -69,9 +69,9 @@ def test_pipeline_vs_oracle(S, name):
     off6 = S.seer_layer_workspace_offsets(st.dims, T)   # layout of calls made with rows_ub = T
     h1 = host(view_ws(st.workspace, off6[2], T, sh.d_model, w.dtype))
     b = rms_norm(h1, W64[w.l_det]["g2"], w.rms_eps)
-    dmax, ties = check_counts(host(cnt), b, W64[w.l_det]["wg"], W64[w.l_det]["wu"], w.act_eps,
-                              sh.d_ff)
-    log("  count diff teacher-forced max %d / I=%d, rounding ties %d" % (dmax, sh.d_ff, ties))
+    cr = check_counts(host(cnt), b, W64[w.l_det]["wg"], W64[w.l_det]["wu"], w.act_eps, sh.d_ff,
+                      band=True)
+    log("  teacher-forced %s (I=%d)" % (fmt_counts(cr), sh.d_ff))
 
     # -- the product path: step0 = layers + count + detect + repack + remaining layers
     log("pipeline %s: step0 through the runner" % name)
@@ -84,7 +84,7 @@ def test_pipeline_vs_oracle(S, name):
     np.testing.assert_array_equal(host(r.boundary), res.boundary)
     np.testing.assert_array_equal(host(r.keep_len), res.keep_len)
     cdiff = np.abs(host(r.counts) - res.counts).max()
-    log("  untethered count diff max %d (reported)" % cdiff)
+    log("  untethered count diff max %d (fraction %.2e, reported)" % (cdiff, cdiff / sh.d_ff))
     np.testing.assert_array_equal(host(r.cu_trunc), res.cu_trunc)
     np.testing.assert_array_equal(host(r.seqused), res.seqused)
     route = host(r.route)
@@ -123,3 +123,29 @@ def test_pipeline_vs_oracle(S, name):
     log("  truncated step end-to-end rel err %.3e" % e_end)
     if w.n_layers == 1:
         assert e_end <= tol
+
+
+def test_step0_capacity_and_overflow(S):
+    """The runner's default compacted capacity holds the routing's worst case
+    (every window padded to the longest); a capacity the routed batch does not
+    fit raises SeerError (the repack kernel's status) before any later layer."""
+    import torch
+    w = WORKLOADS["small_bf16_stack"]
+    layers, batch = make_workload(w)
+    T = w.rows_full
+    st = build_stack(w, layers, T + 256)
+    x = dev(batch.x, w.dtype)
+    cu, off, wl = dev(batch.cu_seqlens), dev(batch.win_off), dev(batch.win_len)
+    log("step0: default capacity")
+    r = st.step0(x, cu, off, wl, w.batch, T, w.l_det, w.act_eps, granule=256)
+    torch.cuda.synchronize()
+    worst = int(np.sum(batch.win_off)) + w.batch * int(np.max(batch.win_len))
+    assert r.x_trunc.shape[0] == -(-worst // 256) * 256
+    ctrl = host(r.ctrl)
+    assert ctrl[7] == 0 and ctrl[8] == 1 and ctrl[1] <= r.x_trunc.shape[0]
+    np.testing.assert_array_equal(host(r.boundary), batch.planted)
+    log("step0: a 256-row capacity (the compacted batch needs %d rows)" % int(ctrl[0]))
+    assert ctrl[0] > 256
+    with pytest.raises(S.SeerError) as ei:
+        st.step0(x, cu, off, wl, w.batch, T, w.l_det, w.act_eps, granule=256, trunc_capacity=256)
+    assert ei.value.code == S.SEER_EWORKSPACE

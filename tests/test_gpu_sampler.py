@@ -165,7 +165,8 @@ def test_sampled_denoising_loop(S):
     bufs = [torch.zeros_like(x_w), torch.zeros_like(x_w)]
     cu_h, used_h = host(cu_w), host(used_w)
     max_used = int(used_h.max())
-    W, embh, x0h = _bf(w_lm), _bf(emb), _bf(x0)
+    # only rows [0, cu_w[B]) of the window buffer are written by the library
+    W, embh, x0h = _bf(w_lm), _bf(emb), _bf(x0[:int(cu_h[-1])])
     steps = 4
     x_in = x0
     prev = None
@@ -179,7 +180,7 @@ def test_sampled_denoising_loop(S):
         tg, ph, chf = host(smp.tokens), host(smp.pred), host(smp.conf)
         R = int(cu_h[-1])
         _check_predictions("step %d" % s, ph[:R], chf[:R], _bf(h[:R]), W, w.rms_eps)
-        xg = _bf(x_next)
+        xg = _bf(x_next[:R])
         for b in range(B):
             s0, s1 = int(cu_h[b]), int(cu_h[b + 1])
             ref = remask_step(tok_before[s0:s1], ph[s0:s1], chf[s0:s1].astype(np.float64), int(used_h[b]),

@@ -9,8 +9,8 @@ SeerStack.forward) is run and then replayed call by call to capture the
 intermediates the oracle needs; the replay must reproduce it bit for bit.
 Against the oracle:
   * boundaries: equal to the planted ones, and the oracle's SNR criterion on
-    the GPU counts over window positions [0, b + lookahead) gives b; counts
-    within the fp32-consistent band of the oracle's count recomputed from the
+    the GPU counts of the whole window gives b; on every window row the
+    sparsity fraction is within 1e-3 of the oracle's, recomputed from the
     GPU's own detection-layer residual (teacher-forced);
   * routes, offsets and compacted rows: bit-exact against the oracle router;
   * hidden states: sampled rows of the first and last sequence, teacher-forced
@@ -21,7 +21,7 @@ Against the oracle:
 import numpy as np
 import pytest
 
-from gpu_util import check_counts, dev, host, log, rel_err, view_ws
+from gpu_util import check_counts, dev, fmt_counts, host, log, rel_err, view_ws
 from oracle.detect import detect_boundary
 from oracle.layer import layer_forward_rows, rms_norm
 from oracle.route import repack_rows, route_batch
@@ -111,8 +111,7 @@ def test_stack_parity(S, name):
     win_rows = {}
     for b in range(B):
         r0 = int(batch.cu_seqlens[b]) + P
-        hi = min(int(bnd[b]) + 3, w.window)
-        win_rows[b] = (host(h1_dev[r0:r0 + hi]), host(cnt[r0:r0 + hi]))
+        win_rows[b] = (host(h1_dev[r0:r0 + w.window]), host(cnt[r0:r0 + w.window]))
     y_det = cur
     bnd2 = torch.empty(B, dtype=torch.int32, device="cuda")
     keep2 = torch.empty(B, dtype=torch.int32, device="cuda")
@@ -172,14 +171,17 @@ def test_stack_parity(S, name):
     # -- boundaries and counts against the oracle (teacher-forced)
     log("stack %s: oracle checks" % name)
     W_det = _w64(layer_weights_torch(w, w.l_det, "cuda"))
+    worst = 0.0
     for b in range(B):
         h1, cg = win_rows[b]
-        dmax, ties = check_counts(cg, rms_norm(h1, W_det["g2"], w.rms_eps), W_det["wg"], W_det["wu"],
-                                  w.act_eps, I)
+        cr = check_counts(cg, rms_norm(h1, W_det["g2"], w.rms_eps), W_det["wg"], W_det["wu"],
+                          w.act_eps, I)
         ib, _ = detect_boundary(cg, I)
         assert ib == bnd[b], "seq %d: oracle criterion on the GPU counts gives %d" % (b, ib)
-        log("  seq %d: boundary %d, count diff %d (ties %d) over %d positions" % (b, ib, dmax, ties,
-                                                                                  len(cg)))
+        log("  seq %d: boundary %d, teacher-forced %s (whole window)" % (b, ib, fmt_counts(cr)))
+        worst = max(worst, cr["max_frac_diff"])
+    log("  %s teacher-forced sparsity fraction diff max %.2e over all %d window rows" %
+        (name, worst, B * w.window))
 
     # -- hidden states, teacher-forced at sampled layers
     for l in sorted(set(step0_layers) | set(trunc_layers)):

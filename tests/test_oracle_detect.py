@@ -7,7 +7,7 @@ import numpy as np
 import pytest
 
 from oracle.detect import detect_boundary, detect_batch
-from oracle.sparsity import near_zero_count
+from oracle.sparsity import near_zero_count, sparsity_fraction
 from conftest import GOLDEN
 
 
@@ -106,3 +106,16 @@ def test_count_against_loops():
     c = near_zero_count(act, eps)
     for r in range(6):
         assert c[r] == sum(1 for v in act[r] if abs(v) < eps)
+
+
+def test_sparsity_fraction_hand_values():
+    """The statistic is count / I (Sec. 3.2-3.3): hand values with I = 688 (the
+    tiny layer's SwiGLU width, not a power of two) and I = 12288; a fraction
+    divided by the model width instead (256 or 4096) fails every nonzero case."""
+    f = sparsity_fraction(np.array([0, 1, 43, 344, 688]), 688)
+    np.testing.assert_array_equal(f, [0.0, 1.0 / 688, 0.0625, 0.5, 1.0])
+    f = sparsity_fraction(np.array([[3072, 12288], [0, 96]]), 12288)
+    np.testing.assert_array_equal(f, [[0.25, 1.0], [0.0, 0.0078125]])
+    # as the count's companion: an all-near-zero row is fraction 1, none is 0
+    act = np.array([[0.0, 1e-9, -1e-9, 0.0], [5.0, -5.0, 6.0, -7.0]])
+    np.testing.assert_array_equal(sparsity_fraction(near_zero_count(act, 1e-3), 4), [1.0, 0.0])
