@@ -100,15 +100,49 @@ class Hip:
         return float(f.value)
 
 
+def host_cpu():
+    """The host's CPU model, logical CPU count, the CPUs this process may run
+    on, and the BLAS threads NumPy uses (what the oracle actually runs on)."""
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        avail = len(os.sched_getaffinity(0))
+    except AttributeError:
+        avail = os.cpu_count()
+    try:
+        import numpy  # noqa: F401  (loads the BLAS threadpool)
+        from threadpoolctl import threadpool_info
+        blas = max([i.get("num_threads", 0) for i in threadpool_info() if i.get("user_api") == "blas"]
+                   or [avail])
+    except Exception:
+        blas = avail
+    return {"cpu_model": model, "nproc": os.cpu_count(), "cpus_available": avail, "blas_threads": int(blas)}
+
+
+def layer_flop(sh, seq_rows, used=None):
+    """Algorithmic flop of one layer over sequences of seq_rows rows (keys: the
+    used rows): 2 rows (4 d^2 + 3 d I) in the projections, 4 S_q S_k d in
+    attention (scores and the weighted sum)."""
+    d, I = sh.d_model, sh.d_ff
+    used = seq_rows if used is None else used
+    g = sum(2 * int(s) * (4 * d * d + 3 * d * I) for s in seq_rows)
+    a = sum(4 * int(min(u, s)) * int(u) * d for s, u in zip(seq_rows, used))
+    return g + a
+
+
 def cpu_baseline(w, layers, batch, seconds):
     """Oracle (fp64 NumPy) on the first sequences of the batch, ~`seconds` of work."""
     import numpy as np
     import oracle
-    try:
-        from threadpoolctl import threadpool_info
-        cores = max([i.get("num_threads", 0) for i in threadpool_info()] or [os.cpu_count()])
-    except Exception:
-        cores = os.cpu_count()
+    hc = host_cpu()
+    cores = hc["blas_threads"]
     sh = w.shape
     t0 = time.perf_counter()
     toks = 0
@@ -126,7 +160,92 @@ def cpu_baseline(w, layers, batch, seconds):
     return {"value": toks / dt, "unit": "tokens/s", "cores": int(cores), "kind": "oracle",
             "sample": "oracle step 0 (full-window layer + count + SNR scan + routing/compaction) and "
                       "one truncated step, fp64 NumPy, on the first %d of %d sequences (%.1f s)"
-                      % (nseq, w.batch, dt)}
+                      % (nseq, w.batch, dt),
+            "cpu_model": hc["cpu_model"], "nproc": hc["nproc"], "cpus_available": hc["cpus_available"]}
+
+
+def oracle_timing(names):
+    """The oracle timed on this host's cores, per workload (one JSON line).
+
+    Single-layer workloads: the whole path end to end (step 0: full-window
+    layer with the count, SNR scan, routing + compaction; then one truncated
+    step), in fp64 (the oracle) and in fp32 (the same definitions, for
+    reference).  32-layer stacks: the step-0 detection pass (the layers up to
+    and including the detection layer on the full window, the count, the scan,
+    routing + compaction) and one layer of a truncated step, fp64; their
+    weights are drawn on the GPU (inputs only) and read back one layer at a
+    time.  Seconds are measured, flop counted from the shapes; nothing is
+    extrapolated."""
+    import numpy as np
+    import oracle
+    from oracle.detect import detect_batch
+    from oracle.route import repack_rows, route_batch
+    from workloads import WORKLOADS
+    from workloads.generate import layer_weights_torch, make_stack_batch, make_workload
+
+    hc = host_cpu()
+    out = []
+    for name in names:
+        w = WORKLOADS[name]
+        sh = w.shape
+        S_full = [int(w.seq_len_full)] * w.batch
+        if w.n_layers == 1:
+            layers, batch = make_workload(w)
+            for dt in (np.float64, np.float32):
+                log("oracle %s %s: end to end" % (name, np.dtype(dt).name))
+                t0 = time.perf_counter()
+                res = oracle.run_pipeline(layers, batch.x, batch.cu_seqlens, batch.win_off, batch.win_len,
+                                          sh.n_heads, sh.d_ff, w.rms_eps, w.act_eps, w.l_det, dtype=dt)
+                sec = time.perf_counter() - t0
+                cu_t = np.asarray(res.cu_trunc)
+                f0 = layer_flop(sh, S_full)
+                f1 = layer_flop(sh, np.diff(cu_t), res.seqused)
+                assert np.array_equal(res.boundary, batch.planted)
+                out.append({"workload": name, "what": "step 0 + one truncated step, end to end",
+                            "precision": np.dtype(dt).name, "seconds": round(sec, 3),
+                            "flop": f0 + f1, "gflop_per_s": round((f0 + f1) / sec / 1e9, 1),
+                            "sum_keep_len": int(np.sum(res.keep_len))})
+                log("  %.2f s, %.1f GFLOP/s" % (sec, (f0 + f1) / sec / 1e9))
+            continue
+        import torch
+        batch = make_stack_batch(w, "cuda")
+        host_w = lambda l: {k: v.double().cpu().numpy() for k, v in layer_weights_torch(w, l, "cuda").items()}
+        log("oracle %s: detection pass, layers 0..%d on the full window" % (name, w.l_det))
+        t_pass, h, counts = 0.0, np.asarray(batch.x, np.float64), None
+        for l in range(w.l_det + 1):
+            W = host_w(l)
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            h, c = oracle.layer_forward(h, batch.cu_seqlens, W, sh.n_heads, w.rms_eps,
+                                        act_eps=w.act_eps if l == w.l_det else None)
+            t_pass += time.perf_counter() - t0
+            if l == w.l_det:
+                counts = c
+            del W
+            log("  layer %d done (%.1f s so far)" % (l, t_pass))
+        t0 = time.perf_counter()
+        bnd, keep = detect_batch(counts, batch.cu_seqlens, batch.win_off, batch.win_len, sh.d_ff)
+        rt = route_batch(keep, batch.win_len)
+        x_t, cu_t, used, _ = repack_rows(batch.x, batch.cu_seqlens, batch.win_off, keep, rt.alloc, 256)
+        t_pass += time.perf_counter() - t0
+        assert np.array_equal(bnd, batch.planted)
+        f_pass = (w.l_det + 1) * layer_flop(sh, S_full)
+        out.append({"workload": name, "what": "step-0 detection pass (layers 0..%d, count, scan, "
+                    "routing + compaction)" % w.l_det, "precision": "float64", "seconds": round(t_pass, 3),
+                    "flop": f_pass, "gflop_per_s": round(f_pass / t_pass / 1e9, 1)})
+        del h
+        W = host_w(0)
+        log("oracle %s: one layer of a truncated step (%d rows)" % (name, int(cu_t[-1])))
+        t0 = time.perf_counter()
+        oracle.layer_forward(x_t[:int(cu_t[-1])], cu_t, W, sh.n_heads, w.rms_eps, seqused=used)
+        sec = time.perf_counter() - t0
+        f1 = layer_flop(sh, np.diff(cu_t), used)
+        out.append({"workload": name, "what": "one layer of a truncated step", "precision": "float64",
+                    "seconds": round(sec, 3), "flop": f1, "gflop_per_s": round(f1 / sec / 1e9, 1)})
+        log("  %.1f s" % sec)
+        del W
+    line = {"metric": "oracle seconds on the host cores", "kind": "oracle", **hc, "entries": out}
+    print(json.dumps(line), flush=True)
 
 
 def bench_stack(args, w):
@@ -400,7 +519,13 @@ def main():
     ap.add_argument("--kv-cache", action="store_true",
                     help="32-layer stacks: after step 0, one full truncated step caches every layer's "
                          "prefix keys/values and the remaining steps run on the kept window rows")
+    ap.add_argument("--oracle-timing", default=None, metavar="WORKLOADS",
+                    help="comma-separated workloads: time the oracle on this host's cores instead "
+                         "(single layers end to end in fp64 and fp32; stacks: the step-0 detection "
+                         "pass and one truncated layer) and print one JSON line")
     args = ap.parse_args()
+    if args.oracle_timing:
+        return oracle_timing(args.oracle_timing.split(","))
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:

@@ -16,7 +16,8 @@ layer applies to them row by row.
 
 Everything is computed in float64 from the given (bf16- or fp32-valued) inputs,
 directly from the definitions: softmax is evaluated on the full logit row,
-not online.
+not online.  (``dtype`` exists only so that the benchmark can also time the
+same definitions in float32; every check uses the float64 default.)
 """
 import numpy as np
 
@@ -27,10 +28,10 @@ def silu(z):
     return z / (1.0 + np.exp(-z))
 
 
-def rms_norm(x, gain, eps):
-    x = np.asarray(x, np.float64)
+def rms_norm(x, gain, eps, dtype=np.float64):
+    x = np.asarray(x, dtype)
     ms = np.mean(x * x, axis=-1, keepdims=True)
-    return x / np.sqrt(ms + eps) * np.asarray(gain, np.float64)
+    return x / np.sqrt(ms + eps) * np.asarray(gain, dtype)
 
 
 def softmax_rows(e):
@@ -39,18 +40,18 @@ def softmax_rows(e):
     return p / np.sum(p, axis=-1, keepdims=True)
 
 
-def attention_seq(q, k, v, n_heads, q_rows=None):
+def attention_seq(q, k, v, n_heads, q_rows=None, dtype=np.float64):
     """Bidirectional multi-head attention of one sequence.
 
     q: [Sq, d] (the query rows wanted), k, v: [Sk, d] (every key of the
     sequence).  Returns [Sq, d] = concat_h softmax(q_h k_h^T / sqrt(d_h)) v_h.
     """
-    q = np.asarray(q, np.float64)
-    k = np.asarray(k, np.float64)
-    v = np.asarray(v, np.float64)
+    q = np.asarray(q, dtype)
+    k = np.asarray(k, dtype)
+    v = np.asarray(v, dtype)
     d = q.shape[1]
     dh = d // n_heads
-    out = np.empty((q.shape[0], d), np.float64)
+    out = np.empty((q.shape[0], d), dtype)
     for h in range(n_heads):
         sl = slice(h * dh, (h + 1) * dh)
         e = q[:, sl] @ k[:, sl].T / np.sqrt(dh)
@@ -58,12 +59,12 @@ def attention_seq(q, k, v, n_heads, q_rows=None):
     return out
 
 
-def _w(W, name):
-    return np.asarray(W[name], np.float64)
+def _w(W, name, dtype=np.float64):
+    return np.asarray(W[name], dtype)
 
 
 def layer_forward_rows(x_seq, used, W, n_heads, rms_eps, rows, want_act=False, rope_theta=None,
-                       pos_offset=0):
+                       pos_offset=0, dtype=np.float64):
     """Layer outputs for selected rows of one sequence.
 
     x_seq: [S, d] rows of one sequence; ``used``: rows [0, used) are real,
@@ -72,30 +73,30 @@ def layer_forward_rows(x_seq, used, W, n_heads, rms_eps, rows, want_act=False, r
     and when want_act the SwiGLU activation act [len(rows), I] and the
     intermediates h1.
     """
-    x_seq = np.asarray(x_seq, np.float64)
+    x_seq = np.asarray(x_seq, dtype)
     rows = np.asarray(rows, np.int64)
-    g1, g2 = _w(W, "g1"), _w(W, "g2")
+    g1, g2 = _w(W, "g1", dtype), _w(W, "g2", dtype)
     # attention sub-block
-    a_keys = rms_norm(x_seq[:used], g1, rms_eps)
-    k = a_keys @ _w(W, "wk").T
-    v = a_keys @ _w(W, "wv").T
+    a_keys = rms_norm(x_seq[:used], g1, rms_eps, dtype)
+    k = a_keys @ _w(W, "wk", dtype).T
+    v = a_keys @ _w(W, "wv", dtype).T
     xr = x_seq[rows]
-    ar = rms_norm(xr, g1, rms_eps)
-    q = ar @ _w(W, "wq").T
+    ar = rms_norm(xr, g1, rms_eps, dtype)
+    q = ar @ _w(W, "wq", dtype).T
     if rope_theta:
         k = apply_rope(k, pos_offset + np.arange(used), n_heads, rope_theta)
         q = apply_rope(q, pos_offset + rows, n_heads, rope_theta)
     o = np.zeros_like(xr)
     real = rows < used
     if used > 0 and np.any(real):
-        o[real] = attention_seq(q[real], k, v, n_heads)
-    h1 = xr + o @ _w(W, "wo").T
+        o[real] = attention_seq(q[real], k, v, n_heads, dtype=dtype)
+    h1 = xr + o @ _w(W, "wo", dtype).T
     # SwiGLU MLP sub-block
-    b = rms_norm(h1, g2, rms_eps)
-    gate = b @ _w(W, "wg").T
-    up = b @ _w(W, "wu").T
+    b = rms_norm(h1, g2, rms_eps, dtype)
+    gate = b @ _w(W, "wg", dtype).T
+    up = b @ _w(W, "wu", dtype).T
     act = silu(gate) * up
-    y = h1 + act @ _w(W, "wd").T
+    y = h1 + act @ _w(W, "wd", dtype).T
     out = {"y": y}
     if want_act:
         out["act"] = act
@@ -103,14 +104,15 @@ def layer_forward_rows(x_seq, used, W, n_heads, rms_eps, rows, want_act=False, r
     return out
 
 
-def layer_forward(x, cu_seqlens, W, n_heads, rms_eps, seqused=None, act_eps=None, rope_theta=None):
+def layer_forward(x, cu_seqlens, W, n_heads, rms_eps, seqused=None, act_eps=None, rope_theta=None,
+                  dtype=np.float64):
     """One layer over packed sequences (rows of sequence b are cu[b]..cu[b+1]).
 
     Returns (y [T, d] float64, counts [T] int64 or None).  ``counts`` is the
     per-row number of SwiGLU activations with |act| < act_eps, for every row.
     """
     from .sparsity import near_zero_count
-    x = np.asarray(x, np.float64)
+    x = np.asarray(x, dtype)
     cu = np.asarray(cu_seqlens, np.int64)
     B = len(cu) - 1
     y = np.array(x, copy=True)
@@ -122,7 +124,7 @@ def layer_forward(x, cu_seqlens, W, n_heads, rms_eps, seqused=None, act_eps=None
         if S == 0:
             continue
         r = layer_forward_rows(x[s0:s1], used, W, n_heads, rms_eps, np.arange(S),
-                               want_act=act_eps is not None, rope_theta=rope_theta)
+                               want_act=act_eps is not None, rope_theta=rope_theta, dtype=dtype)
         y[s0:s1] = r["y"]
         if act_eps is not None:
             counts[s0:s1] = near_zero_count(r["act"], act_eps)

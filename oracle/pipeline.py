@@ -39,13 +39,13 @@ class PipelineResult:
 def run_pipeline(layers: List[dict], x, cu_seqlens, win_off, win_len, n_heads, d_ff,
                  rms_eps, act_eps, l_det, policy=POLICY_HYBRID, tau_pad=Fraction(1, 5),
                  granule=1, tau=Fraction(3, 100), gamma=Fraction(3, 5), lookahead=3,
-                 run_trunc_step=True):
-    x = np.asarray(x, np.float64)
+                 run_trunc_step=True, dtype=np.float64):
+    x = np.asarray(x, dtype)
     h = x
     counts = None
     for l in range(l_det + 1):
         h, c = layer_forward(h, cu_seqlens, layers[l], n_heads, rms_eps,
-                             act_eps=act_eps if l == l_det else None)
+                             act_eps=act_eps if l == l_det else None, dtype=dtype)
         if l == l_det:
             counts = c
     boundary, keep = detect_batch(counts, cu_seqlens, win_off, win_len, d_ff,
@@ -54,12 +54,12 @@ def run_pipeline(layers: List[dict], x, cu_seqlens, win_off, win_len, n_heads, d
     h_t, cu_t, used, cap = repack_rows(h, cu_seqlens, win_off, keep, route.alloc, granule)
     x_t, _, _, _ = repack_rows(x, cu_seqlens, win_off, keep, route.alloc, granule)
     for l in range(l_det + 1, len(layers)):
-        h_t, _ = layer_forward(h_t, cu_t, layers[l], n_heads, rms_eps, seqused=used)
+        h_t, _ = layer_forward(h_t, cu_t, layers[l], n_heads, rms_eps, seqused=used, dtype=dtype)
     y_step = None
     if run_trunc_step:
         y_step = x_t
         for l in range(len(layers)):
-            y_step, _ = layer_forward(y_step, cu_t, layers[l], n_heads, rms_eps, seqused=used)
+            y_step, _ = layer_forward(y_step, cu_t, layers[l], n_heads, rms_eps, seqused=used, dtype=dtype)
     return PipelineResult(counts=counts, boundary=boundary, keep_len=keep, route=route,
                           cu_trunc=cu_t, seqused=used, capacity=cap, x_trunc=x_t,
                           y_step0=h_t, y_step=y_step)

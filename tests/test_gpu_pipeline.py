@@ -69,8 +69,10 @@ def test_pipeline_vs_oracle(S, name):
     off6 = S.seer_layer_workspace_offsets(st.dims, T)   # layout of calls made with rows_ub = T
     h1 = host(view_ws(st.workspace, off6[2], T, sh.d_model, w.dtype))
     b = rms_norm(h1, W64[w.l_det]["g2"], w.rms_eps)
+    # fp32 layers store the activations unrounded: the kernel's own values
+    act_gpu = host(view_ws(st.workspace, off6[3], T, sh.d_ff, w.dtype)) if w.dtype == "f32" else None
     cr = check_counts(host(cnt), b, W64[w.l_det]["wg"], W64[w.l_det]["wu"], w.act_eps, sh.d_ff,
-                      band=True)
+                      band=True, act_gpu=act_gpu)
     log("  teacher-forced %s (I=%d)" % (fmt_counts(cr), sh.d_ff))
 
     # -- the product path: step0 = layers + count + detect + repack + remaining layers
