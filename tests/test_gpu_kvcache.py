@@ -92,13 +92,14 @@ def test_cached_truncated_step(S, name):
     np.testing.assert_array_equal(cu_w_h, np.concatenate([[0], np.cumsum(rt.alloc)]))
     np.testing.assert_array_equal(used_w_h, keep)
     np.testing.assert_array_equal(host(route_w), np.stack([rt.path, rt.group, rt.alloc], 1))
-    xw_h = host(x_w)
+    tot_w = int(cu_w_h[-1])
+    cap_w = ((tot_w + granule - 1) // granule) * granule
+    xw_h = host(x_w[:cap_w])                  # the repack writes rows up to the routed capacity only
     for b in range(B):
         s0 = int(batch.cu_seqlens[b]) + int(P[b])
         np.testing.assert_array_equal(xw_h[cu_w_h[b]:cu_w_h[b] + keep[b]], host(x[s0:s0 + keep[b]]))
         assert not np.any(xw_h[cu_w_h[b] + keep[b]:cu_w_h[b + 1]])
-    tot_w = int(cu_w_h[-1])
-    assert not np.any(xw_h[tot_w:((tot_w + granule - 1) // granule) * granule])
+    assert not np.any(xw_h[tot_w:cap_w])
 
     # -- full truncated step, caching each layer's prefix K | V
     cu_kv_h = np.concatenate([[0], np.cumsum(P)]).astype(np.int64)
@@ -135,7 +136,7 @@ def test_cached_truncated_step(S, name):
     torch.cuda.synchronize()
 
     # -- against the full step's window rows
-    yf, yc = host(y_full), host(cur)
+    yf, yc = host(y_full[:int(cu_t_h[-1])]), host(cur[:tot_w])    # the rows the layers write
     worst = 0.0
     for b in range(B):
         a = yf[cu_t_h[b] + P[b]:cu_t_h[b] + P[b] + keep[b]]

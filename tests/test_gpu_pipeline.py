@@ -95,25 +95,25 @@ def test_pipeline_vs_oracle(S, name):
     np.testing.assert_array_equal(route[:, 2], res.route.alloc)
     ctrl = host(r.ctrl)
     assert ctrl[0] == res.cu_trunc[-1] and ctrl[1] == res.capacity and ctrl[7] == 0 and ctrl[8] == 1
-    np.testing.assert_array_equal(host(r.x_trunc)[:res.capacity], res.x_trunc)
+    np.testing.assert_array_equal(host(r.x_trunc[:res.capacity]), res.x_trunc)
 
     # -- step-0 output (compacted) and the truncated step, gated per layer
     cu_t = r.cu_trunc
     used = r.seqused
     if w.n_layers == 1:
-        e0 = rel_err(host(r.h_trunc)[:int(res.cu_trunc[-1])], res.y_step0[:int(res.cu_trunc[-1])])
+        e0 = rel_err(host(r.h_trunc[:int(res.cu_trunc[-1])]), res.y_step0[:int(res.cu_trunc[-1])])
         log("  step-0 output rel err %.3e" % e0)
         assert e0 <= tol
     else:
         log("  step-0 end-to-end rel err %.3e (reported)" %
-            rel_err(host(r.h_trunc)[:int(res.cu_trunc[-1])], res.y_step0[:int(res.cu_trunc[-1])]))
+            rel_err(host(r.h_trunc[:int(res.cu_trunc[-1])]), res.y_step0[:int(res.cu_trunc[-1])]))
     tot = int(res.cu_trunc[-1])          # the layer writes rows [0, cu[B]) only
     cur = r.x_trunc
     for l in range(w.n_layers):
         nxt = torch.zeros_like(cur)
         st.layer(l, cur, nxt, cu_t, used, w.batch, cap)
         torch.cuda.synchronize()
-        xin = host(cur)[:tot]
+        xin = host(cur[:tot])
         y_ref, _ = layer_forward(xin, res.cu_trunc, W64[l], sh.n_heads, w.rms_eps, seqused=res.seqused)
         y = host(nxt)
         e = rel_err(y[:tot], y_ref)

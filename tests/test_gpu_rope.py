@@ -133,7 +133,7 @@ def test_rope_cached_step(S):
         cur = nxt
     torch.cuda.synchronize()
     cu_t_h, cu_w_h = host(cu_t), host(cu_w)
-    yf, yc = host(y_full), host(cur)
+    yf, yc = host(y_full[:int(cu_t_h[-1])]), host(cur[:int(cu_w_h[-1])])    # the rows the layers write
     worst = 0.0
     for b in range(B):
         a = yf[cu_t_h[b] + P[b]:cu_t_h[b] + P[b] + keep[b]]
