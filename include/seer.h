@@ -196,6 +196,29 @@ int seer_layer_forward_varlen(const seer_dims* dims, const void* w_packed,
                               void* workspace, size_t workspace_bytes,
                               hipStream_t stream);
 
+/* seer_layer_forward_varlen for callers that cannot allocate (code recorded
+ * into a graph, tight serving loops, hosts that forbid allocation): the same
+ * kernels, with the workspace taken from a device array inside the library
+ * instead of a caller buffer.  The array holds 256 MiB (268435456 bytes) per
+ * GPU the library runs on, from its first call on that device until the
+ * process ends; the call allocates nothing (the array's device address is
+ * looked up once per device, on the first call made with it current).
+ * Arguments as in seer_layer_forward_varlen, without the workspace; status:
+ * optional device int32 that receives the SEER_STATUS_* bits of this call
+ * (atomic OR; the caller zeroes it), NULL for none.  Limit: a rows bound
+ * whose seer_layer_workspace_bytes(dims, total_rows_ub) exceeds 268435456 is
+ * refused with SEER_EWORKSPACE (the LLaDA-8B layer shape, d_model 4096 and
+ * d_ff 12288 in bf16, takes up to 3640 rows).  Every call on one GPU shares
+ * that GPU's array: calls that overlap in time on one GPU (other streams,
+ * other host threads) race and must not be issued.  Intermediates are not
+ * exposed (seer_layer_workspace_offsets does not apply).  Errors: as
+ * seer_layer_forward_varlen; EWORKSPACE (rows bound too large), EHIP (the
+ * array could not be located on the current device). */
+int seer_layer_forward_varlen_noalloc(const seer_dims* dims, const void* w_packed, const void* x_in,
+                                      void* x_out, int32_t total_rows_ub, const int32_t* cu_seqlens,
+                                      const int32_t* seqused, int32_t batch, float act_eps,
+                                      int32_t* act_count, int32_t* status, hipStream_t stream);
+
 /* As seer_layer_forward_varlen, recording events[k] (created by the caller)
  * on `stream` around its kernels for live per-kernel timing:
  *   events[0] -> [1] RMS statistics of x       [1] -> [2] QKV GEMM

@@ -5,6 +5,7 @@
 #include <stdarg.h>
 #include <stdio.h>
 
+#include <mutex>
 #include <string>
 
 #include "../../include/seer.h"
@@ -162,7 +163,8 @@ static int layer_forward_impl(const seer_dims* dims, const void* w_packed, const
                               const int32_t* seqused, int32_t batch, float act_eps,
                               int32_t* act_count, void* workspace, size_t workspace_bytes,
                               hipStream_t stream, hipEvent_t* ev, const void* kv_cache = nullptr,
-                              const int32_t* cu_kv = nullptr) {
+                              const int32_t* cu_kv = nullptr, bool own_status = false,
+                              int32_t* status = nullptr) {
   int rc = check_dims(dims);
   if (rc) return rc;
   if (!w_packed || !x_in || !x_out || !cu_seqlens || !workspace)
@@ -231,7 +233,9 @@ static int layer_forward_impl(const seer_dims* dims, const void* w_packed, const
     g.m_ptr = m_ptr; g.m_ub = R; g.N = 3 * d; g.K = d;
     g.lda = d; g.ldb = d; g.ldc = 3 * d;
     g.f16_col0 = bf16 ? 2 * d : 0;     // V goes to the attention's fp16 PV product
-    g.status = bf16 ? reinterpret_cast<int*>(ws) : nullptr;   // V beyond fp16 range is reported
+    // V beyond fp16 range is reported in the workspace status word (or in the
+    // caller's word, for the no-allocation entry point)
+    g.status = !bf16 ? nullptr : own_status ? status : reinterpret_cast<int*>(ws);
     g.perm_col1 = bf16 ? 2 * d : 0;    // q and k rows are packed head-permuted
     if (rope && bf16) {
       // q and k rotated in the epilogue, where each lane holds rotary pairs
@@ -308,6 +312,59 @@ int seer_layer_forward_varlen(const seer_dims* dims, const void* w_packed, const
                               hipStream_t stream) {
   return layer_forward_impl(dims, w_packed, x_in, x_out, total_rows_ub, cu_seqlens, seqused, batch,
                             act_eps, act_count, workspace, workspace_bytes, stream, nullptr);
+}
+
+}  // extern "C"
+
+// ---- the layer without allocation ------------------------------------------
+// A workspace that lives in the library, for callers that cannot allocate:
+// one copy of this array per GPU, held until the process ends.  Host code
+// never uses the array's name as an address: its device address is looked up
+// once per device (hipGetSymbolAddress) and kept in scratch_ptr.
+static constexpr size_t kScratchBytes = (size_t)256 << 20;
+static __device__ __attribute__((aligned(256))) uint8_t scratch[kScratchBytes];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+int scratch_of_current_device(void** out) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return hip_fail("hipGetDevice");
+  if (dev < 0 || dev >= kMaxDevices) return fail(SEER_EUNSUPPORTED, "device %d beyond the %d supported", dev, kMaxDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_ptr[dev] == nullptr) {
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || p == nullptr)
+      return fail(SEER_EHIP, "hipGetSymbolAddress(scratch) on device %d: %s", dev, hipGetErrorString(e));
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return SEER_OK;
+}
+}  // namespace
+
+extern "C" {
+
+int seer_layer_forward_varlen_noalloc(const seer_dims* dims, const void* w_packed, const void* x_in,
+                                      void* x_out, int32_t total_rows_ub, const int32_t* cu_seqlens,
+                                      const int32_t* seqused, int32_t batch, float act_eps,
+                                      int32_t* act_count, int32_t* status, hipStream_t stream) {
+  int rc = check_dims(dims);
+  if (rc) return rc;
+  if (total_rows_ub < 1) return fail(SEER_EINVAL, "total_rows_ub must be >= 1 (got %d)", total_rows_ub);
+  const size_t need = ws_layout(dims, total_rows_ub).total;
+  if (need > kScratchBytes)
+    return fail(SEER_EWORKSPACE,
+                "total_rows_ub %d needs %zu bytes of workspace; the no-allocation entry point has %zu "
+                "(seer_layer_workspace_bytes gives the need per rows bound)", total_rows_ub, need, kScratchBytes);
+  void* ws = nullptr;
+  rc = scratch_of_current_device(&ws);
+  if (rc) return rc;
+  return layer_forward_impl(dims, w_packed, x_in, x_out, total_rows_ub, cu_seqlens, seqused, batch, act_eps,
+                            act_count, ws, kScratchBytes, stream, nullptr, nullptr, nullptr, true, status);
 }
 
 int seer_layer_forward_varlen_timed(const seer_dims* dims, const void* w_packed, const void* x_in,

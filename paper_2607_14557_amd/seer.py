@@ -21,6 +21,7 @@ SEER_STATUS_V_RANGE = 1
 
 EXPORTED = ("seer_prepacked_bytes", "seer_prepack_weights", "seer_layer_workspace_bytes",
             "seer_layer_status_reset", "seer_layer_workspace_offsets", "seer_layer_forward_varlen",
+            "seer_layer_forward_varlen_noalloc",
             "seer_layer_forward_varlen_timed", "seer_step0_detect", "seer_batch_repack",
             "seer_layer_forward_cached", "seer_kv_export", "seer_graph_begin", "seer_graph_end",
             "seer_graph_launch", "seer_graph_destroy", "seer_lm_head_workspace_bytes", "seer_lm_head_prepack",
@@ -96,6 +97,9 @@ def load_library():
     L.seer_layer_forward_varlen.argtypes = [ctypes.POINTER(seer_dims), _P, _P, _P, _I, _P, _P, _I,
                                             ctypes.c_float, _P, _P, ctypes.c_size_t, _P]
     L.seer_layer_forward_varlen.restype = ctypes.c_int
+    L.seer_layer_forward_varlen_noalloc.argtypes = [ctypes.POINTER(seer_dims), _P, _P, _P, _I, _P, _P, _I,
+                                                    ctypes.c_float, _P, _P, _P]
+    L.seer_layer_forward_varlen_noalloc.restype = ctypes.c_int
     L.seer_layer_forward_varlen_timed.argtypes = L.seer_layer_forward_varlen.argtypes + [
         ctypes.POINTER(_P)]
     L.seer_layer_forward_varlen_timed.restype = ctypes.c_int
@@ -191,6 +195,13 @@ def seer_layer_workspace_offsets(dims, max_rows):
     off = (ctypes.c_size_t * 8)()
     _check(load_library().seer_layer_workspace_offsets(ctypes.byref(dims), int(max_rows), off))
     return list(off)
+
+
+def seer_layer_forward_varlen_noalloc(dims, w_packed, x_in, x_out, total_rows_ub, cu_seqlens, seqused,
+                                      batch, act_eps, act_count, status=None, stream=None):
+    _check(load_library().seer_layer_forward_varlen_noalloc(
+        ctypes.byref(dims), _ptr(w_packed), _ptr(x_in), _ptr(x_out), int(total_rows_ub), _ptr(cu_seqlens),
+        _ptr(seqused), int(batch), float(act_eps), _ptr(act_count), _ptr(status), _stream(stream)))
 
 
 def seer_layer_forward_varlen(dims, w_packed, x_in, x_out, total_rows_ub, cu_seqlens, seqused,
