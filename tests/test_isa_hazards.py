@@ -19,9 +19,10 @@ HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 def _asm(tmp_path, name):
     src = os.path.join(ROOT, "paper_2607_14557_amd", "csrc", name)
     out = tmp_path / (name + ".s")
+    from paper_2607_14557_amd.build import FILE_FLAGS
     cmd = [HIPCC, "--offload-arch=gfx950", "-O3", "-std=c++17", "--cuda-device-only", "-S",
            "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-           "-I" + os.path.join(ROOT, "include"), src, "-o", str(out)]
+           "-I" + os.path.join(ROOT, "include")] + FILE_FLAGS.get(name, []) + [src, "-o", str(out)]
     subprocess.run(cmd, check=True, capture_output=True)
     return kernel_bodies(out.read_text())
 
