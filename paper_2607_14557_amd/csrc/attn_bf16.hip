@@ -238,31 +238,32 @@ __global__ __launch_bounds__(NT, 2) void attn_bf16_kernel(AttnParams p) {
         for (int r = 0; r < 16; ++r) o[i][r] *= alpha;
     }
     const float mc = m_run * c;
-    float lsum = 0.0f;
 #pragma unroll
     for (int i = 0; i < 2; ++i)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const float e = __builtin_amdgcn_exp2f(s[i][r] * c - mc);
-        s[i][r] = e;
-        lsum += e;
-      }
-    l_run += lsum;
+      for (int r = 0; r < 16; ++r) s[i][r] = __builtin_amdgcn_exp2f(s[i][r] * c - mc);
 
     // O^T += V^T P^T over four 16-key slices x four 32-dim tiles; the V^T
     // fragment of step n + 2 is read while step n multiplies.
     {
+      // The row sum is taken over the fp16 probabilities the product uses:
+      // one v_dot2_f32_f16 with (1, 1) per packed pair, accumulated in fp32.
       f16x8_t pf[4];
+      float lsum = 0.0f;
+      const f16x2_t one2 = {(_Float16)1.0f, (_Float16)1.0f};
 #pragma unroll
       for (int sl = 0; sl < 4; ++sl) {
         const int i = sl >> 1, hf = sl & 1;
         u32x4_t pk;
-        pk[0] = pack_h2(s[i][hf * 8 + 0], s[i][hf * 8 + 1]);
-        pk[1] = pack_h2(s[i][hf * 8 + 2], s[i][hf * 8 + 3]);
-        pk[2] = pack_h2(s[i][hf * 8 + 4], s[i][hf * 8 + 5]);
-        pk[3] = pack_h2(s[i][hf * 8 + 6], s[i][hf * 8 + 7]);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const f16x2_t h = __builtin_convertvector(f32x2_t{s[i][hf * 8 + 2 * e], s[i][hf * 8 + 2 * e + 1]}, f16x2_t);
+          lsum = __builtin_amdgcn_fdot2(h, one2, lsum, false);
+          pk[e] = __builtin_bit_cast(uint32_t, h);
+        }
         pf[sl] = __builtin_bit_cast(f16x8_t, pk);
       }
+      l_run += lsum;
       // A operand of step n (16-key slice sl = n/4, 32-dim tile dt = n%4): lane
       // l needs 8 keys of dim 32 dt + l%32, in the order the P fragment holds
       // them (keys 16 hf + 4 kh + 0..3, then + 8).  In each group of 16 lanes
