@@ -118,7 +118,10 @@ int seer_prepack_weights(const seer_dims* dims, const seer_layer_weights* src,
 
 /* Workspace bytes needed by seer_layer_forward_varlen for up to max_rows
  * packed rows (qkv, attention output, post-attention residual, SwiGLU
- * activations and two per-row RMS statistics), plus a 256-byte header.
+ * activations and two per-row RMS statistics), plus a 256-byte header and,
+ * for bf16 layers, 64 MiB for the fp32 partial sums of projections that split
+ * their K dimension (those whose 256x256 output tiles would fill at most a
+ * third of the GPU's compute units: few rows, as in prefix-cached steps).
  *
  * Status word: the int32 at byte 0 of the workspace (for every rows bound).
  * Layer calls only ever set bits in it (atomic OR), so it accumulates over
@@ -208,7 +211,7 @@ int seer_layer_forward_varlen(const seer_dims* dims, const void* w_packed,
  * (atomic OR; the caller zeroes it), NULL for none.  Limit: a rows bound
  * whose seer_layer_workspace_bytes(dims, total_rows_ub) exceeds 268435456 is
  * refused with SEER_EWORKSPACE (the LLaDA-8B layer shape, d_model 4096 and
- * d_ff 12288 in bf16, takes up to 3640 rows).  Every call on one GPU shares
+ * d_ff 12288 in bf16, takes up to 2730 rows).  Every call on one GPU shares
  * that GPU's array: calls that overlap in time on one GPU (other streams,
  * other host threads) race and must not be issued.  Intermediates are not
  * exposed (seer_layer_workspace_offsets does not apply).  Errors: as

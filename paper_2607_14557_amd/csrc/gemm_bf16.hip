@@ -106,12 +106,14 @@ __device__ __forceinline__ void seer_slice_schedule() {
   __builtin_amdgcn_sched_group_barrier(0x008, NM - NR / 2 - NV, 0);
 }
 
-// One BMTx256 output tile over the whole K range.  BMT = 256 is the main
-// tile; BMT = 128 serves the halves of the tiles of a partly filled last
-// round.  Wave w owns columns n0 + 64 w .. +63 and all BMT rows.
-template <int EPI, int BMT>
+// One BMTx256 output tile over K tiles [kt0, kt0 + KT) of 64.  BMT = 256 is
+// the main tile; BMT = 128 serves the halves of the tiles of a partly filled
+// last round.  Wave w owns columns n0 + 64 w .. +63 and all BMT rows.  PART:
+// the tile is split `split` of a K-split launch, and its fp32 sums go to the
+// partial scratch instead of through the epilogue.
+template <int EPI, int BMT, bool PART = false>
 __device__ __forceinline__ void gemm_tile(const GemmParams& p, uint8_t* st0, uint8_t* st1, uint8_t* st2, uint8_t* st3,
-                                          int M, int m0, int n0) {
+                                          int M, int m0, int n0, int kt0, int KT, int split = 0) {
   constexpr int NI = BMT / 32;                      // 32-row MFMA tiles per wave
   constexpr int NA = BMT / 32;                      // A loads (1 KiB each) per wave and K tile
   constexpr int AP = NA / 4;                        // ... per slice
@@ -141,11 +143,10 @@ __device__ __forceinline__ void gemm_tile(const GemmParams& p, uint8_t* st0, uin
     ga = ga < M ? ga : M - 1;
     a_src[i] = (uint32_t)ga * (uint32_t)p.lda * 2u + (uint32_t)(((lane & 7) ^ swz(row)) << 4);
   }
-  const int KT = p.K / BK;
   // quarter q (instructions AP q .. AP q + AP - 1) of A tile t into stage stg
   auto dma_a = [&](uint8_t* stg, int t, int q) {
     const int t_ = t < KT ? t : KT - 1;
-    const uint32_t ko = (uint32_t)t_ * (BK * 2);
+    const uint32_t ko = (uint32_t)(kt0 + t_) * (BK * 2);
 #pragma unroll
     for (int i = AP * q; i < AP * q + AP; ++i)
       __builtin_amdgcn_raw_ptr_buffer_load_lds(rsa, (lds_void_t*)(stg + 8 * (NA * wv + i) * ROW_BYTES), 16, a_src[i],
@@ -189,7 +190,7 @@ __device__ __forceinline__ void gemm_tile(const GemmParams& p, uint8_t* st0, uin
 #define SEER_GLOAD_B(BQ, T, KS)                                                     \
   {                                                                                 \
     const int t_ = (T) < KT ? (T) : KT - 1;                                         \
-    const char* bk_ = Bb + (size_t)t_ * B_TILE + (KS) * B_SLICE;                    \
+    const char* bk_ = Bb + (size_t)(kt0 + t_) * B_TILE + (KS) * B_SLICE;            \
     _Pragma("unroll") for (int j = 0; j < 2; ++j)                                   \
       BQ[j][KS] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const u32x4_t*>(bk_ + b_off[j])); \
   }
@@ -261,6 +262,25 @@ __device__ __forceinline__ void gemm_tile(const GemmParams& p, uint8_t* st0, uin
 #undef SEER_GLOAD_B
 #undef SEER_FLOAD
 #undef SEER_TILE
+
+  // ---- K split: the fp32 sums of this split, row-major in the packed column
+  // order of the weight (the finalize kernel applies the epilogue) ----------
+  if constexpr (PART) {
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+      const int row = m0 + i * 32 + fr;
+      if (row < M) {
+        float* prow = p.partial + ((size_t)split * (size_t)p.m_ub + (size_t)row) * (size_t)p.N + wcol + 4 * fhalf;
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+          for (int q = 0; q < 4; ++q)
+            *reinterpret_cast<f32x4_t*>(prow + 32 * j + 8 * q) =
+                f32x4_t{acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
+      }
+    }
+    return;
+  }
 
   // ---- epilogue -----------------------------------------------------------
   // The MFMAs take the B fragment as the matrix-core row operand, so tile
@@ -554,21 +574,159 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmParams p) {
     if (2 * rem <= p.n_units) full = ntiles - rem;
   }
   const int u = blockIdx.x;
-  if (u >= full + 2 * (ntiles - full)) return;
+  const int KT = p.K / BK;
   int tm, tn;
+  if (u >= full + 2 * (ntiles - full)) return;
   if (u < full) {
     raster(xcd_remap(u, full), tiles_m, tiles_n, tm, tn);
-    gemm_tile<EPI, 256>(p, st0, st1, st2, st3, M, tm * 256, tn * 256);
+    gemm_tile<EPI, 256>(p, st0, st1, st2, st3, M, tm * 256, tn * 256, 0, KT);
   } else {
     const int v = u - full;
     raster(full + (v >> 1), tiles_m, tiles_n, tm, tn);
     const int m0 = tm * 256 + (v & 1) * 128;
     if (m0 >= M) return;
-    gemm_tile<EPI, 128>(p, st0, st1, st2, st3, M, m0, tn * 256);
+    gemm_tile<EPI, 128>(p, st0, st1, st2, st3, M, m0, tn * 256, 0, KT);
   }
 }
 
-int launch_gemm_bf16(int epi, const GemmParams& p, hipStream_t s) {
+// K-split launches (a kernel of its own, so that the register allocation of
+// the main kernel does not change): unit u computes split u % S of tile u / S
+// over K tiles [s KT/S, (s+1) KT/S) and stores its fp32 sums; the host chose S
+// so that KT/S is even and the units fit one round.
+template <int EPI>
+__global__ __launch_bounds__(NT, 1) void gemm_bf16_split_kernel(GemmParams p) {
+  __shared__ __attribute__((aligned(1024))) uint8_t st0[256 * ROW_BYTES];
+  __shared__ __attribute__((aligned(1024))) uint8_t st1[256 * ROW_BYTES];
+  __shared__ __attribute__((aligned(1024))) uint8_t st2[256 * ROW_BYTES];
+  __shared__ __attribute__((aligned(1024))) uint8_t st3[256 * ROW_BYTES];
+  const int M = rows_from(p.m_ptr, p.m_ub);
+  const int tiles_m = (M + 255) / 256;
+  const int tiles_n = p.N / 256;
+  const int S = p.k_splits;
+  const int u = blockIdx.x;
+  if (u >= tiles_m * tiles_n * S) return;
+  const int tile = u / S, sp = u - tile * S;
+  const int kts = p.K / BK / S;
+  int tm, tn;
+  raster(tile, tiles_m, tiles_n, tm, tn);
+  gemm_tile<EPI, 256, true>(p, st0, st1, st2, st3, M, tm * 256, tn * 256, sp * kts, kts, sp);
+}
+
+// The epilogue of a K-split launch: for row r < M and 8 consecutive output
+// columns per thread, the splits' fp32 sums are added in split order (the
+// result does not depend on timing) and the launch's epilogue is applied to
+// them exactly as the GEMM applies it to its accumulators.  Partial column
+// order is the packed weight's: SWIGLU takes gate and up from packed columns
+// 64 k + e and 64 k + 32 + e for output column 32 k + e; SCALE's head-permuted
+// q/k columns go back to head order.
+template <int EPI>
+__global__ __launch_bounds__(256) void gemm_finalize_kernel(GemmParams p) {
+  constexpr bool kGlu = EPI == EPI_SWIGLU;
+  const int M = rows_from(p.m_ptr, p.m_ub);
+  const int groups = kGlu ? p.N / 16 : p.N / 8;          // 8-column output groups per row
+  const long long idx = (long long)blockIdx.x * 256 + threadIdx.x;
+  const int row = (int)(idx / groups);
+  if (row >= M) return;
+  const int g = (int)(idx - (long long)row * groups);
+  const int S = p.k_splits;
+  auto sum8 = [&](int col, float* v) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[e] = 0.0f;
+    for (int sp = 0; sp < S; ++sp) {
+      const float* src = p.partial + ((size_t)sp * (size_t)p.m_ub + (size_t)row) * (size_t)p.N + col;
+      const f32x4_t a = *reinterpret_cast<const f32x4_t*>(src);
+      const f32x4_t b = *reinterpret_cast<const f32x4_t*>(src + 4);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        v[e] += a[e];
+        v[4 + e] += b[e];
+      }
+    }
+  };
+  auto pack8_bf = [](const float* v) {
+    return u32x4_t{pack_bf2(v[0], v[1]), pack_bf2(v[2], v[3]), pack_bf2(v[4], v[5]), pack_bf2(v[6], v[7])};
+  };
+  auto add8_bf = [](float* v, u32x4_t r) {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      v[2 * e] += __uint_as_float(r[e] << 16);
+      v[2 * e + 1] += __uint_as_float(r[e] & 0xffff0000u);
+    }
+  };
+  float v[8];
+  if constexpr (kGlu) {
+    const int oc = 8 * g, kb = oc >> 5, e0 = oc & 31;
+    float u[8];
+    sum8(64 * kb + e0, v);
+    sum8(64 * kb + 32 + e0, u);
+    const float sc = p.rs[row];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[e] = silu(v[e] * sc) * (u[e] * sc);
+    *reinterpret_cast<u32x4_t*>(static_cast<uint16_t*>(p.C) + (size_t)row * p.ldc + oc) = pack8_bf(v);
+  } else {
+    const int pc = 8 * g;
+    sum8(pc, v);
+    if constexpr (EPI == EPI_SCALE) {
+      int oc = pc;
+      if (pc < p.perm_col1) {
+        const int hsel = (pc >> 6) & 1, j = (pc >> 5) & 1;
+        oc = (pc & ~127) + 32 * (hsel + 2 * j) + (pc & 31);
+      }
+      const float sc = p.rs[row];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[e] *= sc;
+      uint16_t* dst = static_cast<uint16_t*>(p.C) + (size_t)row * p.ldc + oc;
+      if (p.f16_col0 > 0 && oc >= p.f16_col0) {
+        float mx = 0.0f;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) mx = fmaxf(mx, fabsf(v[e]));
+        *reinterpret_cast<u32x4_t*>(dst) =
+            u32x4_t{pack_h2(v[0], v[1]), pack_h2(v[2], v[3]), pack_h2(v[4], v[5]), pack_h2(v[6], v[7])};
+        if (p.status && mx > 65504.0f) atomicOr(p.status, SEER_STATUS_V_RANGE);
+      } else {
+        *reinterpret_cast<u32x4_t*>(dst) = pack8_bf(v);
+      }
+    } else {
+      // residual adds: v + R (RESID_SPLIT: stored as the bf16 pair hi, lo) or
+      // v + R + R2 (RESID_PAIR)
+      add8_bf(v, *reinterpret_cast<const u32x4_t*>(static_cast<const uint16_t*>(p.R) + (size_t)row * p.ldr + pc));
+      if constexpr (EPI == EPI_RESID_PAIR)
+        add8_bf(v, *reinterpret_cast<const u32x4_t*>(static_cast<const uint16_t*>(p.R2) + (size_t)row * p.ldr + pc));
+      const u32x4_t hi = pack8_bf(v);
+      *reinterpret_cast<u32x4_t*>(static_cast<uint16_t*>(p.C) + (size_t)row * p.ldc + pc) = hi;
+      if constexpr (EPI == EPI_RESID_SPLIT) {
+        float lo[8];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          lo[2 * e] = v[2 * e] - __uint_as_float(hi[e] << 16);
+          lo[2 * e + 1] = v[2 * e + 1] - __uint_as_float(hi[e] & 0xffff0000u);
+        }
+        *reinterpret_cast<u32x4_t*>(static_cast<uint16_t*>(p.C2) + (size_t)row * p.ldc + pc) = pack8_bf(lo);
+      }
+    }
+  }
+}
+
+// K splits for a launch of `tiles` 256x256 tiles: the most splits (<= 16)
+// whose units fit one round on the n_units workgroups that run at once, with
+// an even number of 64-wide K tiles per split (the main loop's unroll) and
+// partials that fit the scratch -- used only when that is at least 3 and the
+// epilogue can be split.  Two splits gain nothing over the half-height tiles
+// of the unsplit launch and cost the finalize pass (measured: the prefix-
+// cached B=16 step 0.745 -> 0.763 ms); at 3 and more the launch takes a
+// fraction of one tile's time (the B=1 cached step 0.359 -> 0.198 ms).
+static int k_splits_for(int epi, const GemmParams& p, int tiles, int tiles_m) {
+  const bool splittable = epi == EPI_SCALE || epi == EPI_RESID_SPLIT || epi == EPI_RESID_PAIR || epi == EPI_SWIGLU;
+  if (!splittable || !p.partial || p.n_units <= 0 || tiles < 1) return 1;
+  const int KT = p.K / BK;
+  int S = p.n_units / tiles;
+  S = S < 16 ? S : 16;
+  while (S > 1 && (KT % (2 * S) != 0 || (size_t)S * (size_t)tiles_m * 256u * (size_t)p.N * 4u > p.partial_bytes)) --S;
+  return S >= 3 ? S : 1;
+}
+
+int launch_gemm_bf16(int epi, const GemmParams& p_in, hipStream_t s) {
+  GemmParams p = p_in;
   // the head permutation and the rotary pairs work on whole 128-wide heads of
   // the SCALE epilogues, and rotation needs the permuted layout
   const bool scale = epi == EPI_SCALE || epi == EPI_SCALE_ROPE;
@@ -577,9 +735,20 @@ int launch_gemm_bf16(int epi, const GemmParams& p, hipStream_t s) {
   if (p.rope_pos && (!p.rope_freq || p.rope_col1 % 128 != 0 || p.rope_col1 > p.perm_col1)) return -1;
   const int tiles_m = (p.m_ub + 255) / 256;
   const int tiles_n = p.N / 256;
-  // the split last round adds at most n_units / 2 units
-  dim3 grid(tiles_m * tiles_n + (p.n_units > 0 ? p.n_units / 2 : 0)), block(NT);
-  switch (epi) {
+  p.k_splits = k_splits_for(epi, p, tiles_m * tiles_n, tiles_m);
+  // the split last round adds at most n_units / 2 units; a K split has
+  // k_splits units per tile
+  dim3 grid(p.k_splits > 1 ? tiles_m * tiles_n * p.k_splits : tiles_m * tiles_n + (p.n_units > 0 ? p.n_units / 2 : 0)),
+      block(NT);
+  if (p.k_splits > 1) {
+    switch (epi) {
+      case EPI_SCALE: hipLaunchKernelGGL(gemm_bf16_split_kernel<EPI_SCALE>, grid, block, 0, s, p); break;
+      case EPI_RESID_SPLIT: hipLaunchKernelGGL(gemm_bf16_split_kernel<EPI_RESID_SPLIT>, grid, block, 0, s, p); break;
+      case EPI_RESID_PAIR: hipLaunchKernelGGL(gemm_bf16_split_kernel<EPI_RESID_PAIR>, grid, block, 0, s, p); break;
+      case EPI_SWIGLU: hipLaunchKernelGGL(gemm_bf16_split_kernel<EPI_SWIGLU>, grid, block, 0, s, p); break;
+      default: return -1;
+    }
+  } else switch (epi) {
     case EPI_SCALE: hipLaunchKernelGGL(gemm_bf16_kernel<EPI_SCALE>, grid, block, 0, s, p); break;
     case EPI_SCALE_ROPE: hipLaunchKernelGGL(gemm_bf16_kernel<EPI_SCALE_ROPE>, grid, block, 0, s, p); break;
     case EPI_RESID: hipLaunchKernelGGL(gemm_bf16_kernel<EPI_RESID>, grid, block, 0, s, p); break;
@@ -592,6 +761,17 @@ int launch_gemm_bf16(int epi, const GemmParams& p, hipStream_t s) {
       hipLaunchKernelGGL(gemm_bf16_kernel<EPI_RESID_PAIR>, grid, block, 0, s, p); break;
     case EPI_ARGMAX: hipLaunchKernelGGL(gemm_bf16_kernel<EPI_ARGMAX>, grid, block, 0, s, p); break;
     default: return -1;
+  }
+  if (p.k_splits > 1) {
+    const long long groups = (long long)p.m_ub * (epi == EPI_SWIGLU ? p.N / 16 : p.N / 8);
+    dim3 fgrid((unsigned)((groups + 255) / 256)), fblock(256);
+    switch (epi) {
+      case EPI_SCALE: hipLaunchKernelGGL(gemm_finalize_kernel<EPI_SCALE>, fgrid, fblock, 0, s, p); break;
+      case EPI_RESID_SPLIT: hipLaunchKernelGGL(gemm_finalize_kernel<EPI_RESID_SPLIT>, fgrid, fblock, 0, s, p); break;
+      case EPI_RESID_PAIR: hipLaunchKernelGGL(gemm_finalize_kernel<EPI_RESID_PAIR>, fgrid, fblock, 0, s, p); break;
+      case EPI_SWIGLU: hipLaunchKernelGGL(gemm_finalize_kernel<EPI_SWIGLU>, fgrid, fblock, 0, s, p); break;
+      default: return -1;
+    }
   }
   return hipGetLastError() == hipSuccess ? 0 : -1;
 }

@@ -68,6 +68,15 @@ struct GemmParams {
   // SEER_STATUS_V_RANGE (atomic OR) when a column stored as fp16 had a
   // magnitude above fp16's largest finite value
   int* status;
+  // bf16 SCALE, RESID_SPLIT, RESID_PAIR and SWIGLU, optional: scratch for
+  // fp32 partial tiles (partial_bytes bytes).  A launch whose 256x256 tiles
+  // fill at most a third of the n_units workgroups that run at once splits K
+  // over k_splits units per tile: each stores its fp32 partial sums, and a
+  // second kernel adds the splits in order and applies the epilogue.  The
+  // launcher sets k_splits; callers leave it 0.
+  float* partial;
+  size_t partial_bytes;
+  int k_splits;
 };
 
 // Weight layout of the bf16 GEMM's B operand ("fragment-major"): element

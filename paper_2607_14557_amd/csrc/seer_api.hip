@@ -66,8 +66,13 @@ int check_dims(const seer_dims* d) {
 }
 
 struct WsLayout {
-  size_t qkv, o, h1, act, inv1, inv2, h1lo, pos, freq, total;
+  size_t qkv, o, h1, act, inv1, inv2, h1lo, pos, freq, part, part_bytes, total;
 };
+
+// bf16 layers: fp32 partial tiles of the GEMMs that split K (launches whose
+// tiles fill at most half of the CUs; at most one 256x256 fp32 tile per
+// workgroup of one round, 256 CUs x 256 KiB).
+constexpr size_t PART_BYTES = (size_t)64 << 20;
 
 // The first 256 bytes of a layer workspace are a header whose first int32 is
 // the status word (same place for every rows bound, so it persists across
@@ -92,6 +97,9 @@ WsLayout ws_layout(const seer_dims* d, int rows) {
   // rotary embedding: per-row positions and the per-pair frequencies
   L.pos = off;  off = up256(off + R * 4);
   L.freq = off; off = up256(off + 64 * 8);
+  L.part = off;
+  L.part_bytes = d->dtype == SEER_DTYPE_BF16 ? PART_BYTES : 0;
+  off = up256(off + L.part_bytes);
   L.total = off;
   return L;
 }
@@ -201,6 +209,7 @@ static int layer_forward_impl(const seer_dims* dims, const void* w_packed, const
   const bool rope = dims->rope_theta > 0.0f;
   int* rpos = reinterpret_cast<int*>(ws + L.pos);
   double* rfreq = reinterpret_cast<double*>(ws + L.freq);
+  float* part = L.part_bytes ? reinterpret_cast<float*>(ws + L.part) : nullptr;
   int n_units = 0;                      // CUs: sizes the split of a partly filled last GEMM round
   if (bf16) {
     int dev = 0;
@@ -229,6 +238,7 @@ static int layer_forward_impl(const seer_dims* dims, const void* w_packed, const
   {
     seer::GemmParams g{};
     g.n_units = n_units;
+    g.partial = part; g.partial_bytes = L.part_bytes;
     g.A = x_in; g.B = wb + P.qkv * es; g.C = qkv; g.rs = inv1;
     g.m_ptr = m_ptr; g.m_ub = R; g.N = 3 * d; g.K = d;
     g.lda = d; g.ldb = d; g.ldc = 3 * d;
@@ -263,6 +273,7 @@ static int layer_forward_impl(const seer_dims* dims, const void* w_packed, const
   {
     seer::GemmParams g{};
     g.n_units = n_units;
+    g.partial = part; g.partial_bytes = L.part_bytes;
     g.A = o; g.B = wb + P.o * es; g.C = h1; g.R = x_in; g.C2 = h1lo;
     g.m_ptr = m_ptr; g.m_ub = R; g.N = d; g.K = d;
     g.lda = d; g.ldb = d; g.ldc = d; g.ldr = d;
@@ -277,6 +288,7 @@ static int layer_forward_impl(const seer_dims* dims, const void* w_packed, const
     if (act_count && seer::launch_zero_i32(act_count, R, stream)) return hip_fail("zero launch");
     seer::GemmParams g{};
     g.n_units = n_units;
+    g.partial = part; g.partial_bytes = L.part_bytes;
     g.A = h1; g.C = act; g.rs = inv2; g.cnt = act_count; g.eps = act_eps;
     g.m_ptr = m_ptr; g.m_ub = R; g.K = d; g.lda = d; g.ldb = d; g.ldc = I;
     if (bf16) {
@@ -296,6 +308,7 @@ static int layer_forward_impl(const seer_dims* dims, const void* w_packed, const
   {
     seer::GemmParams g{};
     g.n_units = n_units;
+    g.partial = part; g.partial_bytes = L.part_bytes;
     g.A = act; g.B = wb + P.dn * es; g.C = x_out; g.R = h1; g.R2 = h1lo;
     g.m_ptr = m_ptr; g.m_ub = R; g.N = d; g.K = I;
     g.lda = I; g.ldb = I; g.ldc = d; g.ldr = d;

@@ -260,12 +260,12 @@ def test_status_reset_argument_errors(S):
 def test_noalloc_refuses_rows_beyond_its_array(S):
     """The no-allocation layer call checks its rows bound against the 256 MiB
     in-library workspace before touching the device (the LLaDA-8B bf16 layer
-    fits 3640 rows)."""
+    fits 2730 rows)."""
     d = dims(S)
     L = S.load_library()
-    assert S.seer_layer_workspace_bytes(d, 3640) <= (256 << 20) < S.seer_layer_workspace_bytes(d, 3641)
-    rc = L.seer_layer_forward_varlen_noalloc(ctypes.byref(d), FAKE, FAKE, FAKE + 4096, 3641, FAKE, None, 1,
+    assert S.seer_layer_workspace_bytes(d, 2730) <= (256 << 20) < S.seer_layer_workspace_bytes(d, 2731)
+    rc = L.seer_layer_forward_varlen_noalloc(ctypes.byref(d), FAKE, FAKE, FAKE + 4096, 2731, FAKE, None, 1,
                                              0.0, None, None, 0)
-    assert rc == S.SEER_EWORKSPACE and "3641" in S.seer_last_error()
+    assert rc == S.SEER_EWORKSPACE and "2731" in S.seer_last_error()
     assert L.seer_layer_forward_varlen_noalloc(ctypes.byref(d), FAKE, FAKE, FAKE + 4096, 0, FAKE, None, 1,
                                                0.0, None, None, 0) == S.SEER_EINVAL

@@ -457,3 +457,25 @@ def test_v_fp16_range_status(S):
     assert status(L) == 0
     L.run(xd, dev(cu), len(lens))
     assert status(L) == 0
+
+
+def test_layer_many_rows_unsplit_k_tail(S):
+    """A bf16 layer with d_ff = 640 over 33280 rows (130 sequences of 256): every
+    projection has more 256x256 tiles than half the CUs, so none splits K, and
+    the down projection (K / 64 = 10) ends its four-stage ring on the two-tile
+    tail.  (Small layers like the other cases split K instead.)"""
+    d, H, dh, I = 256, 2, 128, 640
+    rng = np.random.default_rng(43)
+    W = _round(_rand_layer(rng, d, I, 0.02), "bf16")
+    lens = [256] * 130
+    cu = np.concatenate([[0], np.cumsum(lens)])
+    T = int(cu[-1])
+    xd = dev(rng.standard_normal((T, d)), "bf16")
+    x = host(xd)
+    log("layer bf16 %d rows (d %d, d_ff %d)" % (T, d, I))
+    L = _Layer(S, d, H, dh, I, "bf16", T, W)
+    y, _ = L.run(xd, dev(cu), len(lens))
+    y_ref, _ = layer_forward(x, cu, W, H, 1e-5)
+    e = rel_err(host(y), y_ref)
+    log("  y rel err %.3e" % e)
+    assert e <= BF16_TOL

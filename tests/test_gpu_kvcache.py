@@ -55,7 +55,9 @@ def _bits(t):
     return t.contiguous().view(torch.int16 if t.element_size() == 2 else torch.int32)
 
 
-@pytest.mark.parametrize("name", ["tiny_f32", "small_bf16_ragged", "small_bf16_stack", "llada_b16_ragged"])
+# llada_b1: about 100 window rows, so the cached step's QKV, O and down
+# projections split their K dimension (4 to 16 ways); llada_b16_ragged: unsplit
+@pytest.mark.parametrize("name", ["tiny_f32", "small_bf16_ragged", "small_bf16_stack", "llada_b1", "llada_b16_ragged"])
 def test_cached_truncated_step(S, name):
     import torch
     from paper_2607_14557_amd.runner import SeerStack, dims_for

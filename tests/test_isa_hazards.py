@@ -30,6 +30,7 @@ def _asm(tmp_path, name):
 @pytest.mark.skipif(not os.path.exists(HIPCC), reason="hipcc not available")
 @pytest.mark.parametrize("src,kernel,min_count,read_op", [
     ("gemm_bf16.hip", "gemm_bf16_kernel", 6, "ds_read_b128"),
+    ("gemm_bf16.hip", "gemm_bf16_split_kernel", 4, "ds_read_b128"),
     ("attn_bf16.hip", "attn_bf16_kernel", 1, "ds_read_b64_tr_b16"),
 ])
 def test_lds_reads_are_never_clobbered(tmp_path, src, kernel, min_count, read_op):

@@ -92,9 +92,9 @@ def test_noalloc_llada_shape_and_limit(S):
     lens[0] += 1592 - int(lens.sum())
     _compare(S, dims, packed, "bf16", lens, 1792, rng, eps)
     _compare(S, dims, packed, "bf16", [300, 100], 512, rng, eps)
-    assert S.seer_layer_workspace_bytes(dims, 3640) <= (256 << 20) < S.seer_layer_workspace_bytes(dims, 3641)
-    x = torch.zeros(3641, d, dtype=torch.bfloat16, device="cuda")
-    cu = dev(np.array([0, 3641]))
+    assert S.seer_layer_workspace_bytes(dims, 2730) <= (256 << 20) < S.seer_layer_workspace_bytes(dims, 2731)
+    x = torch.zeros(2731, d, dtype=torch.bfloat16, device="cuda")
+    cu = dev(np.array([0, 2731]))
     with pytest.raises(S.SeerError) as ei:
-        S.seer_layer_forward_varlen_noalloc(dims, packed, x, torch.empty_like(x), 3641, cu, None, 1, 0.0, None)
+        S.seer_layer_forward_varlen_noalloc(dims, packed, x, torch.empty_like(x), 2731, cu, None, 1, 0.0, None)
     assert ei.value.code == S.SEER_EWORKSPACE
