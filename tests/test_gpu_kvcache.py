@@ -28,9 +28,12 @@ pytestmark = pytest.mark.gpu
 TOL = {"bf16": 2e-2, "f32": 1e-4}
 # cached vs full step, both on the GPU.  The cached step places the window's
 # own keys after the prefix rounded up to a multiple of 4, so its key tiles
-# (and the softmax rescale points) differ from the full step's and bf16 results
-# differ by a few ulps; each side is also held to TOL against the oracle.
-SAME = {"bf16": 2e-2, "f32": 1e-5}
+# (and the softmax rescale points) differ from the full step's, and a few-row
+# step splits K in its projections: the fp32 values differ in rounding order
+# only, and the bf16 outputs by at most about two ulps (2^-8 relative each at
+# the bottom of a binade; measured 8.1e-3 at most over the five workloads).
+# Each side is also held to TOL against the oracle.
+SAME = {"bf16": 1e-2, "f32": 1e-5}
 
 
 @pytest.fixture(scope="module")

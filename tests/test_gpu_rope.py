@@ -140,7 +140,7 @@ def test_rope_cached_step(S):
         c = yc[cu_w_h[b]:cu_w_h[b] + keep[b]]
         worst = max(worst, rel_err(c, a))
     log("  cached vs full step, window rows: max rel diff %.3e" % worst)
-    assert worst <= TOL["bf16"]
+    assert worst <= 1e-2      # two GPU results, rounding order only (as the cached-step test's bar)
     # teacher-forced: layer 0 and the last layer of the first and last sequence
     for l in sorted({0, L - 1}):
         W = {k: np.asarray(v, np.float64) for k, v in layers[l].items()}
