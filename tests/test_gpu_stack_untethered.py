@@ -1,0 +1,78 @@
+"""Untethered detection on the two 32-layer stacks (LLaDA-8B layer shape, bf16):
+the oracle runs the step-0 detection pass itself -- layers 0..3 on the full
+window from the inputs, in fp64, with the near-zero count at the detection
+layer -- and the GPU does the same through the C ABI.  Both must find the
+planted boundaries; the difference of the two sparsity fractions on every
+window row is reported (not gated: four layers of bf16 rounding move a few
+activations across eps, see the count checks of test_gpu_stack.py for the
+teacher-forced gate).  The oracle pass takes one to two minutes on the host.
+"""
+import numpy as np
+import pytest
+
+from gpu_util import dev, host, log
+from oracle.detect import detect_batch
+from oracle.layer import layer_forward
+from oracle.sparsity import sparsity_fraction
+from workloads import WORKLOADS
+from workloads.generate import layer_weights_torch, make_stack_batch
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def S():
+    from paper_2607_14557_amd import seer
+    seer.load_library()
+    return seer
+
+
+@pytest.mark.timeout(420)
+@pytest.mark.parametrize("name", ["llada32_multicrop_b8", "llada32_video_b4"])
+def test_stack_detection_pass_untethered(S, name):
+    import torch
+    from paper_2607_14557_amd.runner import SeerStack, dims_for
+    w = WORKLOADS[name]
+    sh = w.shape
+    d, I, B, P = sh.d_model, sh.d_ff, w.batch, w.prefix_len
+    T = w.rows_full
+    L = w.l_det + 1
+    log("untethered %s: inputs, layers 0..%d" % (name, w.l_det))
+    batch = make_stack_batch(w, "cuda")
+    st = SeerStack(dims_for(d, sh.n_heads, sh.head_dim, I, "bf16", w.rms_eps), L, T)
+    for l in range(L):
+        st.set_layer(l, layer_weights_torch(w, l, "cuda"))
+    x = dev(batch.x, "bf16")
+    cu = dev(batch.cu_seqlens)
+    cnt = torch.empty(T, dtype=torch.int32, device="cuda")
+    cur = x
+    for l in range(L):
+        nxt = torch.empty_like(x)
+        st.layer(l, cur, nxt, cu, None, B, T, act_eps=w.act_eps, act_count=cnt if l == w.l_det else None)
+        cur = nxt
+    torch.cuda.synchronize()
+    cnt_gpu = host(cnt)
+    del st, cur, nxt
+    torch.cuda.empty_cache()
+    h = host(x)
+    c_ref = None
+    for l in range(L):
+        W = {k: host(v) for k, v in layer_weights_torch(w, l, "cuda").items()}
+        h, c = layer_forward(h, batch.cu_seqlens, W, sh.n_heads, w.rms_eps,
+                             act_eps=w.act_eps if l == w.l_det else None)
+        if l == w.l_det:
+            c_ref = c
+        del W
+        log("  oracle layer %d done" % l)
+    b_ref, _ = detect_batch(c_ref, batch.cu_seqlens, batch.win_off, batch.win_len, I)
+    b_gpu, _ = detect_batch(cnt_gpu, batch.cu_seqlens, batch.win_off, batch.win_len, I)
+    np.testing.assert_array_equal(b_ref, batch.planted)
+    np.testing.assert_array_equal(b_gpu, batch.planted)
+    worst = 0.0
+    for b in range(B):
+        r0 = int(batch.cu_seqlens[b]) + P
+        sl = slice(r0, r0 + w.window)
+        df = np.abs(sparsity_fraction(cnt_gpu[sl], I) - sparsity_fraction(c_ref[sl], I))
+        worst = max(worst, float(df.max()))
+        log("  seq %d: boundary %d, untethered window fraction diff max %.2e" % (b, int(b_ref[b]), df.max()))
+    log("  %s untethered sparsity fraction diff max %.2e over %d window rows (reported)" % (name, worst, B * w.window))
