@@ -15,6 +15,8 @@
  *                              packed variable-length sequences, with the
  *                              optional fused near-zero activation count
  *   seer_step0_detect          the SNR boundary criterion per sequence
+ *   seer_layer_forward_detect  the detection layer: count, criterion, and a
+ *                              down projection truncated to the kept rows
  *   seer_batch_repack          padding-waste-aware routing plus compaction
  *   seer_kv_export,            truncated steps on the window rows with the
  *   seer_layer_forward_cached  prefix keys/values cached (Appendix D)
@@ -301,6 +303,45 @@ int seer_step0_detect(const int32_t* act_count, const int32_t* cu_seqlens,
                       int32_t d_ff, const seer_snr_params* params,
                       int32_t* boundary, int32_t* keep_len, hipStream_t stream);
 
+/* The detection layer of step 0 (Sec. 3.2-3.5): seer_layer_forward_varlen
+ * with the near-zero count (act_count required, seqused none), the SNR scan
+ * of seer_step0_detect on those counts once the gate/up projection has
+ * written them, and then the down projection + residual only where its rows
+ * are kept.  The boundary is known before the layer's last GEMM, and the rows
+ * past it are dropped by the compaction that follows, so that GEMM is
+ * truncated already: with bf16 it computes the 256-row tiles of x_out that
+ * hold a kept row, rows [cu_seqlens[b], cu_seqlens[b] + win_off[b] +
+ * keep_len[b]) of sequence b, and leaves the rows of the other tiles
+ * unwritten; fp32 computes every row.
+ * Arguments: those of seer_layer_forward_varlen (seqused absent) and of
+ * seer_step0_detect (d_ff = dims->d_ff).  Outputs: act_count, boundary and
+ * keep_len; x_out on every kept row.  These equal, bit for bit, what
+ * seer_layer_forward_varlen followed by seer_step0_detect gives with the same
+ * total_rows_ub; x_out rows past a sequence's kept rows are unspecified.
+ * The workspace holds the list of kept tiles (seer_layer_workspace_bytes
+ * counts it).  Errors: those of the two calls. */
+int seer_layer_forward_detect(const seer_dims* dims, const void* w_packed, const void* x_in,
+                              void* x_out, int32_t total_rows_ub, const int32_t* cu_seqlens,
+                              int32_t batch, float act_eps, int32_t* act_count,
+                              const int32_t* win_off, const int32_t* win_len,
+                              const seer_snr_params* params, int32_t* boundary,
+                              int32_t* keep_len, void* workspace, size_t workspace_bytes,
+                              hipStream_t stream);
+
+/* As seer_layer_forward_detect, recording events[k] (created by the caller)
+ * on `stream` for live per-kernel timing: events[0] .. [6] as in
+ * seer_layer_forward_varlen_timed, then
+ *   events[6] -> [7] SNR scan + list of kept row tiles
+ *   events[7] -> [8] down GEMM + residual (kept tiles)
+ * Errors: as seer_layer_forward_detect, EINVAL if events or an entry is NULL. */
+int seer_layer_forward_detect_timed(const seer_dims* dims, const void* w_packed, const void* x_in,
+                                    void* x_out, int32_t total_rows_ub, const int32_t* cu_seqlens,
+                                    int32_t batch, float act_eps, int32_t* act_count,
+                                    const int32_t* win_off, const int32_t* win_len,
+                                    const seer_snr_params* params, int32_t* boundary,
+                                    int32_t* keep_len, void* workspace, size_t workspace_bytes,
+                                    hipStream_t stream, hipEvent_t events[9]);
+
 /* Routing policies (Sec. 3.4 and the system study of Sec. 4):
  * HYBRID = three-tier Static / Varlen / Eager routing by padding waste ratio;
  * NAIVE_PAD = every sequence padded to the bucket of the batch-max length;
@@ -451,7 +492,7 @@ int seer_graph_destroy(seer_graph_t graph);
 const char* seer_last_error(void);
 
 /* ABI version of this library (major * 100 + minor). */
-int32_t seer_abi_version(void);   /* 103: workspace header with the status word */
+int32_t seer_abi_version(void);   /* 104: the detection layer (seer_layer_forward_detect) */
 
 #ifdef __cplusplus
 }

@@ -554,8 +554,9 @@ __device__ __forceinline__ void gemm_tile(const GemmParams& p, uint8_t* st0, uin
 // round of r < n_units/2 tiles on the n_units workgroups that run at once,
 // each of those r tiles becomes two 128x256 halves (disjoint outputs, no
 // reduction), so the last round keeps twice as many CUs busy.  Tile geometry
-// follows the real row count read on the device; surplus blocks of the
-// upper-bound grid, and halves that start past the last row, exit at once.
+// follows the real row count read on the device (or the row-tile list of
+// p.mtiles); surplus blocks of the upper-bound grid, and halves that start
+// past the last row, exit at once.
 template <int EPI>
 __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmParams p) {
   // the four stages of the A ring, each its own array: the compiler then
@@ -565,7 +566,7 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmParams p) {
   __shared__ __attribute__((aligned(1024))) uint8_t st2[256 * ROW_BYTES];
   __shared__ __attribute__((aligned(1024))) uint8_t st3[256 * ROW_BYTES];
   const int M = rows_from(p.m_ptr, p.m_ub);
-  const int tiles_m = (M + 255) / 256;
+  const int tiles_m = p.mtiles ? p.mtiles[0] : (M + 255) / 256;
   const int tiles_n = p.N / 256;
   const int ntiles = tiles_m * tiles_n;
   int full = ntiles;
@@ -579,10 +580,12 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmParams p) {
   if (u >= full + 2 * (ntiles - full)) return;
   if (u < full) {
     raster(xcd_remap(u, full), tiles_m, tiles_n, tm, tn);
+    if (p.mtiles) tm = p.mtiles[1 + tm];
     gemm_tile<EPI, 256>(p, st0, st1, st2, st3, M, tm * 256, tn * 256, 0, KT);
   } else {
     const int v = u - full;
     raster(full + (v >> 1), tiles_m, tiles_n, tm, tn);
+    if (p.mtiles) tm = p.mtiles[1 + tm];
     const int m0 = tm * 256 + (v & 1) * 128;
     if (m0 >= M) return;
     gemm_tile<EPI, 128>(p, st0, st1, st2, st3, M, m0, tn * 256, 0, KT);
@@ -600,7 +603,7 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_split_kernel(GemmParams p) {
   __shared__ __attribute__((aligned(1024))) uint8_t st2[256 * ROW_BYTES];
   __shared__ __attribute__((aligned(1024))) uint8_t st3[256 * ROW_BYTES];
   const int M = rows_from(p.m_ptr, p.m_ub);
-  const int tiles_m = (M + 255) / 256;
+  const int tiles_m = p.mtiles ? p.mtiles[0] : (M + 255) / 256;
   const int tiles_n = p.N / 256;
   const int S = p.k_splits;
   const int u = blockIdx.x;
@@ -609,6 +612,7 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_split_kernel(GemmParams p) {
   const int kts = p.K / BK / S;
   int tm, tn;
   raster(tile, tiles_m, tiles_n, tm, tn);
+  if (p.mtiles) tm = p.mtiles[1 + tm];
   gemm_tile<EPI, 256, true>(p, st0, st1, st2, st3, M, tm * 256, tn * 256, sp * kts, kts, sp);
 }
 
@@ -618,16 +622,22 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_split_kernel(GemmParams p) {
 // them exactly as the GEMM applies it to its accumulators.  Partial column
 // order is the packed weight's: SWIGLU takes gate and up from packed columns
 // 64 k + e and 64 k + 32 + e for output column 32 k + e; SCALE's head-permuted
-// q/k columns go back to head order.
+// q/k columns go back to head order.  With a row-tile list, thread rows run
+// over the listed tiles only.
 template <int EPI>
 __global__ __launch_bounds__(256) void gemm_finalize_kernel(GemmParams p) {
   constexpr bool kGlu = EPI == EPI_SWIGLU;
   const int M = rows_from(p.m_ptr, p.m_ub);
   const int groups = kGlu ? p.N / 16 : p.N / 8;          // 8-column output groups per row
   const long long idx = (long long)blockIdx.x * 256 + threadIdx.x;
-  const int row = (int)(idx / groups);
+  const int vrow = (int)(idx / groups);
+  const int g = (int)(idx - (long long)vrow * groups);
+  int row = vrow;
+  if (p.mtiles) {
+    if ((vrow >> 8) >= p.mtiles[0]) return;
+    row = p.mtiles[1 + (vrow >> 8)] * 256 + (vrow & 255);
+  }
   if (row >= M) return;
-  const int g = (int)(idx - (long long)row * groups);
   const int S = p.k_splits;
   auto sum8 = [&](int col, float* v) {
 #pragma unroll

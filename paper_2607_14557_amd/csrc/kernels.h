@@ -77,6 +77,12 @@ struct GemmParams {
   float* partial;
   size_t partial_bytes;
   int k_splits;
+  // bf16, optional: the 256-row tiles to compute.  mtiles[0] = their number,
+  // mtiles[1 ..] = their indices t (rows 256 t .. 256 t + 255) in increasing
+  // order, written on the device (launch_kept_tiles); the launch covers them
+  // as if they were consecutive and leaves the other rows of C untouched.
+  // Null: every row.
+  const int* mtiles;
 };
 
 // Weight layout of the bf16 GEMM's B operand ("fragment-major"): element
@@ -165,6 +171,23 @@ struct DetectParams {
   int* keep_len;
 };
 int launch_detect(const DetectParams& p, hipStream_t s);
+
+// The 256-row tiles of a packed batch that hold rows the compaction keeps:
+// row r of sequence b is kept when r - cu[b] < win_off[b] + keep_len[b]
+// (keep_len clamped to [0, win_len[b]], the sum to the sequence's length).
+// map[0] = the number of such tiles t < ceil(min(cu[B], rows_ub) / 256),
+// map[1 ..] = the tiles in increasing order (the mtiles of GemmParams); map
+// holds 1 + ceil(rows_ub / 256) entries.  One workgroup.
+struct KeptTilesParams {
+  const int* cu;
+  const int* win_off;
+  const int* win_len;
+  const int* keep_len;
+  int B;
+  int rows_ub;
+  int* map;
+};
+int launch_kept_tiles(const KeptTilesParams& p, hipStream_t s);
 
 constexpr int kRepackMaxBatch = 1024;
 constexpr int kRepackMaxBuffers = 4;

@@ -138,6 +138,64 @@ int launch_detect(const DetectParams& p, hipStream_t s) {
 }
 
 // ---------------------------------------------------------------------------
+// Kept row tiles after the scan (the rows the compaction copies), so that the
+// detection layer's down projection computes only those.  Thread t of each
+// 1024-tile chunk finds the first sequence reaching into tile t by bisection
+// of cu and walks the sequences that start inside it; the live tiles are
+// then listed in order (wave ballots, per-wave counts in LDS).
+__global__ __launch_bounds__(1024) void kept_tiles_kernel(KeptTilesParams p) {
+  __shared__ int s_wave[16];
+  __shared__ int s_base;
+  const int M = rows_from(p.cu + p.B, p.rows_ub);
+  const int tiles = (M + 255) / 256;
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  if (threadIdx.x == 0) s_base = 0;
+  __syncthreads();
+  for (int t0 = 0; t0 < tiles; t0 += 1024) {
+    const int t = t0 + (int)threadIdx.x;
+    bool live = false;
+    if (t < tiles) {
+      const int r0 = 256 * t, r1 = min(r0 + 256, M);
+      int lo = 0, hi = p.B - 1;               // last b with cu[b] <= r0
+      while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (p.cu[mid] <= r0) lo = mid; else hi = mid - 1;
+      }
+      for (int b = lo; b < p.B && !live; ++b) {
+        const int s0 = p.cu[b];
+        if (s0 >= r1) break;
+        const int len = p.cu[b + 1] - s0;
+        int keep = p.keep_len[b];
+        keep = keep < 0 ? 0 : (keep > p.win_len[b] ? p.win_len[b] : keep);
+        int used = p.win_off[b] + keep;
+        used = used < 0 ? 0 : (used > len ? len : used);
+        live = max(s0, r0) < min(s0 + used, r1);
+      }
+    }
+    const unsigned long long bal = __ballot(live);
+    const int below = __popcll(bal & ((1ull << lane) - 1ull));
+    if (lane == 0) s_wave[wv] = __popcll(bal);
+    __syncthreads();
+    int off = s_base;
+    for (int k = 0; k < wv; ++k) off += s_wave[k];
+    if (live) p.map[1 + off + below] = t;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      int n = 0;
+      for (int k = 0; k < 16; ++k) n += s_wave[k];
+      s_base += n;
+    }
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) p.map[0] = s_base;
+}
+
+int launch_kept_tiles(const KeptTilesParams& p, hipStream_t s) {
+  hipLaunchKernelGGL(kept_tiles_kernel, dim3(1), dim3(1024), 0, s, p);
+  return hipGetLastError() == hipSuccess ? 0 : -1;
+}
+
+// ---------------------------------------------------------------------------
 // Routing + compaction (Sec. 3.4-3.5).  Every workgroup rebuilds the routing
 // plan of the (small) batch in LDS -- classes, buckets, padding waste, paths,
 // allocations and the exclusive prefix sum of the packed lengths -- so a

@@ -66,7 +66,7 @@ int check_dims(const seer_dims* d) {
 }
 
 struct WsLayout {
-  size_t qkv, o, h1, act, inv1, inv2, h1lo, pos, freq, part, part_bytes, total;
+  size_t qkv, o, h1, act, inv1, inv2, h1lo, pos, freq, tmap, part, part_bytes, total;
 };
 
 // bf16 layers: fp32 partial tiles of the GEMMs that split K (launches whose
@@ -97,6 +97,8 @@ WsLayout ws_layout(const seer_dims* d, int rows) {
   // rotary embedding: per-row positions and the per-pair frequencies
   L.pos = off;  off = up256(off + R * 4);
   L.freq = off; off = up256(off + 64 * 8);
+  // the detection layer's list of kept 256-row tiles
+  L.tmap = off; off = up256(off + (1 + (R + 255) / 256) * 4);
   L.part = off;
   L.part_bytes = d->dtype == SEER_DTYPE_BF16 ? PART_BYTES : 0;
   off = up256(off + L.part_bytes);
@@ -110,7 +112,7 @@ extern "C" {
 
 const char* seer_last_error(void) { return g_err.c_str(); }
 
-int32_t seer_abi_version(void) { return 103; }
+int32_t seer_abi_version(void) { return 104; }
 
 size_t seer_prepacked_bytes(const seer_dims* dims) {
   if (check_dims(dims) != SEER_OK) return 0;
@@ -166,13 +168,30 @@ int seer_layer_workspace_offsets(const seer_dims* dims, int32_t max_rows, size_t
   return ok();
 }
 
+static int check_snr(const seer_snr_params* params) {
+  if (params->tau_den < 1 || params->gamma_den < 1 || params->tau_num < 0 || params->gamma_num < 0)
+    return fail(SEER_EINVAL, "tau/gamma must be non-negative rationals with positive denominators");
+  if (params->lookahead < 1) return fail(SEER_EINVAL, "lookahead must be >= 1");
+  return SEER_OK;
+}
+
+// The SNR scan run inside the detection layer, between the count and the
+// down projection.
+struct DetectStep {
+  const int32_t* win_off;
+  const int32_t* win_len;
+  const seer_snr_params* snr;
+  int32_t* boundary;
+  int32_t* keep_len;
+};
+
 static int layer_forward_impl(const seer_dims* dims, const void* w_packed, const void* x_in,
                               void* x_out, int32_t total_rows_ub, const int32_t* cu_seqlens,
                               const int32_t* seqused, int32_t batch, float act_eps,
                               int32_t* act_count, void* workspace, size_t workspace_bytes,
                               hipStream_t stream, hipEvent_t* ev, const void* kv_cache = nullptr,
                               const int32_t* cu_kv = nullptr, bool own_status = false,
-                              int32_t* status = nullptr) {
+                              int32_t* status = nullptr, const DetectStep* det = nullptr) {
   int rc = check_dims(dims);
   if (rc) return rc;
   if (!w_packed || !x_in || !x_out || !cu_seqlens || !workspace)
@@ -303,8 +322,30 @@ static int layer_forward_impl(const seer_dims* dims, const void* w_packed, const
     if (gemm(act_count ? seer::EPI_SWIGLU_COUNT : seer::EPI_SWIGLU, g, stream))
       return hip_fail("gate/up gemm launch");
   }
+  // 6b. (detection layer) the SNR scan on the counts, and the row tiles that
+  // hold kept rows: the down projection computes only those
+  int* tmap = nullptr;
+  if (det) {
+    if (mark(6) != hipSuccess) return hip_fail("event record");
+    seer::DetectParams dp{};
+    dp.cnt = act_count; dp.cu = cu_seqlens; dp.win_off = det->win_off; dp.win_len = det->win_len;
+    dp.B = batch; dp.d_ff = I;
+    dp.tau_num = det->snr->tau_num; dp.tau_den = det->snr->tau_den;
+    dp.gamma_num = det->snr->gamma_num; dp.gamma_den = det->snr->gamma_den;
+    dp.lookahead = det->snr->lookahead;
+    dp.boundary = det->boundary; dp.keep_len = det->keep_len;
+    if (seer::launch_detect(dp, stream)) return hip_fail("detect launch");
+    if (bf16) {
+      tmap = reinterpret_cast<int*>(ws + L.tmap);
+      seer::KeptTilesParams kp{};
+      kp.cu = cu_seqlens; kp.win_off = det->win_off; kp.win_len = det->win_len; kp.keep_len = det->keep_len;
+      kp.B = batch; kp.rows_ub = R; kp.map = tmap;
+      if (seer::launch_kept_tiles(kp, stream)) return hip_fail("kept tiles launch");
+    }
+  }
+  const int e_down = det ? 7 : 6;
   // 7. down projection + residual
-  if (mark(6) != hipSuccess) return hip_fail("event record");
+  if (mark(e_down) != hipSuccess) return hip_fail("event record");
   {
     seer::GemmParams g{};
     g.n_units = n_units;
@@ -312,10 +353,50 @@ static int layer_forward_impl(const seer_dims* dims, const void* w_packed, const
     g.A = act; g.B = wb + P.dn * es; g.C = x_out; g.R = h1; g.R2 = h1lo;
     g.m_ptr = m_ptr; g.m_ub = R; g.N = d; g.K = I;
     g.lda = I; g.ldb = I; g.ldc = d; g.ldr = d;
+    g.mtiles = tmap;
     if (gemm(bf16 ? seer::EPI_RESID_PAIR : seer::EPI_RESID, g, stream)) return hip_fail("down gemm launch");
   }
-  if (mark(7) != hipSuccess) return hip_fail("event record");
+  if (mark(e_down + 1) != hipSuccess) return hip_fail("event record");
   return ok();
+}
+
+static int layer_detect_impl(const seer_dims* dims, const void* w_packed, const void* x_in, void* x_out,
+                             int32_t total_rows_ub, const int32_t* cu_seqlens, int32_t batch, float act_eps,
+                             int32_t* act_count, const int32_t* win_off, const int32_t* win_len,
+                             const seer_snr_params* params, int32_t* boundary, int32_t* keep_len,
+                             void* workspace, size_t workspace_bytes, hipStream_t stream, hipEvent_t* ev) {
+  if (!act_count || !win_off || !win_len || !params || !boundary || !keep_len)
+    return fail(SEER_EINVAL, "a required pointer is NULL");
+  int rc = check_snr(params);
+  if (rc) return rc;
+  const DetectStep det{win_off, win_len, params, boundary, keep_len};
+  return layer_forward_impl(dims, w_packed, x_in, x_out, total_rows_ub, cu_seqlens, nullptr, batch, act_eps,
+                            act_count, workspace, workspace_bytes, stream, ev, nullptr, nullptr, false, nullptr,
+                            &det);
+}
+
+int seer_layer_forward_detect(const seer_dims* dims, const void* w_packed, const void* x_in, void* x_out,
+                              int32_t total_rows_ub, const int32_t* cu_seqlens, int32_t batch, float act_eps,
+                              int32_t* act_count, const int32_t* win_off, const int32_t* win_len,
+                              const seer_snr_params* params, int32_t* boundary, int32_t* keep_len,
+                              void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  return layer_detect_impl(dims, w_packed, x_in, x_out, total_rows_ub, cu_seqlens, batch, act_eps, act_count,
+                           win_off, win_len, params, boundary, keep_len, workspace, workspace_bytes, stream,
+                           nullptr);
+}
+
+int seer_layer_forward_detect_timed(const seer_dims* dims, const void* w_packed, const void* x_in, void* x_out,
+                                    int32_t total_rows_ub, const int32_t* cu_seqlens, int32_t batch,
+                                    float act_eps, int32_t* act_count, const int32_t* win_off,
+                                    const int32_t* win_len, const seer_snr_params* params, int32_t* boundary,
+                                    int32_t* keep_len, void* workspace, size_t workspace_bytes,
+                                    hipStream_t stream, hipEvent_t* events) {
+  if (!events) return fail(SEER_EINVAL, "events is NULL");
+  for (int k = 0; k < 9; ++k)
+    if (!events[k]) return fail(SEER_EINVAL, "events[%d] is NULL", k);
+  return layer_detect_impl(dims, w_packed, x_in, x_out, total_rows_ub, cu_seqlens, batch, act_eps, act_count,
+                           win_off, win_len, params, boundary, keep_len, workspace, workspace_bytes, stream,
+                           events);
 }
 
 int seer_layer_forward_varlen(const seer_dims* dims, const void* w_packed, const void* x_in,
@@ -438,9 +519,8 @@ int seer_step0_detect(const int32_t* act_count, const int32_t* cu_seqlens, const
     return fail(SEER_EINVAL, "a required pointer is NULL");
   if (batch < 1) return fail(SEER_EINVAL, "batch must be >= 1 (got %d)", batch);
   if (d_ff < 1) return fail(SEER_EINVAL, "d_ff must be >= 1");
-  if (params->tau_den < 1 || params->gamma_den < 1 || params->tau_num < 0 || params->gamma_num < 0)
-    return fail(SEER_EINVAL, "tau/gamma must be non-negative rationals with positive denominators");
-  if (params->lookahead < 1) return fail(SEER_EINVAL, "lookahead must be >= 1");
+  int rc = check_snr(params);
+  if (rc) return rc;
   seer::DetectParams p{};
   p.cnt = act_count; p.cu = cu_seqlens; p.win_off = win_off; p.win_len = win_len;
   p.B = batch; p.d_ff = d_ff;

@@ -327,9 +327,10 @@ class SeerStack:
               snr=(3, 100, 3, 5, 3), policy=S.SEER_ROUTE_HYBRID, tau_pad=(1, 5), granule=256,
               trunc_capacity=None, ctrl_host=None, check_status=True, stream=None):
         """Step 0 (Sec. 3.2-3.5): layers 0..l_det on the full window with the
-        near-zero count at l_det, the SNR scan, routing + compaction of the
-        step-input embeddings and the in-flight residual, then the remaining
-        layers on the compacted batch.
+        near-zero count at l_det and the SNR scan inside that layer (whose
+        down projection then runs on the kept rows only), routing +
+        compaction of the step-input embeddings and the in-flight residual,
+        then the remaining layers on the compacted batch.
 
         trunc_capacity: rows of the compacted buffers.  By default the worst
         case of the routing: every window padded to the longest one,
@@ -349,10 +350,9 @@ class SeerStack:
             trunc_capacity = max(granule, -(-worst // granule) * granule)
         counts = torch.empty(rows_full, dtype=torch.int32, device=dev)
         cur = x_full
-        for l in range(l_det + 1):
+        for l in range(l_det):
             nxt = self.buf[l % 2]
-            self.layer(l, cur, nxt, cu_full, None, batch, rows_full,
-                       act_eps=act_eps, act_count=counts if l == l_det else None, stream=stream)
+            self.layer(l, cur, nxt, cu_full, None, batch, rows_full, stream=stream)
             cur = nxt
         cap = trunc_capacity
         key = (cap, batch)
@@ -372,8 +372,12 @@ class SeerStack:
         tb = self._trunc_bufs[key]
         boundary, keep, x_t, h_t = tb["boundary"], tb["keep"], tb["x_t"], tb["h_t"]
         cu_t, used, route, ctrl = tb["cu_t"], tb["used"], tb["route"], tb["ctrl"]
-        S.seer_step0_detect(counts, cu_full, win_off, win_len, batch, self.dims.d_ff,
-                            S.seer_snr_params(*snr), boundary, keep, stream=stream)
+        # the detection layer: count, scan, and its down projection on the kept rows only
+        nxt = self.buf[l_det % 2]
+        S.seer_layer_forward_detect(self.dims, self.packed[l_det], cur, nxt, rows_full, cu_full, batch, act_eps,
+                                    counts, win_off, win_len, S.seer_snr_params(*snr), boundary, keep,
+                                    self.workspace, self.ws_bytes, stream=stream)
+        cur = nxt
         desc = S.seer_repack_desc(policy, tau_pad[0], tau_pad[1], granule,
                                   self.dims.d_model * (2 if self.dtype == torch.bfloat16 else 4),
                                   cap, 0, 0)

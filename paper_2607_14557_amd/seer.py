@@ -22,7 +22,8 @@ SEER_STATUS_V_RANGE = 1
 EXPORTED = ("seer_prepacked_bytes", "seer_prepack_weights", "seer_layer_workspace_bytes",
             "seer_layer_status_reset", "seer_layer_workspace_offsets", "seer_layer_forward_varlen",
             "seer_layer_forward_varlen_noalloc",
-            "seer_layer_forward_varlen_timed", "seer_step0_detect", "seer_batch_repack",
+            "seer_layer_forward_varlen_timed", "seer_step0_detect", "seer_layer_forward_detect",
+            "seer_layer_forward_detect_timed", "seer_batch_repack",
             "seer_layer_forward_cached", "seer_kv_export", "seer_graph_begin", "seer_graph_end",
             "seer_graph_launch", "seer_graph_destroy", "seer_lm_head_workspace_bytes", "seer_lm_head_prepack",
             "seer_lm_head_predict", "seer_remask_step", "seer_last_error", "seer_abi_version")
@@ -105,6 +106,12 @@ def load_library():
     L.seer_layer_forward_varlen_timed.restype = ctypes.c_int
     L.seer_step0_detect.argtypes = [_P, _P, _P, _P, _I, _I, ctypes.POINTER(seer_snr_params), _P, _P, _P]
     L.seer_step0_detect.restype = ctypes.c_int
+    L.seer_layer_forward_detect.argtypes = [ctypes.POINTER(seer_dims), _P, _P, _P, _I, _P, _I, ctypes.c_float,
+                                            _P, _P, _P, ctypes.POINTER(seer_snr_params), _P, _P, _P,
+                                            ctypes.c_size_t, _P]
+    L.seer_layer_forward_detect.restype = ctypes.c_int
+    L.seer_layer_forward_detect_timed.argtypes = L.seer_layer_forward_detect.argtypes + [ctypes.POINTER(_P)]
+    L.seer_layer_forward_detect_timed.restype = ctypes.c_int
     L.seer_batch_repack.argtypes = [ctypes.POINTER(seer_repack_desc), ctypes.POINTER(_P),
                                     ctypes.POINTER(_P), _I, _P, _P, _P, _P, _I, _P, _P, _P, _P, _P, _P]
     L.seer_batch_repack.restype = ctypes.c_int
@@ -248,6 +255,22 @@ def seer_step0_detect(act_count, cu_seqlens, win_off, win_len, batch, d_ff, para
     _check(load_library().seer_step0_detect(
         _ptr(act_count), _ptr(cu_seqlens), _ptr(win_off), _ptr(win_len), int(batch), int(d_ff),
         ctypes.byref(params), _ptr(boundary), _ptr(keep_len), _stream(stream)))
+
+
+def seer_layer_forward_detect(dims, w_packed, x_in, x_out, total_rows_ub, cu_seqlens, batch, act_eps,
+                              act_count, win_off, win_len, params, boundary, keep_len, workspace,
+                              workspace_bytes=None, stream=None, events=None):
+    """The detection layer; with events (9 raw hipEvent_t handles) the timed
+    variant."""
+    nbytes = workspace_bytes if workspace_bytes is not None else workspace.numel() * workspace.element_size()
+    args = [ctypes.byref(dims), _ptr(w_packed), _ptr(x_in), _ptr(x_out), int(total_rows_ub), _ptr(cu_seqlens),
+            int(batch), float(act_eps), _ptr(act_count), _ptr(win_off), _ptr(win_len), ctypes.byref(params),
+            _ptr(boundary), _ptr(keep_len), _ptr(workspace), nbytes, _stream(stream)]
+    L = load_library()
+    if events is None:
+        _check(L.seer_layer_forward_detect(*args))
+    else:
+        _check(L.seer_layer_forward_detect_timed(*args, (_P * 9)(*events)))
 
 
 def seer_batch_repack(desc, srcs, dsts, cu_src, win_off, win_len, keep_len, batch, cu_dst,

@@ -34,7 +34,7 @@ def test_every_declared_symbol_is_exported(S):
     for n in names:
         assert hasattr(lib, n), n
     assert set(names) == set(S.EXPORTED)
-    assert S.seer_abi_version() == 103
+    assert S.seer_abi_version() == 104
 
 
 def dims(S, d=4096, h=32, dh=128, i=12288, dtype=1):
@@ -122,6 +122,33 @@ def test_detect_argument_errors(S):
     assert call(p=S.seer_snr_params(3, 0, 3, 5, 3)) == S.SEER_EINVAL
     assert call(p=S.seer_snr_params(-1, 100, 3, 5, 3)) == S.SEER_EINVAL
     assert call(p=S.seer_snr_params(3, 100, 3, 5, 0)) == S.SEER_EINVAL
+
+
+def test_detection_layer_argument_errors(S):
+    L = S.load_library()
+    d = dims(S)
+    good = S.seer_snr_params(3, 100, 3, 5, 3)
+
+    def call(cnt=FAKE, off=FAKE, wl=FAKE, p=good, bnd=FAKE, keep=FAKE, ws_bytes=1 << 40, batch=1, eps=0.01,
+             events=None):
+        args = (ctypes.byref(d), FAKE, FAKE, FAKE + 4096, 100, FAKE, batch, eps, cnt, off, wl, ctypes.byref(p),
+                bnd, keep, FAKE, ws_bytes, 0)
+        if events is None:
+            return L.seer_layer_forward_detect(*args)
+        return L.seer_layer_forward_detect_timed(*args, events)
+
+    assert call(cnt=None) == S.SEER_EINVAL                       # the count is required
+    assert call(off=None) == S.SEER_EINVAL
+    assert call(wl=None) == S.SEER_EINVAL
+    assert call(bnd=None) == S.SEER_EINVAL
+    assert call(keep=None) == S.SEER_EINVAL
+    assert call(p=S.seer_snr_params(3, 0, 3, 5, 3)) == S.SEER_EINVAL
+    assert call(p=S.seer_snr_params(3, 100, 3, 5, 0)) == S.SEER_EINVAL
+    assert call(batch=0) == S.SEER_EINVAL
+    assert call(eps=-1.0) == S.SEER_EINVAL
+    assert call(ws_bytes=S.seer_layer_workspace_bytes(d, 100) - 1) == S.SEER_EWORKSPACE
+    ev = (ctypes.c_void_p * 9)(*([FAKE] * 8 + [None]))
+    assert call(events=ev) == S.SEER_EINVAL and "events[8]" in S.seer_last_error()
 
 
 def test_repack_argument_errors(S):

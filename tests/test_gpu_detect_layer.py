@@ -1,0 +1,141 @@
+"""The detection layer (seer_layer_forward_detect) against the two calls it
+replaces: seer_layer_forward_varlen with the count, then seer_step0_detect.
+
+Counts, boundaries and keep lengths must be equal, and every row the
+compaction keeps bit-identical.  With bf16 the down projection computes only
+the 256-row tiles that hold a kept row: those tiles must equal the reference
+on every row (discarded rows included), and the rows of the other tiles must
+keep what the output held before the call.  Cases: windows much longer than
+their prefix, so that whole tiles are discarded (a small layer whose down
+projection splits K, with an empty sequence and a grid bound above the real
+row count), no boundary at all (every tile kept), the fp32 layer, and the
+LLaDA-shaped B=1 and B=16 layers of the benchmark.
+"""
+import numpy as np
+import pytest
+
+from gpu_util import dev, host, log, upload_weights
+from workloads import WORKLOADS, scaled
+from workloads.generate import make_workload
+
+pytestmark = pytest.mark.gpu
+TILE = 256
+
+CASES = {
+    # 4 sequences of 48 prefix rows and a 1024-position window, boundaries in
+    # [16, 200]: runs of 800+ discarded rows, so whole row tiles drop out
+    "small_long_windows": scaled(WORKLOADS["small_bf16_ragged"], name="small_long_windows", batch=4,
+                                 n_visual=40, n_prompt=8, window=1024, boundary=("uniform", 16, 200),
+                                 seed=1313),
+    "tiny_f32": WORKLOADS["tiny_f32"],
+    "llada_b1": WORKLOADS["llada_b1"],
+    "llada_b16_ragged": WORKLOADS["llada_b16_ragged"],
+}
+
+
+@pytest.fixture(scope="module")
+def S():
+    from paper_2607_14557_amd import seer
+    seer.load_library()
+    return seer
+
+
+def _insert_empty(batch, at):
+    """The batch with an empty sequence (no rows, empty window) inserted at
+    index `at`."""
+    cu = np.asarray(batch.cu_seqlens, np.int64)
+    cu2 = np.concatenate([cu[:at + 1], cu[at:]])
+    off = np.insert(np.asarray(batch.win_off, np.int64), at, 0)
+    wl = np.insert(np.asarray(batch.win_len, np.int64), at, 0)
+    planted = np.insert(np.asarray(batch.planted, np.int64), at, 0)
+    return cu2, off, wl, planted
+
+
+def _kept_tiles(cu, off, keep, wl, rows):
+    live = np.zeros(-(-rows // TILE), bool)
+    for b in range(len(cu) - 1):
+        k = min(max(int(keep[b]), 0), int(wl[b]))
+        used = min(max(int(off[b]) + k, 0), int(cu[b + 1] - cu[b]))
+        for r in range(int(cu[b]), int(cu[b]) + used):
+            live[r // TILE] = True
+    return live
+
+
+def _bits(t):
+    import torch
+    return t.view(torch.int16) if t.dtype == torch.bfloat16 else t.view(torch.int32)
+
+
+def _run_case(S, st, w, x, cu, off, wl, B, rows, rows_ub, act_eps, planted):
+    import torch
+    snr = S.seer_snr_params(3, 100, 3, 5, 3)
+    d, I = w.shape.d_model, w.shape.d_ff
+    # reference: the layer with the count, then the scan
+    y_ref = torch.empty(rows_ub, d, dtype=x.dtype, device="cuda")
+    cnt_ref = torch.empty(rows_ub, dtype=torch.int32, device="cuda")
+    b_ref = torch.empty(B, dtype=torch.int32, device="cuda")
+    k_ref = torch.empty(B, dtype=torch.int32, device="cuda")
+    st.layer(0, x, y_ref, cu, None, B, rows_ub, act_eps=act_eps, act_count=cnt_ref)
+    S.seer_step0_detect(cnt_ref, cu, off, wl, B, I, snr, b_ref, k_ref)
+    # the detection layer, into an output filled with a sentinel (a bf16 / fp32 NaN pattern)
+    y = torch.empty(rows_ub, d, dtype=x.dtype, device="cuda")
+    sentinel = 0x7fc1 if x.dtype == torch.bfloat16 else 0x7fc00001
+    _bits(y).fill_(sentinel)
+    cnt = torch.empty(rows_ub, dtype=torch.int32, device="cuda")
+    bnd = torch.empty(B, dtype=torch.int32, device="cuda")
+    keep = torch.empty(B, dtype=torch.int32, device="cuda")
+    S.seer_layer_forward_detect(st.dims, st.packed[0], x, y, rows_ub, cu, B, act_eps, cnt, off, wl, snr, bnd, keep,
+                                st.workspace, st.ws_bytes)
+    torch.cuda.synchronize()
+    assert torch.equal(cnt[:rows], cnt_ref[:rows])
+    assert torch.equal(bnd, b_ref) and torch.equal(keep, k_ref)
+    if planted is not None:
+        np.testing.assert_array_equal(host(bnd), planted)
+    cu_h, off_h, wl_h, keep_h = host(cu), host(off), host(wl), host(keep)
+    kept_rows = 0
+    for b in range(B):
+        n = min(int(off_h[b]) + int(keep_h[b]), int(cu_h[b + 1] - cu_h[b]))
+        s0 = int(cu_h[b])
+        assert torch.equal(_bits(y[s0:s0 + n]), _bits(y_ref[s0:s0 + n])), "sequence %d: kept rows differ" % b
+        kept_rows += n
+    live = _kept_tiles(cu_h, off_h, keep_h, wl_h, rows)
+    if x.dtype == torch.bfloat16:
+        yb, rb = _bits(y), _bits(y_ref)
+        for t in range(len(live)):
+            r0, r1 = t * TILE, min((t + 1) * TILE, rows)
+            if live[t]:
+                assert torch.equal(yb[r0:r1], rb[r0:r1]), "kept tile %d differs" % t
+            else:
+                assert bool((yb[r0:r1] == sentinel).all()), "tile %d was written" % t
+        assert bool((yb[rows:] == sentinel).all()), "rows past the batch were written"
+    else:
+        assert torch.equal(_bits(y[:rows]), _bits(y_ref[:rows]))
+    log("  %d sequences, %d rows (grid bound %d): %d kept rows, %d of %d row tiles kept" %
+        (B, rows, rows_ub, kept_rows, int(live.sum()), len(live)))
+    return int(live.sum()), len(live)
+
+
+@pytest.mark.parametrize("name", list(CASES))
+def test_detect_layer_matches_layer_then_scan(S, name):
+    from paper_2607_14557_amd.runner import SeerStack, dims_for
+    w = CASES[name]
+    sh = w.shape
+    log("detection layer %s: inputs" % name)
+    layers, batch = make_workload(w)
+    T = w.rows_full
+    small = name == "small_long_windows"
+    rows_ub = T + 300 if small else T
+    st = SeerStack(dims_for(sh.d_model, sh.n_heads, sh.head_dim, sh.d_ff, w.dtype, w.rms_eps), 1, rows_ub)
+    st.set_layer(0, upload_weights(layers[0], w.dtype))
+    x = dev(np.concatenate([batch.x, np.zeros((rows_ub - T, sh.d_model), np.float32)]), w.dtype)
+    cu, off, wl = dev(batch.cu_seqlens), dev(batch.win_off), dev(batch.win_len)
+    live, tiles = _run_case(S, st, w, x, cu, off, wl, w.batch, T, rows_ub, w.act_eps, batch.planted)
+    if w.dtype == "bf16":
+        assert live < tiles, "no row tile was discarded: the case does not test the truncated down projection"
+    if small:
+        log("detection layer %s: with an empty sequence inserted" % name)
+        cu2, off2, wl2, planted2 = _insert_empty(batch, 2)
+        _run_case(S, st, w, x, dev(cu2), dev(off2), dev(wl2), w.batch + 1, T, rows_ub, w.act_eps, planted2)
+        log("detection layer %s: act_eps 0 (no boundary, every window kept whole)" % name)
+        live, tiles = _run_case(S, st, w, x, cu, off, wl, w.batch, T, rows_ub, 0.0, None)
+        assert live == tiles
