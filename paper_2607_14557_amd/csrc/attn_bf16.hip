@@ -52,11 +52,21 @@ __global__ __launch_bounds__(NT, 2) void attn_bf16_kernel(AttnParams p) {
   __shared__ __attribute__((aligned(1024))) uint8_t v_lds0[KT * K_ROW];
   __shared__ __attribute__((aligned(1024))) uint8_t v_lds1[KT * K_ROW];
 
-  // ---- which (sequence, query tile) this block owns -------------------------
+  // ---- which (sequence, query tile, head) this block owns -------------------
+  // Units are (head, query tile over the batch), query tiles fastest; each XCD
+  // takes a contiguous range of them, so the query tiles of one sequence and
+  // head run together on one XCD and find their K and V tiles in its L2.
+  int xt, h;
+  {
+    const int gx = gridDim.x;
+    const int w = xcd_remap(blockIdx.x + gx * blockIdx.y, gx * gridDim.y);
+    xt = w % gx;
+    h = w / gx;
+  }
   int b = -1, t = 0;
   {
     int acc = 0;
-    const int j = blockIdx.x;
+    const int j = xt;
     for (int s = 0; s < p.B; ++s) {
       int len = p.cu[s + 1] - p.cu[s];
       len = len < 0 ? 0 : len;
@@ -66,7 +76,6 @@ __global__ __launch_bounds__(NT, 2) void attn_bf16_kernel(AttnParams p) {
     }
   }
   if (b < 0) return;
-  const int h = blockIdx.y;
   const int s0 = p.cu[b];
   if (s0 < 0 || s0 >= p.rows_ub) return;
   int len = p.cu[b + 1] - s0;

@@ -89,6 +89,15 @@ __device__ __forceinline__ int wave_min_int(int v) {
   return v;
 }
 
+// Workgroup ids are dealt round robin over the 8 XCDs.  xcd_remap turns block
+// id bid in [0, nblk) into a logical unit id such that each XCD walks a
+// contiguous range of logical units (surplus ids past a multiple of 8 map to
+// themselves), so units that share operands run on one XCD and its L2.
+__device__ __forceinline__ int xcd_remap(int bid, int nblk) {
+  const int per = nblk >> 3;
+  return bid < (per << 3) ? (bid & 7) * per + (bid >> 3) : bid;
+}
+
 // Row count of a packed batch: cu_seqlens[batch] when given, clamped to the
 // host-side upper bound that sized the grid.
 __device__ __forceinline__ int rows_from(const int* m_ptr, int m_ub) {

@@ -57,15 +57,9 @@ constexpr int ROW_BYTES = BK * 2;                   // 128 bytes per A tile row
 
 __device__ __forceinline__ int swz(int r) { return (r & 7) ^ ((r >> 3) & 1); }
 
-// Workgroup ids are dealt round robin over the 8 XCDs.  xcd_remap turns block
-// id bid in [0, nblk) into a logical tile id such that each XCD walks a
-// contiguous range of logical tiles; raster lays those out in groups of
+// Tiles in the logical order of xcd_remap are laid out by raster in groups of
 // GROUP_M tile rows, so the blocks resident on one XCD share A row-tiles and
 // B column-tiles in its L2.
-__device__ __forceinline__ int xcd_remap(int bid, int nblk) {
-  const int per = nblk >> 3;
-  return bid < (per << 3) ? (bid & 7) * per + (bid >> 3) : bid;
-}
 
 __device__ __forceinline__ void raster(int lid, int tiles_m, int tiles_n, int& tm, int& tn) {
   const int gsz = GROUP_M * tiles_n;
