@@ -8,8 +8,9 @@ on every row (discarded rows included), and the rows of the other tiles must
 keep what the output held before the call.  Cases: windows much longer than
 their prefix, so that whole tiles are discarded (a small layer whose down
 projection splits K, with an empty sequence and a grid bound above the real
-row count), no boundary at all (every tile kept), the fp32 layer, and the
-LLaDA-shaped B=1 and B=16 layers of the benchmark.
+row count), no boundary at all (every tile kept), more than 1024 row tiles over 420
+sequences, the fp32 layer, and the LLaDA-shaped B=1 and B=16 layers of the
+benchmark.
 """
 import numpy as np
 import pytest
@@ -27,6 +28,12 @@ CASES = {
     "small_long_windows": scaled(WORKLOADS["small_bf16_ragged"], name="small_long_windows", batch=4,
                                  n_visual=40, n_prompt=8, window=1024, boundary=("uniform", 16, 200),
                                  seed=1313),
+    # 420 sequences of 628 rows (263760 rows, 1031 row tiles): the tile list
+    # is built in more than one 1024-tile chunk, the first sequence of a tile
+    # is found by bisection over hundreds of sequences
+    "small_many_sequences": scaled(WORKLOADS["small_bf16_ragged"], name="small_many_sequences", batch=420,
+                                   n_visual=20, n_prompt=8, window=600, boundary=("uniform", 8, 40),
+                                   seed=1414),
     "tiny_f32": WORKLOADS["tiny_f32"],
     "llada_b1": WORKLOADS["llada_b1"],
     "llada_b16_ragged": WORKLOADS["llada_b16_ragged"],
@@ -129,7 +136,11 @@ def test_detect_layer_matches_layer_then_scan(S, name):
     st.set_layer(0, upload_weights(layers[0], w.dtype))
     x = dev(np.concatenate([batch.x, np.zeros((rows_ub - T, sh.d_model), np.float32)]), w.dtype)
     cu, off, wl = dev(batch.cu_seqlens), dev(batch.win_off), dev(batch.win_len)
-    live, tiles = _run_case(S, st, w, x, cu, off, wl, w.batch, T, rows_ub, w.act_eps, batch.planted)
+    # the planted boundaries are checked where the workload is built to give them
+    # exactly; with 420 short-content windows a few are found early by design of
+    # the criterion, and what is checked there is equality with the two calls
+    planted = None if name == "small_many_sequences" else batch.planted
+    live, tiles = _run_case(S, st, w, x, cu, off, wl, w.batch, T, rows_ub, w.act_eps, planted)
     if w.dtype == "bf16":
         assert live < tiles, "no row tile was discarded: the case does not test the truncated down projection"
     if small:
