@@ -473,6 +473,9 @@ def bench_stack(args, w):
                      "flop_per_launch": flop, "launch_ms": round(gu_ms, 4)},
         "trunc_step_ms": round(t_trunc, 3), "full_step_ms": round(t_full, 3),
         "speedup_trunc_vs_full": round(t_full / t_trunc, 3),
+        # raw packed rows through all layers of one step per second
+        "trunc_step_rows_per_s": round(rows_t / (t_trunc * 1e-3), 1),
+        "full_step_rows_per_s": round(T / (t_full * 1e-3), 1),
         "job_speedup_vs_untruncated": round(n_den * t_full / ms_job, 3),
         "cached_step_ms": None if t_cached is None else round(t_cached, 3),
         "speedup_cached_vs_trunc": None if t_cached is None else round(t_trunc / t_cached, 3),
@@ -759,6 +762,9 @@ def main():
         "full_step_ms": None if t_full is None else round(t_full, 4),
         "speedup_trunc_vs_full": None if t_full is None else round(t_full / t_trunc, 3),
         "trunc_step_tokens_per_s": round(sum_keep / (t_trunc * 1e-3), 1),
+        # raw packed rows (prefix + kept window; full window) per second of one step
+        "trunc_step_rows_per_s": round(rows_alg / (t_trunc * 1e-3), 1),
+        "full_step_rows_per_s": None if t_full is None else round(T / (t_full * 1e-3), 1),
         "full_step_tokens_per_s": None if t_full is None else round(sum_keep / (t_full * 1e-3), 1),
         "cached_step_ms": None if t_cached is None else round(t_cached, 4),
         "cached_step_tokens_per_s": None if t_cached is None else round(sum_keep / (t_cached * 1e-3), 1),
