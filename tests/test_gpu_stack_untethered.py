@@ -5,8 +5,12 @@ layer -- and the GPU does the same through the C ABI.  Both must find the
 planted boundaries; the difference of the two sparsity fractions on every
 window row is reported (not gated: four layers of bf16 rounding move a few
 activations across eps, see the count checks of test_gpu_stack.py for the
-teacher-forced gate).  The oracle pass takes one to two minutes on the host.
+teacher-forced gate).  The oracle pass takes one to two minutes per stack on
+the host, so the test runs only with SEER_SLOW_TESTS=1 (measured: multi-crop
+2.85e-3, video 2.52e-3, every boundary equal to the planted one).
 """
+import os
+
 import numpy as np
 import pytest
 
@@ -17,7 +21,10 @@ from oracle.sparsity import sparsity_fraction
 from workloads import WORKLOADS
 from workloads.generate import layer_weights_torch, make_stack_batch
 
-pytestmark = pytest.mark.gpu
+pytestmark = [pytest.mark.gpu,
+              pytest.mark.skipif(os.environ.get("SEER_SLOW_TESTS") != "1",
+                                 reason="about 3.5 min of fp64 host work for both stacks; "
+                                        "run with SEER_SLOW_TESTS=1")]
 
 
 @pytest.fixture(scope="module")
