@@ -150,3 +150,30 @@ def test_detect_layer_matches_layer_then_scan(S, name):
         log("detection layer %s: act_eps 0 (no boundary, every window kept whole)" % name)
         live, tiles = _run_case(S, st, w, x, cu, off, wl, w.batch, T, rows_ub, 0.0, None)
         assert live == tiles
+
+
+def test_detect_layer_with_no_rows(S):
+    """A batch whose sequences are all empty: the scan gives boundary 0 and
+    keep length 0 everywhere, no row tile is kept and nothing is written."""
+    import torch
+    from paper_2607_14557_amd.runner import SeerStack, dims_for
+    w = WORKLOADS["small_bf16_ragged"]
+    sh = w.shape
+    layers, _ = make_workload(w)
+    st = SeerStack(dims_for(sh.d_model, sh.n_heads, sh.head_dim, sh.d_ff, w.dtype, w.rms_eps), 1, 256)
+    st.set_layer(0, upload_weights(layers[0], w.dtype))
+    B = 3
+    x = torch.zeros(256, sh.d_model, dtype=torch.bfloat16, device="cuda")
+    y = torch.empty_like(x)
+    _bits(y).fill_(0x7fc1)
+    cnt = torch.full((256,), -1, dtype=torch.int32, device="cuda")
+    bnd = torch.full((B,), -1, dtype=torch.int32, device="cuda")
+    keep = torch.full((B,), -1, dtype=torch.int32, device="cuda")
+    zeros = dev(np.zeros(B + 1, np.int64))
+    log("detection layer with no rows")
+    S.seer_layer_forward_detect(st.dims, st.packed[0], x, y, 256, zeros, B, w.act_eps, cnt, zeros[:B], zeros[:B],
+                                S.seer_snr_params(3, 100, 3, 5, 3), bnd, keep, st.workspace, st.ws_bytes)
+    torch.cuda.synchronize()
+    assert bool((_bits(y) == 0x7fc1).all())
+    assert torch.count_nonzero(bnd).item() == 0 and torch.count_nonzero(keep).item() == 0
+    assert torch.count_nonzero(cnt).item() == 0      # the count buffer is zeroed over the grid bound
