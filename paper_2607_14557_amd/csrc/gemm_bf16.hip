@@ -547,7 +547,8 @@ __device__ __forceinline__ void gemm_tile(const GemmParams& p, uint8_t* st0, uin
 // Units of work: the 256x256 tiles, except that when the tiles leave a last
 // round of r < n_units/2 tiles on the n_units workgroups that run at once,
 // each of those r tiles becomes two 128x256 halves (disjoint outputs, no
-// reduction), so the last round keeps twice as many CUs busy.  Tile geometry
+// reduction), so the last round keeps twice as many CUs busy; a last tile
+// row of at most 128 rows is computed as half tiles only.  Tile geometry
 // follows the real row count read on the device (or the row-tile list of
 // p.mtiles); surplus blocks of the upper-bound grid, and halves that start
 // past the last row, exit at once.
@@ -562,25 +563,38 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(GemmParams p) {
   const int M = rows_from(p.m_ptr, p.m_ub);
   const int tiles_m = p.mtiles ? p.mtiles[0] : (M + 255) / 256;
   const int tiles_n = p.N / 256;
-  const int ntiles = tiles_m * tiles_n;
-  int full = ntiles;
+  // A last tile row that holds at most 128 rows runs as single half tiles
+  // (their second halves would hold no row); the full tiles are those of the
+  // other rows.
+  const bool half_last = !p.mtiles && tiles_m > 0 && M - 256 * (tiles_m - 1) <= 128;
+  const int tiles_mf = tiles_m - (half_last ? 1 : 0);
+  const int nfull = tiles_mf * tiles_n;
+  const int nlast = half_last ? tiles_n : 0;
+  int full = nfull;
   if (p.n_units > 0) {
-    const int rem = ntiles % p.n_units;
-    if (2 * rem <= p.n_units) full = ntiles - rem;
+    const int rem = nfull % p.n_units;
+    if (2 * rem + nlast <= p.n_units) full = nfull - rem;
   }
+  const int nsplit = 2 * (nfull - full);           // halves of the tiles past `full`
   const int u = blockIdx.x;
   const int KT = p.K / BK;
   int tm, tn;
-  if (u >= full + 2 * (ntiles - full)) return;
+  if (u >= full + nsplit + nlast) return;
   if (u < full) {
-    raster(xcd_remap(u, full), tiles_m, tiles_n, tm, tn);
+    raster(xcd_remap(u, full), tiles_mf, tiles_n, tm, tn);
     if (p.mtiles) tm = p.mtiles[1 + tm];
     gemm_tile<EPI, 256>(p, st0, st1, st2, st3, M, tm * 256, tn * 256, 0, KT);
   } else {
     const int v = u - full;
-    raster(full + (v >> 1), tiles_m, tiles_n, tm, tn);
-    if (p.mtiles) tm = p.mtiles[1 + tm];
-    const int m0 = tm * 256 + (v & 1) * 128;
+    int m0;
+    if (v < nsplit) {
+      raster(full + (v >> 1), tiles_mf, tiles_n, tm, tn);
+      if (p.mtiles) tm = p.mtiles[1 + tm];
+      m0 = tm * 256 + (v & 1) * 128;
+    } else {
+      tn = v - nsplit;
+      m0 = (tiles_m - 1) * 256;
+    }
     if (m0 >= M) return;
     gemm_tile<EPI, 128>(p, st0, st1, st2, st3, M, m0, tn * 256, 0, KT);
   }
