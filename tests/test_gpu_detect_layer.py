@@ -122,28 +122,34 @@ def _run_case(S, st, w, x, cu, off, wl, B, rows, rows_ub, act_eps, planted):
     return int(live.sum()), len(live)
 
 
-@pytest.mark.parametrize("name", list(CASES))
+@pytest.mark.parametrize("name", list(CASES) + ["small_long_windows_rope"])
 def test_detect_layer_matches_layer_then_scan(S, name):
     from paper_2607_14557_amd.runner import SeerStack, dims_for
+    # the rotary variant: the same inputs through the layer with the rotary
+    # embedding of q and k (its boundaries need not be the planted ones)
+    rope = name.endswith("_rope")
+    if rope:
+        name = name[:-len("_rope")]
     w = CASES[name]
     sh = w.shape
-    log("detection layer %s: inputs" % name)
+    log("detection layer %s%s: inputs" % (name, " (rotary)" if rope else ""))
     layers, batch = make_workload(w)
     T = w.rows_full
     small = name == "small_long_windows"
     rows_ub = T + 300 if small else T
-    st = SeerStack(dims_for(sh.d_model, sh.n_heads, sh.head_dim, sh.d_ff, w.dtype, w.rms_eps), 1, rows_ub)
+    st = SeerStack(dims_for(sh.d_model, sh.n_heads, sh.head_dim, sh.d_ff, w.dtype, w.rms_eps,
+                            rope_theta=10000.0 if rope else 0.0), 1, rows_ub)
     st.set_layer(0, upload_weights(layers[0], w.dtype))
     x = dev(np.concatenate([batch.x, np.zeros((rows_ub - T, sh.d_model), np.float32)]), w.dtype)
     cu, off, wl = dev(batch.cu_seqlens), dev(batch.win_off), dev(batch.win_len)
     # the planted boundaries are checked where the workload is built to give them
     # exactly; with 420 short-content windows a few are found early by design of
     # the criterion, and what is checked there is equality with the two calls
-    planted = None if name == "small_many_sequences" else batch.planted
+    planted = None if name == "small_many_sequences" or rope else batch.planted
     live, tiles = _run_case(S, st, w, x, cu, off, wl, w.batch, T, rows_ub, w.act_eps, planted)
-    if w.dtype == "bf16":
+    if w.dtype == "bf16" and not rope:
         assert live < tiles, "no row tile was discarded: the case does not test the truncated down projection"
-    if small:
+    if small and not rope:
         log("detection layer %s: with an empty sequence inserted" % name)
         cu2, off2, wl2, planted2 = _insert_empty(batch, 2)
         _run_case(S, st, w, x, dev(cu2), dev(off2), dev(wl2), w.batch + 1, T, rows_ub, w.act_eps, planted2)
