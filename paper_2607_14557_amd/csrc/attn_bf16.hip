@@ -18,8 +18,9 @@
 // its A-operand fragments (8 keys of one dim per lane) come from pairs of LDS
 // transpose reads (ds_read_b64_tr_b16).  The P V product runs in
 // fp16: the probabilities keep three more mantissa bits than bf16 would give.
-// The running maximum is moved only when a tile raises it by more than 2^8
-// (log2 units), so the O rescale is rare and P stays <= 256, exact in fp16.
+// The softmax's reference maximum is set on a sequence's first key tile and
+// moved only when a later tile overflows the fp16 probabilities: the common
+// tile takes no maximum at all, and the O rescale is rare.
 #include <math.h>
 
 #include <type_traits>
@@ -228,20 +229,51 @@ __global__ __launch_bounds__(NT, 2) void attn_bf16_kernel(AttnParams p) {
           if (key >= nk || (key >= P && key < P4)) s[i][r] = -INFINITY;
         }
     }
-    float mt = s[0][0];
+    // Probabilities against the reference maximum, packed to fp16 as the
+    // P V product takes them, and their row sum over the packed values (one
+    // v_dot2_f32_f16 with (1, 1) per pair, accumulated in fp32).
+    f16x8_t pf[4];
+    float lsum;
+    auto probs = [&]() {
+      const float mc = m_run * c;
+      const f16x2_t one2 = {(_Float16)1.0f, (_Float16)1.0f};
+      lsum = 0.0f;
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+      for (int sl = 0; sl < 4; ++sl) {
+        const int i = sl >> 1, hf = sl & 1;
+        u32x4_t pk;
 #pragma unroll
-      for (int r = 0; r < 16; ++r) mt = fmaxf(mt, s[i][r]);
-    {
+        for (int e = 0; e < 4; ++e) {
+          const float p0 = __builtin_amdgcn_exp2f(s[i][hf * 8 + 2 * e] * c - mc);
+          const float p1 = __builtin_amdgcn_exp2f(s[i][hf * 8 + 2 * e + 1] * c - mc);
+          const f16x2_t h = __builtin_convertvector(f32x2_t{p0, p1}, f16x2_t);
+          lsum = __builtin_amdgcn_fdot2(h, one2, lsum, false);
+          pk[e] = __builtin_bit_cast(uint32_t, h);
+        }
+        pf[sl] = __builtin_bit_cast(f16x8_t, pk);
+      }
+    };
+    // The reference maximum is set on the first tile and moved only when a
+    // later tile holds a probability fp16 cannot represent (a score about 16
+    // log2 units above it): its row sum is then inf, and the tile is redone
+    // against the true running maximum, with O and the sum rescaled.  Any
+    // reference at or below the running maximum gives the same softmax; the
+    // common tile skips the maximum.
+    bool redo = kt == 0;
+    if (!redo) {
+      probs();
+      redo = __any(!(lsum < INFINITY));
+    }
+    if (redo) {
+      float mt = s[0][0];
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) mt = fmaxf(mt, s[i][r]);
       // lanes l and l ^ 32 hold the two 32-key halves of one query's column:
       // a register swap across the halves, no LDS round trip
       const u32x2_t sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mt), __float_as_uint(mt), false, false);
       mt = fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1]));
-    }
-    // Move the reference maximum only when some lane's tile maximum exceeds it
-    // by more than 2^8 in the exponent (always on the first tile).
-    if (__any((mt - m_run) * c > 8.0f)) {
       const float m_new = fmaxf(m_run, mt);
       const float alpha = __builtin_amdgcn_exp2f((m_run - m_new) * c);
       m_run = m_new;
@@ -250,34 +282,13 @@ __global__ __launch_bounds__(NT, 2) void attn_bf16_kernel(AttnParams p) {
       for (int i = 0; i < 4; ++i)
 #pragma unroll
         for (int r = 0; r < 16; ++r) o[i][r] *= alpha;
+      probs();
     }
-    const float mc = m_run * c;
-#pragma unroll
-    for (int i = 0; i < 2; ++i)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) s[i][r] = __builtin_amdgcn_exp2f(s[i][r] * c - mc);
+    l_run += lsum;
 
     // O^T += V^T P^T over four 16-key slices x four 32-dim tiles; the V^T
     // fragment of step n + 2 is read while step n multiplies.
     {
-      // The row sum is taken over the fp16 probabilities the product uses:
-      // one v_dot2_f32_f16 with (1, 1) per packed pair, accumulated in fp32.
-      f16x8_t pf[4];
-      float lsum = 0.0f;
-      const f16x2_t one2 = {(_Float16)1.0f, (_Float16)1.0f};
-#pragma unroll
-      for (int sl = 0; sl < 4; ++sl) {
-        const int i = sl >> 1, hf = sl & 1;
-        u32x4_t pk;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const f16x2_t h = __builtin_convertvector(f32x2_t{s[i][hf * 8 + 2 * e], s[i][hf * 8 + 2 * e + 1]}, f16x2_t);
-          lsum = __builtin_amdgcn_fdot2(h, one2, lsum, false);
-          pk[e] = __builtin_bit_cast(uint32_t, h);
-        }
-        pf[sl] = __builtin_bit_cast(f16x8_t, pk);
-      }
-      l_run += lsum;
       // A operand of step n (16-key slice sl = n/4, 32-dim tile dt = n%4): lane
       // l needs 8 keys of dim 32 dt + l%32, in the order the P fragment holds
       // them (keys 16 hf + 4 kh + 0..3, then + 8).  In each group of 16 lanes

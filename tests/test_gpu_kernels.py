@@ -280,6 +280,47 @@ def test_layer_vs_oracle_ragged(S, case):
     assert e_dn <= tol
 
 
+def test_attention_peaked_softmax(S):
+    """Scores spread over hundreds of log2 units (q and k projections 12x the
+    usual scale): for most queries a later key tile holds a score far above
+    the first tile's maximum, so the softmax's reference maximum has to move
+    mid-sequence, past the range fp16 probabilities can hold.  The attention
+    stage, teacher-forced from the kernel's own q, k and v, must match the
+    oracle's softmax within the bf16 bar."""
+    d, H, dh, I = 512, 4, 128, 1024
+    rng = np.random.default_rng(4242)
+    W = _rand_layer(rng, d, I, 0.02)
+    W["wq"] = W["wq"] * 12.0
+    W["wk"] = W["wk"] * 12.0
+    W = _round(W, "bf16")
+    lens = [700, 64, 1, 333, 129]
+    cu = np.concatenate([[0], np.cumsum(lens)])
+    T = int(cu[-1])
+    x = rng.standard_normal((T, d))
+    xd = dev(x, "bf16")
+    log("peaked softmax: lens=%s, q/k projections x12" % lens)
+    L = _Layer(S, d, H, dh, I, "bf16", T, W)
+    L.run(xd, dev(cu), len(lens))
+    qkv = host(L.inter("qkv", T, 3 * d))
+    o = host(L.inter("o", T, d))
+    c = np.log2(np.e) / np.sqrt(dh)
+    jumps = []
+    for b in range(len(lens)):
+        s = slice(cu[b], cu[b + 1])
+        q, k = qkv[s, :d], qkv[s, d:2 * d]
+        for h in range(H):
+            hs = slice(h * dh, (h + 1) * dh)
+            e = (q[:, hs] @ k[:, hs].T) * c               # log2 units
+            jumps.append(e.max(axis=1) - e[:, :64].max(axis=1))
+        o_ref = attention_seq(q, k, qkv[s, 2 * d:], H)
+        eo = rel_err(o[s], o_ref)
+        assert eo <= BF16_TOL, "attention seq %d err %.3e" % (b, eo)
+    jumps = np.concatenate(jumps)
+    log("  max over later key tiles above the first tile's: >8 for %.0f%%, >16 for %.0f%% of query heads "
+        "(largest %.0f log2 units)" % (100 * np.mean(jumps > 8), 100 * np.mean(jumps > 16), jumps.max()))
+    assert np.mean(jumps > 16) > 0.2, "the case does not move the reference maximum far enough"
+
+
 def test_layer_static_padding_equals_cut_layout_bitwise(S):
     """Pad rows masked by seqused leave the kept rows bit-identical."""
     import torch

@@ -9,7 +9,7 @@ cached step then runs on the kept window rows alone.
   * K | V export: bit-exact against the K | V columns of the full step's qkv
     rows (the layer call's own workspace);
   * the cached step against the full step's window rows: the same inputs, so
-    equal up to rounding (the attention's lazy rescale is decided per wave, and
+    equal up to rounding (the attention's reference maximum is chosen per wave, and
     the window rows are grouped into waves differently in the two layouts);
   * teacher-forced against oracle.layer_forward_cached_rows fed with the GPU's
     layer input and cache, on sampled sequences, layers and rows.
