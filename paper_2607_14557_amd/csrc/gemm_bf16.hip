@@ -147,6 +147,29 @@ __device__ __forceinline__ void gemm_tile(const GemmParams& p, uint8_t* st0, uin
                                                ko, 0, 0);
   };
 
+  // Output projection (RESID_SPLIT, full tiles, K tiles a multiple of four):
+  // the ring loads of the last three K tiles, which would re-read the last A
+  // tile, bring rows 0..191 of the residual tile instead, 64 rows into each of
+  // stages 0, 1, 2 (those of tiles KT - 4 .. KT - 2).  Wave w loads the 64
+  // columns its own epilogue adds, into the 8 KiB of the stage its A loads
+  // fill (rows of 128 bytes, the swizzle of A), so its epilogue reads them
+  // after its own vmcnt wait, with no barrier.  Per quarter the same number of
+  // loads as dma_a, so the ring's wait counts hold.
+  constexpr bool kResLds = EPI == EPI_RESID_SPLIT && BMT == 256 && !PART;
+  const bool res_lds = kResLds && KT >= 4 && (KT & 3) == 0;
+  auto dma_r = [&](uint8_t* stg, int part, int q) {
+    const __amdgpu_buffer_rsrc_t rsr = __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p.R), 0, -1, 0x00020000);
+#pragma unroll
+    for (int k = AP * q; k < AP * q + AP; ++k) {
+      const int rs = 8 * k + (lane >> 3);                // row inside the 64-row part
+      int row = m0 + 64 * part + rs;
+      row = row < M ? row : M - 1;                       // rows past M are never stored
+      const uint32_t col = (uint32_t)(n0 + 64 * wave + 8 * ((lane & 7) ^ swz(rs)));
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsr, (lds_void_t*)(stg + wv * 8192 + k * 1024), 16,
+                                               (uint32_t)row * (uint32_t)p.ldr * 2u + col * 2u, 0, 0, 0);
+    }
+  };
+
   // Fragment geometry: lane l holds row (l & 31) of a 32-row MFMA tile and
   // the 8 K values 16 s + 8 (l >> 5) .. +7 of K slice s.
   const int fr = lane & 31;
@@ -206,12 +229,12 @@ __device__ __forceinline__ void gemm_tile(const GemmParams& p, uint8_t* st0, uin
   // landed -- at most the 7 slices of loads issued since may be in flight --
   // and until its LDS reads are done.  The barrier is bare (no fence): a
   // fence would also wait for the loads of tiles T+2 and T+3.
-#define SEER_TILE(T, SC, SN, SF, BC, BNX)                                           \
+#define SEER_TILE_D(T, SC, SN, SF, BC, BNX, DMA)                                    \
   {                                                                                 \
     _Pragma("unroll") for (int ks = 0; ks < 4; ++ks) {                              \
       const int cur = ks & 1;                                                       \
       SEER_FLOAD(ks < 3 ? SC : SN, ks < 3 ? ks + 1 : 0, cur ^ 1);                   \
-      dma_a(SF, (T) + 3, ks);                                                       \
+      DMA;                                                                          \
       SEER_GLOAD_B(BNX, (T) + 1, ks);                                               \
       _Pragma("unroll") for (int i = 0; i < NI; ++i)                                \
         _Pragma("unroll") for (int j = 0; j < 2; ++j)                               \
@@ -225,6 +248,7 @@ __device__ __forceinline__ void gemm_tile(const GemmParams& p, uint8_t* st0, uin
       }                                                                             \
     }                                                                               \
   }
+#define SEER_TILE(T, SC, SN, SF, BC, BNX) SEER_TILE_D(T, SC, SN, SF, BC, BNX, dma_a(SF, (T) + 3, ks))
 
   // prologue: A tiles 0, 1, 2 into stages 0, 1, 2 and B tile 0 into set 0;
   // wait for all but tile 2 (its NA loads may stay in flight)
@@ -241,21 +265,33 @@ __device__ __forceinline__ void gemm_tile(const GemmParams& p, uint8_t* st0, uin
   __builtin_amdgcn_sched_barrier(0);
   SEER_FLOAD(st0, 0, 0);
   int kt = 0;
-  for (; kt + 4 <= KT; kt += 4) {
+  const int kt_ring = res_lds ? KT - 4 : KT;
+  for (; kt + 4 <= kt_ring; kt += 4) {
     SEER_TILE(kt, st0, st1, st3, bq0, bq1);
     SEER_TILE(kt + 1, st1, st2, st0, bq1, bq0);
     SEER_TILE(kt + 2, st2, st3, st1, bq0, bq1);
     SEER_TILE(kt + 3, st3, st0, st2, bq1, bq0);
   }
+  if constexpr (kResLds) {
+    if (res_lds) {                                  // the last four K tiles
+      SEER_TILE(kt, st0, st1, st3, bq0, bq1);
+      SEER_TILE_D(kt + 1, st1, st2, st0, bq1, bq0, dma_r(st0, 0, ks));
+      SEER_TILE_D(kt + 2, st2, st3, st1, bq0, bq1, dma_r(st1, 1, ks));
+      SEER_TILE_D(kt + 3, st3, st0, st2, bq1, bq0, dma_r(st2, 2, ks));
+      kt += 4;
+    }
+  }
   if (kt < KT) {                                   // K/64 = 2 mod 4
     SEER_TILE(kt, st0, st1, st3, bq0, bq1);
     SEER_TILE(kt + 1, st1, st2, st0, bq1, bq0);
   }
-  // the loads past the last tile (clamped re-reads) land before the epilogue
+  // the loads past the last tile (clamped re-reads, or the output projection's
+  // residual rows) land before the epilogue
   __builtin_amdgcn_s_waitcnt(waitcnt_imm(0, 15));
 #undef SEER_GLOAD_B
 #undef SEER_FLOAD
 #undef SEER_TILE
+#undef SEER_TILE_D
 
   // ---- K split: the fp32 sums of this split, row-major in the packed column
   // order of the weight (the finalize kernel applies the epilogue) ----------
@@ -306,9 +342,19 @@ __device__ __forceinline__ void gemm_tile(const GemmParams& p, uint8_t* st0, uin
     int row = m0 + i * 32 + fr;
     row = row < M ? row : M - 1;             // rows past M are never stored
     if constexpr (kRes) {
-      const uint16_t* rb = R + (size_t)row * p.ldr + colw;
+      bool lds = false;
+      if constexpr (kResLds) lds = res_lds && i < 6;
+      if (lds) {
+        // row 32 (i % 2) + fr of residual part i / 2 (stage i / 2); its
+        // swizzle is that of fr
+        const uint8_t* sb = (i < 2 ? st0 : i < 4 ? st1 : st2) + wv * 8192 + (32 * (i & 1) + fr) * ROW_BYTES;
 #pragma unroll
-      for (int jt = 0; jt < 4; ++jt) dst[jt] = *reinterpret_cast<const u32x4_t*>(rb + 16 * jt);
+        for (int jt = 0; jt < 4; ++jt) dst[jt] = *reinterpret_cast<const u32x4_t*>(sb + (((fhalf + 2 * jt) ^ fsw) << 4));
+      } else {
+        const uint16_t* rb = R + (size_t)row * p.ldr + colw;
+#pragma unroll
+        for (int jt = 0; jt < 4; ++jt) dst[jt] = *reinterpret_cast<const u32x4_t*>(rb + 16 * jt);
+      }
     }
     if constexpr (kPair) {
       const uint16_t* rb = static_cast<const uint16_t*>(p.R2) + (size_t)row * p.ldr + colw;
