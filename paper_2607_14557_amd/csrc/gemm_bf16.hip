@@ -147,22 +147,28 @@ __device__ __forceinline__ void gemm_tile(const GemmParams& p, uint8_t* st0, uin
                                                ko, 0, 0);
   };
 
-  // Output projection (RESID_SPLIT, full tiles, K tiles a multiple of four):
-  // the ring loads of the last three K tiles, which would re-read the last A
-  // tile, bring rows 0..191 of the residual tile instead, 64 rows into each of
-  // stages 0, 1, 2 (those of tiles KT - 4 .. KT - 2).  Wave w loads the 64
+  // Residual epilogues of full tiles (RESID_SPLIT after the output
+  // projection, RESID_PAIR after the down projection) with K tiles a multiple
+  // of four: the ring loads of the last three K tiles, which would re-read the
+  // last A tile, bring 64-row parts of the residual instead, one into each of
+  // stages 0, 1, 2 (those of tiles KT - 4 .. KT - 2): rows 0..191 of R.  Wave w loads the 64
   // columns its own epilogue adds, into the 8 KiB of the stage its A loads
   // fill (rows of 128 bytes, the swizzle of A), so its epilogue reads them
   // after its own vmcnt wait, with no barrier.  Per quarter the same number of
   // loads as dma_a, so the ring's wait counts hold.
-  constexpr bool kResLds = EPI == EPI_RESID_SPLIT && BMT == 256 && !PART;
+  constexpr bool kResLds = (EPI == EPI_RESID_SPLIT || EPI == EPI_RESID_PAIR) && BMT == 256 && !PART;
   const bool res_lds = kResLds && KT >= 4 && (KT & 3) == 0;
+  // For the residual pair (R high, R2 low) the three parts are R rows 0..63,
+  // R2 rows 0..63 and R rows 64..127.
   auto dma_r = [&](uint8_t* stg, int part, int q) {
-    const __amdgpu_buffer_rsrc_t rsr = __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p.R), 0, -1, 0x00020000);
+    constexpr bool pair = EPI == EPI_RESID_PAIR;
+    const void* base = pair && part == 1 ? p.R2 : p.R;
+    const int r0 = pair ? (part == 2 ? 64 : 0) : 64 * part;
+    const __amdgpu_buffer_rsrc_t rsr = __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, -1, 0x00020000);
 #pragma unroll
     for (int k = AP * q; k < AP * q + AP; ++k) {
       const int rs = 8 * k + (lane >> 3);                // row inside the 64-row part
-      int row = m0 + 64 * part + rs;
+      int row = m0 + r0 + rs;
       row = row < M ? row : M - 1;                       // rows past M are never stored
       const uint32_t col = (uint32_t)(n0 + 64 * wave + 8 * ((lane & 7) ^ swz(rs)));
       __builtin_amdgcn_raw_ptr_buffer_load_lds(rsr, (lds_void_t*)(stg + wv * 8192 + k * 1024), 16,
@@ -285,8 +291,8 @@ __device__ __forceinline__ void gemm_tile(const GemmParams& p, uint8_t* st0, uin
     SEER_TILE(kt, st0, st1, st3, bq0, bq1);
     SEER_TILE(kt + 1, st1, st2, st0, bq1, bq0);
   }
-  // the loads past the last tile (clamped re-reads, or the output projection's
-  // residual rows) land before the epilogue
+  // the loads past the last tile (clamped re-reads, or the residual parts)
+  // land before the epilogue
   __builtin_amdgcn_s_waitcnt(waitcnt_imm(0, 15));
 #undef SEER_GLOAD_B
 #undef SEER_FLOAD
@@ -341,15 +347,18 @@ __device__ __forceinline__ void gemm_tile(const GemmParams& p, uint8_t* st0, uin
   auto fetch = [&](int i, u32x4_t* dst) {
     int row = m0 + i * 32 + fr;
     row = row < M ? row : M - 1;             // rows past M are never stored
+    // row 32 (i % 2) + fr of a 64-row residual part in stage st; its swizzle
+    // is that of fr
+    auto lds_words = [&](const uint8_t* st, u32x4_t* w) {
+      const uint8_t* sb = st + wv * 8192 + (32 * (i & 1) + fr) * ROW_BYTES;
+#pragma unroll
+      for (int jt = 0; jt < 4; ++jt) w[jt] = *reinterpret_cast<const u32x4_t*>(sb + (((fhalf + 2 * jt) ^ fsw) << 4));
+    };
     if constexpr (kRes) {
       bool lds = false;
-      if constexpr (kResLds) lds = res_lds && i < 6;
+      if constexpr (kResLds) lds = res_lds && (kPair ? i < 4 : i < 6);
       if (lds) {
-        // row 32 (i % 2) + fr of residual part i / 2 (stage i / 2); its
-        // swizzle is that of fr
-        const uint8_t* sb = (i < 2 ? st0 : i < 4 ? st1 : st2) + wv * 8192 + (32 * (i & 1) + fr) * ROW_BYTES;
-#pragma unroll
-        for (int jt = 0; jt < 4; ++jt) dst[jt] = *reinterpret_cast<const u32x4_t*>(sb + (((fhalf + 2 * jt) ^ fsw) << 4));
+        lds_words(kPair ? (i < 2 ? st0 : st2) : (i < 2 ? st0 : i < 4 ? st1 : st2), dst);
       } else {
         const uint16_t* rb = R + (size_t)row * p.ldr + colw;
 #pragma unroll
@@ -357,9 +366,15 @@ __device__ __forceinline__ void gemm_tile(const GemmParams& p, uint8_t* st0, uin
       }
     }
     if constexpr (kPair) {
-      const uint16_t* rb = static_cast<const uint16_t*>(p.R2) + (size_t)row * p.ldr + colw;
+      bool lds = false;
+      if constexpr (kResLds) lds = res_lds && i < 2;
+      if (lds) {
+        lds_words(st1, dst + 4);
+      } else {
+        const uint16_t* rb = static_cast<const uint16_t*>(p.R2) + (size_t)row * p.ldr + colw;
 #pragma unroll
-      for (int jt = 0; jt < 4; ++jt) dst[4 + jt] = *reinterpret_cast<const u32x4_t*>(rb + 16 * jt);
+        for (int jt = 0; jt < 4; ++jt) dst[4 + jt] = *reinterpret_cast<const u32x4_t*>(rb + 16 * jt);
+      }
     }
   };
   float rsv[NI];
