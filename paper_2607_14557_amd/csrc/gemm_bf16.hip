@@ -30,7 +30,8 @@
 //           the packed weight and are stored back in head order
 //   SCALE_ROPE  as SCALE, and the columns below rope_col1 are rotated
 //           (rotary embedding of q and k) on the way
-//   RESID   C = bf16(R[r,c] + acc)              residual add
+//   RESID   C = bf16(R[r,c] + acc)              residual add (the layer uses the
+//           two forms below; this one is not launched by the bf16 path)
 //   RESID_SPLIT v = R[r,c] + acc: C = bf16(v) and residual after O: h1 as a bf16
 //               C2 = bf16(v - C)                high/low pair, exact to ~2^-17
 //   RESID_PAIR  C = bf16(R + R2 + acc)          residual after down from that pair
@@ -830,7 +831,6 @@ int launch_gemm_bf16(int epi, const GemmParams& p_in, hipStream_t s) {
   } else switch (epi) {
     case EPI_SCALE: hipLaunchKernelGGL(gemm_bf16_kernel<EPI_SCALE>, grid, block, 0, s, p); break;
     case EPI_SCALE_ROPE: hipLaunchKernelGGL(gemm_bf16_kernel<EPI_SCALE_ROPE>, grid, block, 0, s, p); break;
-    case EPI_RESID: hipLaunchKernelGGL(gemm_bf16_kernel<EPI_RESID>, grid, block, 0, s, p); break;
     case EPI_SWIGLU: hipLaunchKernelGGL(gemm_bf16_kernel<EPI_SWIGLU>, grid, block, 0, s, p); break;
     case EPI_SWIGLU_COUNT:
       hipLaunchKernelGGL(gemm_bf16_kernel<EPI_SWIGLU_COUNT>, grid, block, 0, s, p); break;
