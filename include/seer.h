@@ -231,7 +231,10 @@ int seer_layer_forward_varlen_noalloc(const seer_dims* dims, const void* w_packe
  *   events[4] -> [5] RMS statistics of h1 (+ zeroing act_count)
  *   events[5] -> [6] gate/up GEMM + SwiGLU (+ count)
  *   events[6] -> [7] down GEMM + residual
- * Errors: as seer_layer_forward_varlen, EINVAL if events or an entry is NULL. */
+ * A NULL entry is skipped (that point is not recorded): each record delays
+ * the next launch by a few microseconds, so a caller timing one kernel
+ * passes only the two events around it.
+ * Errors: as seer_layer_forward_varlen, EINVAL if events is NULL. */
 int seer_layer_forward_varlen_timed(const seer_dims* dims, const void* w_packed,
                                     const void* x_in, void* x_out, int32_t total_rows_ub,
                                     const int32_t* cu_seqlens, const int32_t* seqused,
@@ -333,7 +336,8 @@ int seer_layer_forward_detect(const seer_dims* dims, const void* w_packed, const
  * seer_layer_forward_varlen_timed, then
  *   events[6] -> [7] SNR scan + list of kept row tiles
  *   events[7] -> [8] down GEMM + residual (kept tiles)
- * Errors: as seer_layer_forward_detect, EINVAL if events or an entry is NULL. */
+ * NULL entries are skipped, as there.
+ * Errors: as seer_layer_forward_detect, EINVAL if events is NULL. */
 int seer_layer_forward_detect_timed(const seer_dims* dims, const void* w_packed, const void* x_in,
                                     void* x_out, int32_t total_rows_ub, const int32_t* cu_seqlens,
                                     int32_t batch, float act_eps, int32_t* act_count,

@@ -242,7 +242,10 @@ static int layer_forward_impl(const seer_dims* dims, const void* w_packed, const
   const uint8_t* wb = static_cast<const uint8_t*>(w_packed);
   auto gemm = bf16 ? seer::launch_gemm_bf16 : seer::launch_gemm_f32;
 
-  auto mark = [&](int k) { return ev ? hipEventRecord(ev[k], stream) : hipSuccess; };
+  // a NULL entry skips that mark: each record on the stream delays the next
+  // launch by a few microseconds, so a caller timing one kernel passes only
+  // the two events around it
+  auto mark = [&](int k) { return ev && ev[k] ? hipEventRecord(ev[k], stream) : hipSuccess; };
   if (mark(0) != hipSuccess) return hip_fail("event record");
   // 1. RMSNorm statistics of the layer input (+ rotary positions)
   {
@@ -392,8 +395,6 @@ int seer_layer_forward_detect_timed(const seer_dims* dims, const void* w_packed,
                                     int32_t* keep_len, void* workspace, size_t workspace_bytes,
                                     hipStream_t stream, hipEvent_t* events) {
   if (!events) return fail(SEER_EINVAL, "events is NULL");
-  for (int k = 0; k < 9; ++k)
-    if (!events[k]) return fail(SEER_EINVAL, "events[%d] is NULL", k);
   return layer_detect_impl(dims, w_packed, x_in, x_out, total_rows_ub, cu_seqlens, batch, act_eps, act_count,
                            win_off, win_len, params, boundary, keep_len, workspace, workspace_bytes, stream,
                            events);
@@ -467,8 +468,6 @@ int seer_layer_forward_varlen_timed(const seer_dims* dims, const void* w_packed,
                                     int32_t* act_count, void* workspace, size_t workspace_bytes,
                                     hipStream_t stream, hipEvent_t* events) {
   if (!events) return fail(SEER_EINVAL, "events is NULL");
-  for (int k = 0; k < 8; ++k)
-    if (!events[k]) return fail(SEER_EINVAL, "events[%d] is NULL", k);
   return layer_forward_impl(dims, w_packed, x_in, x_out, total_rows_ub, cu_seqlens, seqused, batch,
                             act_eps, act_count, workspace, workspace_bytes, stream, events);
 }

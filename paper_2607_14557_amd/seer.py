@@ -224,7 +224,8 @@ def seer_layer_forward_varlen(dims, w_packed, x_in, x_out, total_rows_ub, cu_seq
 def seer_layer_forward_varlen_timed(dims, w_packed, x_in, x_out, total_rows_ub, cu_seqlens,
                                     seqused, batch, act_eps, act_count, workspace, events,
                                     workspace_bytes=None, stream=None):
-    """events: sequence of 8 raw hipEvent_t handles (ints)."""
+    """events: sequence of 8 raw hipEvent_t handles (ints); a None entry
+    skips that point."""
     nbytes = workspace_bytes if workspace_bytes is not None else workspace.numel() * workspace.element_size()
     ev = (_P * 8)(*events)
     _check(load_library().seer_layer_forward_varlen_timed(

@@ -103,10 +103,14 @@ def test_layer_forward_argument_errors(S):
     assert call_layer(S, dims(S, dh=64)) == S.SEER_EINVAL              # 32 x 64 != 4096
     assert call_layer(S, dims(S, h=64, dh=64)) == S.SEER_EUNSUPPORTED  # bf16 needs head_dim 128
     L = S.load_library()
-    ev = (ctypes.c_void_p * 8)(*([FAKE] * 7 + [None]))
     rc = L.seer_layer_forward_varlen_timed(ctypes.byref(d), FAKE, FAKE, FAKE + 4096, 100, FAKE, None,
-                                           1, 0.0, None, FAKE, 1 << 40, 0, ev)
-    assert rc == S.SEER_EINVAL and "events[7]" in S.seer_last_error()
+                                           1, 0.0, None, FAKE, 1 << 40, 0, None)
+    assert rc == S.SEER_EINVAL and "events" in S.seer_last_error()
+    # NULL entries are skipped, not rejected: the call goes on to the next check
+    ev = (ctypes.c_void_p * 8)(*([None] * 5 + [FAKE, FAKE, None]))
+    rc = L.seer_layer_forward_varlen_timed(ctypes.byref(d), FAKE, FAKE, FAKE + 4096, 100, FAKE, None,
+                                           0, 0.0, None, FAKE, 1 << 40, 0, ev)
+    assert rc == S.SEER_EINVAL and "batch" in S.seer_last_error()
 
 
 def test_detect_argument_errors(S):
@@ -148,7 +152,7 @@ def test_detection_layer_argument_errors(S):
     assert call(eps=-1.0) == S.SEER_EINVAL
     assert call(ws_bytes=S.seer_layer_workspace_bytes(d, 100) - 1) == S.SEER_EWORKSPACE
     ev = (ctypes.c_void_p * 9)(*([FAKE] * 8 + [None]))
-    assert call(events=ev) == S.SEER_EINVAL and "events[8]" in S.seer_last_error()
+    assert call(events=ev, batch=0) == S.SEER_EINVAL and "batch" in S.seer_last_error()   # NULL entry skipped
 
 
 def test_repack_argument_errors(S):
