@@ -366,6 +366,44 @@ def test_layer_deterministic(S):
     np.testing.assert_array_equal(host(c1), host(c2))
 
 
+def test_timed_layer_with_one_kernel_timed(S):
+    """The timed entry point with only the two events around the gate/up GEMM
+    set (the others NULL, skipped): the output is bit-identical to the untimed
+    call, and the two recorded events bound a positive kernel time."""
+    import ctypes
+    import torch
+    hip = ctypes.CDLL("libamdhip64.so.7")
+    hip.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+    hip.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p, ctypes.c_void_p]
+    hip.hipEventDestroy.argtypes = [ctypes.c_void_p]
+    d, H, dh, I = 512, 4, 128, 1024
+    rng = np.random.default_rng(19)
+    W = _round(_rand_layer(rng, d, I, 0.02), "bf16")
+    lens = [300, 1, 517]
+    cu = np.concatenate([[0], np.cumsum(lens)])
+    T = int(cu[-1])
+    x = dev(rng.standard_normal((T, d)), "bf16")
+    L = _Layer(S, d, H, dh, I, "bf16", T, W)
+    log("timed layer, gate/up events only")
+    y_ref, _ = L.run(x, dev(cu), len(lens))
+    ev = []
+    for _ in range(2):
+        e = ctypes.c_void_p()
+        assert hip.hipEventCreate(ctypes.byref(e)) == 0
+        ev.append(e.value)
+    y = torch.zeros_like(x)
+    S.seer_layer_forward_varlen_timed(L.dims, L.packed, x, y, T, dev(cu), None, len(lens), 0.0, None, L.ws,
+                                      [None] * 5 + ev + [None])
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(host(y), host(y_ref))
+    ms = ctypes.c_float()
+    assert hip.hipEventElapsedTime(ctypes.byref(ms), ev[0], ev[1]) == 0
+    log("  gate/up GEMM %.4f ms" % ms.value)
+    assert ms.value > 0.0
+    for e in ev:
+        hip.hipEventDestroy(e)
+
+
 def test_layer_batch_permutation_bitwise(S):
     """Reordering the sequences of a packed batch reorders the results and
     changes nothing else, bit for bit: every row's projections, its
