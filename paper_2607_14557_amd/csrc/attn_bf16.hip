@@ -270,8 +270,9 @@ __global__ __launch_bounds__(NT, 2) void attn_bf16_kernel(AttnParams p) {
       for (int i = 0; i < 2; ++i)
 #pragma unroll
         for (int r = 0; r < 16; ++r) mt = fmaxf(mt, s[i][r]);
-      // lanes l and l ^ 32 hold the two 32-key halves of one query's column:
-      // a register swap across the halves, no LDS round trip
+      // lanes l and l ^ 32 each hold 32 of the tile's 64 keys of one query's
+      // column (alternate groups of four): a register swap across the pair,
+      // no LDS round trip
       const u32x2_t sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mt), __float_as_uint(mt), false, false);
       mt = fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1]));
       const float m_new = fmaxf(m_run, mt);
